@@ -1,0 +1,206 @@
+"""Benchmark of the KDA decode step with a 4-bit-mean mixed-precision state.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode]
+
+One step = one kda_step call: a decode token for B x H heads with its
+write-back (recurrence, outputs, weights, layer-budget allocation, fitted
+quantiser, packing).  Workload "decode": B=64 sequences, H=32 heads,
+d_k=d_v=128, mean payload 4 bits, widths in [2, 8], normalisation groups of
+64 rows, prior state = the oracle's quantised record after 512 unquantised
+warm-up tokens.  Steps rotate over L independent layer records (copies of the
+prior state) so the working set exceeds the 256 MB last-level cache.  Inputs
+are resident in HBM before the timed region.
+
+Prints one JSON line (see the fields below).  The oracle leg ("cpu_baseline")
+times the CPU oracle on one sequence of the same workload.
+"""
+import argparse
+import json
+import multiprocessing as mp
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz: one VALU lane-op per lane per clock
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# lane-ops per state element of the requantisation kernel:
+# 16 fit candidates x 5 (scale, round, clamp, residual fma, square fma)
+# + unpack 4 + recurrence 3 + final codes and packing 5
+REQUANT_OPS_PER_ELEMENT = 16 * 5 + 4 + 3 + 5
+
+
+def _warm_chunk(args):
+    name, b0, b1, T = args
+    from oracle import step
+    w = W.WORKLOADS[name]
+    base = W.base_rates(w)
+    xs = {n: [] for n in ("q", "k", "v", "s", "beta")}
+    for t in range(T):
+        x = W.token(w, t, base=base)
+        for n in xs:
+            xs[n].append(x[n][b0:b1])
+    xs = {n: np.stack(a, axis=1) for n, a in xs.items()}
+    wc = W.sized(w, B=b1 - b0)
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
+    st, _ = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
+    from tests._gpu import state_to_bytes
+    return b0, state_to_bytes(st, wc.dk, wc.dv, wc.b_max), st
+
+
+def prior_state(name, T, procs):
+    """Oracle prior records for all sequences (parallel over sequence chunks)."""
+    w = W.WORKLOADS[name]
+    chunk = max(1, w.B // procs)
+    jobs = [(name, b0, min(w.B, b0 + chunk), T) for b0 in range(0, w.B, chunk)]
+    ctx = mp.get_context("fork")
+    with ctx.Pool(min(procs, len(jobs))) as pool:
+        parts = pool.map(_warm_chunk, jobs)
+    parts.sort(key=lambda p: p[0])
+    recs = np.concatenate([p[1] for p in parts])
+    st0 = parts[0][2]
+    return recs, st0
+
+
+def cpu_baseline(name, st0, t_tok, budget_s=12.0):
+    """Oracle decode steps on one sequence (all its heads) until budget_s."""
+    from oracle import step
+    w = W.WORKLOADS[name]
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
+    st = {k: v[:1] for k, v in st0.items()}
+    base = W.base_rates(w)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        x = W.token(w, t_tok + n, base=base)
+        x = {k: v[:1] for k, v in x.items()}
+        st, _, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return dict(value=w.H * n / el, unit="state-tokens/s", cores=1, kind="oracle",
+                sample=f"{n} decode steps of 1 of {w.B} sequences ({w.H} heads, "
+                       f"{w.dk}x{w.dv} states), float32-contract oracle, one thread")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="decode", choices=["decode"])
+    ap.add_argument("--layers", type=int, default=20)
+    ap.add_argument("--warm-tokens", type=int, default=512)
+    ap.add_argument("--procs", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(sequences shard across GPUs without communication; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    w = W.WORKLOADS[args.workload]
+    t0 = time.time()
+    recs_host, st0 = prior_state(args.workload, args.warm_tokens, args.procs)
+    print(f"# prior state from {args.warm_tokens} oracle warm-up tokens in "
+          f"{time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    import torch
+    import paper_2609_30950_amd as K
+
+    torch.cuda.set_device(0)
+    cfg = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                   b_min=w.b_min, b_max=w.b_max)
+    slot = K.record_bytes(cfg)
+    assert recs_host.size == w.B * w.H * slot
+    L = args.layers
+    layers = torch.from_numpy(recs_host).cuda().repeat(L).view(L, -1)
+    ws = K.new_workspace(cfg)
+    o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    n_tok = args.warmup + args.steps
+    base = W.base_rates(w)
+    toks = [W.token(w, args.warm_tokens + t, base=base) for t in range(n_tok)]
+    dtoks = [{n: torch.from_numpy(a).cuda() for n, a in x.items()} for x in toks]
+
+    def run(i):
+        x = dtoks[i]
+        K.kda_step(cfg, layers[i % L], x["q"], x["k"], x["v"], x["s"], x["beta"], o, ws)
+
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+    K.kda_profile_enable(True)
+    K.kda_profile_read()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for i in range(args.warmup, n_tok):
+        run(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    prof = K.kda_profile_read()
+    K.kda_profile_enable(False)
+    ms = ev0.elapsed_time(ev1) / args.steps
+
+    kern = {k: dict(ms_avg=v[0] / v[1], launches=v[1]) for k, v in prof.items()}
+    dom = max(prof, key=lambda k: prof[k][0])
+    elems = w.B * w.H * w.dk * w.dv
+    # algorithmic HBM bytes of one step: records read and written (metadata
+    # plus the budgeted code bits), inputs q, k, v, s, beta and outputs o
+    meta = 16 + w.dk // 2 + 6 * w.dk
+    code_bytes = w.mean_bits * elems / 8
+    io = w.B * w.H * (4 * (w.dk * 3 + w.dv) + 4)
+    step_bytes = 2 * (w.B * w.H * meta + code_bytes) + io
+    hbm = step_bytes / (ms * 1e-3) / 1e9
+    if dom == "requant":
+        t_dom = kern[dom]["ms_avg"] * 1e-3
+        achieved = REQUANT_OPS_PER_ELEMENT * elems / t_dom / 1e12
+        roof = dict(bound="alu", achieved=achieved, peak=VALU_PEAK_TOPS, unit="TOP/s",
+                    frac=achieved / VALU_PEAK_TOPS, traffic=None, kernel="requant",
+                    ops_per_element=REQUANT_OPS_PER_ELEMENT)
+    else:
+        t_dom = kern[dom]["ms_avg"] * 1e-3
+        roof = dict(bound="hbm", achieved=step_bytes / t_dom / 1e9, peak=HBM_PEAK_GBPS,
+                    unit="GB/s", frac=step_bytes / t_dom / 1e9 / HBM_PEAK_GBPS, traffic=None,
+                    kernel=dom)
+
+    out = {
+        "metric": "state-tokens/s (B·H·T) and achieved HBM GB/s, KDA step w/ 4-bit mixed state",
+        "value": w.B * w.H / (ms * 1e-3),
+        "unit": "state-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"decode step B={w.B} H={w.H} d_k=d_v={w.dk}, mean {w.mean_bits} "
+                               f"bits, widths [{w.b_min},{w.b_max}], groups of {w.G} rows, layer "
+                               f"budget, prior state after {args.warm_tokens} warm-up tokens",
+                   "layers_rotated": L},
+        "hbm_GBps_step": hbm,
+        "hbm_frac_step": hbm / HBM_PEAK_GBPS,
+        "bytes_per_step": step_bytes,
+        "kernels": kern,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, st0, args.warm_tokens)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

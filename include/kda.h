@@ -1,0 +1,174 @@
+/*
+ * kda.h — C ABI of libkda: the Kimi Delta Attention (KDA) recurrence with a
+ * decay-aware mixed-precision recurrent state, for AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Low-Bit Recurrent States in Hybrid Language Models"
+ * (arxiv 2609.30950).  Per head, the state S (d_k x d_v, rows = key channels)
+ * follows the gated delta rule (Sec. 2, eq. rule) with the KDA choice of erase
+ * and write vectors:
+ *
+ *     S_t = (I - beta_t k_t k_t^T) diag(exp(-s_t)) S_{t-1} + beta_t k_t v_t^T,
+ *     o_t = S_t^T q_t,
+ *
+ * and is written back every C tokens as Deq(Q(S)) (Sec. 2, Accumulated
+ * readout error; Sec. 5, Protocol): outputs are read before quantisation and no
+ * unquantised residual is kept.  Q is the paper's quantiser (Sec. 3):
+ * per-row widths from the high-rate allocation rule (eq. alloc) on weights
+ * c_i = Gamma_i * R~_i^2 (eq. weight), symmetric levels with a clip factor
+ * fitted over 16 values and stored as an FP16 scale, variable-width rows
+ * addressed by prefix sums of widths, and log-uniform codes of the decay rate.
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ * - All array arguments are DEVICE pointers (HIP device memory) unless stated;
+ *   the config is a host pointer.  Arrays are dense, C-contiguous, in the
+ *   layout given per argument; the caller owns every buffer.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Every call only enqueues work on `stream`: it never synchronises, never
+ *   allocates device memory and never prints.
+ * - Arguments are validated before anything is enqueued; on any error nothing
+ *   is launched and a kda_status other than KDA_OK is returned.  A failed
+ *   kernel launch returns KDA_ERR_HIP.  NaN/Inf in inputs are not checked.
+ * - Records: one fixed-size slot of kda_record_bytes() per (sequence, head),
+ *   slots ordered [B][H].  A zero-filled slot is the zero state (fresh EMA).
+ *   kda_step / kda_prefill update records in place.
+ * - Workspace: kda_workspace_bytes() bytes, 256-byte aligned, ZERO-FILLED by
+ *   the caller before its first use; calls leave its counters at zero again.
+ *   Concurrent calls must not share a workspace.
+ */
+#ifndef KDA_H_
+#define KDA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KDA_OK = 0,
+  KDA_ERR_ARG = 1,          /* bad pointer, size or numeric parameter        */
+  KDA_ERR_SHAPE = 2,        /* unsupported or inconsistent shape             */
+  KDA_ERR_UNSUPPORTED = 3,  /* valid request this build does not implement   */
+  KDA_ERR_WORKSPACE = 4,    /* workspace pointer missing                     */
+  KDA_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed    */
+} kda_status;
+
+enum { KDA_SCOPE_SEQUENCE = 0, KDA_SCOPE_HEAD = 1 };
+
+/* Problem and quantiser configuration (host memory, plain old data). */
+typedef struct {
+  int32_t B;              /* sequences                                        */
+  int32_t H;              /* heads per layer                                  */
+  int32_t d_k;            /* rows (key channels): 64 or 128                   */
+  int32_t d_v;            /* columns (value channels): equal to d_k           */
+  int32_t group_rows;     /* G: rows per output-normalisation group (Sec. 2,
+                             Range normalization); divides d_k                */
+  int32_t scope;          /* allocation scope: KDA_SCOPE_SEQUENCE = all H*d_k
+                             rows of a sequence share the budget (the paper's
+                             layer budget, Sec. 3); KDA_SCOPE_HEAD = per head */
+  double mean_bits;       /* mean payload bits per element, in [b_min, b_max] */
+  int32_t b_min, b_max;   /* width clamp, 1 <= b_min <= b_max <= 16 (Sec. 3)  */
+  int32_t ema_span;       /* EMA span in tokens (Sec. 3: 64); 1 = one-token   */
+  int32_t decay_per_head; /* 0: s is per row [.., H, d_k]; 1: one rate per
+                             head [.., H] (Gated DeltaNet style, Sec. 1)      */
+  int32_t state32;        /* 1: unquantised float32 state ("32-bit mode")     */
+} kda_config;
+
+/* Bytes of one (sequence, head) record slot; 0 if the config is invalid.
+ * Quantised layout (little endian):
+ *   u32 tokens seen; u32 reserved[3];
+ *   widths: d_k 4-bit fields (b - 1), row i in byte i/2, low nibble if i even;
+ *   scale FP16 [d_k]; rate code u16 [d_k]; erase rate FP16 [d_k];
+ *   at the next multiple of 256: code words u32 [ceil(d_k*b_max/32)][d_v];
+ *   column j is a bit stream of the rows' b_i-bit two's complement codes in
+ *   row order, least significant bit first, so row i starts at bit
+ *   sum_{i'<i} b_i' (prefix sums of widths, Sec. 3); bit p of column j is bit
+ *   p%32 of word [p/32][j].  One-bit rows store 1 for a negative value and
+ *   scale = mean |x|.
+ * 32-bit mode: the float32 state, row-major [d_k][d_v]. */
+size_t kda_record_bytes(const kda_config* cfg);
+
+/* Bytes of workspace kda_step / kda_prefill / kda_alloc_bits need. */
+size_t kda_workspace_bytes(const kda_config* cfg);
+
+/* Static description of a status code. */
+const char* kda_status_str(int status);
+
+/* Windowed observability-Gramian row weights (Prop. 1, eq. gram, with the
+ * diagonal erase approximation of Sec. 2, Approximate erasure rate):
+ *   lambda_t,i = exp(-2 s_t,i - beta_t (2 - beta_t) k_t,i^2),
+ *   A_0 = 0, A_t = lambda_t (chi_{t-1} + A_{t-1}),
+ *   gamma_i = (1/W) sum_{t=1}^{W-1} q_t,i^2 A_t,i,
+ * chi_tau = 1 when a write-back follows token tau ((tau+1) % C == 0).
+ * In:  q, k [B][W][H][d_k] f32; s [B][W][H][d_k] f32 (or [B][W][H] with
+ *      decay_per_head); beta [B][W][H] f32.  W >= 1, C >= 1.
+ * Out: gamma [B][H][d_k] f64. */
+int kda_weights(const kda_config* cfg, int32_t W, int32_t C, const float* q,
+                const float* s, const float* beta, const float* k,
+                double* gamma, void* stream);
+
+/* Bit allocation (Sec. 3, eq. weight and eq. alloc, rounded, clipped and
+ * adjusted to the budget): R~ = R / RMS_group(R), c = gamma * R~^2, widths
+ * minimising sum c_i 2^(-2 b_i) with sum b_i = floor(mean_bits*N + 0.5) over
+ * each scope unit of N rows; ties to the lower row index.
+ * In:  gamma [B][H][d_k] f64 (>= 0); R [B][H][d_k] f32 row absolute maxima.
+ * Out: bits [B][H][d_k] u8.  ws: workspace (only its counters are used). */
+int kda_alloc_bits(const kda_config* cfg, const double* gamma, const float* R,
+                   uint8_t* bits, void* ws, void* stream);
+
+/* Quantise and pack states (Sec. 3, Levels and storage).
+ * In:  S [B][H][d_k][d_v] f32; bits [B][H][d_k] u8 in [b_min, b_max];
+ *      s_hat [B][H][d_k] f64 decay rates (stored as 16-bit log-uniform codes,
+ *      Sec. 3, Decay-gate quantization); r [B][H][d_k] f64 erase rates
+ *      (stored as FP16); tokens_seen is written to every slot header.
+ * Out: records, B*H slots.  Not available in 32-bit mode. */
+int kda_pack_state(const kda_config* cfg, const float* S, const uint8_t* bits,
+                   const double* s_hat, const double* r, uint32_t tokens_seen,
+                   void* records, void* stream);
+
+/* Decode records.  Out (each may be NULL): S [B][H][d_k][d_v] f32
+ * dequantised state; bits [B][H][d_k] u8; s_hat [B][H][d_k] f64 decoded
+ * rates; r [B][H][d_k] f64 decoded erase rates.  In 32-bit mode only S. */
+int kda_unpack_state(const kda_config* cfg, const void* records, float* S,
+                     uint8_t* bits, double* s_hat, double* r, void* stream);
+
+/* One decode token for B x H heads with a write-back (C = 1).
+ * In:  q, k [B][H][d_k] f32 (k unit norm); v [B][H][d_v] f32;
+ *      s [B][H][d_k] f32 (or [B][H] with decay_per_head), s > 0;
+ *      beta [B][H] f32; gamma: NULL to weight rows by the EMA estimate of
+ *      eq. weight, else [B][H][d_k] f64 weights (e.g. from kda_weights).
+ * In/out: records.  Out: o [B][H][d_v] f32, read before quantisation. */
+int kda_step(const kda_config* cfg, void* records, const float* q,
+             const float* k, const float* v, const float* s, const float* beta,
+             const double* gamma, float* o, void* ws, void* stream);
+
+/* Prefill of T tokens with a write-back after every C-th token and after the
+ * last one (Sec. 2: once per prefill chunk).
+ * In:  q, k [B][T][H][d_k] bf16 (raw 16-bit patterns); v [B][T][H][d_v] bf16;
+ *      s [B][T][H][d_k] f32 (or [B][T][H]); beta [B][T][H] f32; gamma as in
+ *      kda_step.  In/out: records.  Out: o [B][T][H][d_v] f32. */
+int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records,
+                const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                const float* s, const float* beta, const double* gamma,
+                float* o, void* ws, void* stream);
+
+/* Diagnostics: per-kernel timing.  While enabled (on != 0), every kernel a
+ * call enqueues is bracketed by two hipEvents recorded on the call's stream
+ * (host-side runtime objects from a reusable pool; no device memory).  Not
+ * thread safe; meant for single-threaded benchmark drivers. */
+int kda_profile_enable(int on);
+
+/* Wait for the last recorded event, then report per kernel kind (static
+ * strings such as "stats", "alloc", "requant") the summed milliseconds and
+ * launch counts since the previous read, and forget them.  Host pointers;
+ * kinds/ms/counts hold up to max_kinds entries (each may be NULL);
+ * *n_kinds receives the number of kinds seen. */
+int kda_profile_read(int max_kinds, const char** kinds, double* ms, int* counts,
+                     int* n_kinds);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KDA_H_ */

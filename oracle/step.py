@@ -151,3 +151,27 @@ def mirror_prefill(state, q, k, v, s, beta, C, cfg, gamma=None):
 def truth_outputs(X, q, k, v, s, beta):
     """float64 outputs of one token from the float32 state X (no quantisation)."""
     return recurrence.truth_step_rowform(X, q, k, v, s, beta)[1]
+
+
+def warm_state(q, k, v, s, beta, cfg):
+    """Quantised record after an unquantised warm-up from the zero state.
+
+    q, k: [B,T,H,dk]; v: [B,T,H,dv]; s: [B,T,H,dk|1]; beta: [B,T,H].  The
+    float64 recurrence (eq. rule) and the token-sequential EMAs run over all
+    T tokens; the state is then written back once (quantised with the
+    allocation of that moment).  Returns (state, float64 state before the
+    write-back).
+    """
+    B, T, H, _ = np.asarray(q).shape
+    S = np.zeros((B, H, cfg.dk, cfg.dv), F64)
+    m = e = None
+    for t in range(T):
+        S, _ = recurrence.truth_step_rowform(S, q[:, t], k[:, t], v[:, t], s[:, t], beta[:, t])
+        sr = _rows(s[:, t], cfg.dk)
+        bt = np.asarray(beta[:, t])[..., None]
+        if m is None:
+            m, e = stats.ema_init(sr, k[:, t], bt)
+        else:
+            m, e = stats.ema_update(m, e, sr, k[:, t], bt, cfg.span)
+    st, _ = write_back(S.astype(F32), m, e, np.full((B, H), T, np.int64), cfg)
+    return st, S

@@ -1,0 +1,203 @@
+// C ABI of libkda: argument validation, workspace layout and launches.
+// Declarations and argument contracts: include/kda.h.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+
+#include "../../include/kda.h"
+#include "kda_kernels.hpp"
+
+namespace {
+
+using kda::KParams;
+
+struct WsLayout {
+  size_t c_off, zr_off, bits_off, s32_off, total;
+};
+
+size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+WsLayout ws_layout(const kda_config* cfg) {
+  const size_t rows = (size_t)cfg->B * cfg->H * cfg->d_k;
+  WsLayout w;
+  w.c_off = 0;
+  w.zr_off = up256(w.c_off + rows * sizeof(double));
+  w.bits_off = up256(w.zr_off + rows * sizeof(uint32_t));
+  w.s32_off = up256(w.bits_off + rows);
+  w.total = up256(w.s32_off + rows * (size_t)cfg->d_v * sizeof(float));
+  return w;
+}
+
+// Validate a config; fills the budget of one scope unit.
+int check_cfg(const kda_config* cfg, int* need) {
+  if (cfg == nullptr) return KDA_ERR_ARG;
+  if (cfg->B < 1 || cfg->H < 1) return KDA_ERR_SHAPE;
+  if (cfg->d_k != cfg->d_v) return KDA_ERR_UNSUPPORTED;
+  if (cfg->d_k != 64 && cfg->d_k != 128) return KDA_ERR_UNSUPPORTED;
+  if (cfg->decay_per_head != 0 && cfg->decay_per_head != 1) return KDA_ERR_ARG;
+  if (cfg->state32 != 0 && cfg->state32 != 1) return KDA_ERR_ARG;
+  if (cfg->state32) {
+    if (need) *need = 0;
+    return KDA_OK;
+  }
+  if (cfg->group_rows < 1 || cfg->d_k % cfg->group_rows != 0) return KDA_ERR_ARG;
+  if (cfg->scope != KDA_SCOPE_SEQUENCE && cfg->scope != KDA_SCOPE_HEAD) return KDA_ERR_ARG;
+  if (cfg->b_min < 1 || cfg->b_max < cfg->b_min || cfg->b_max > 16) return KDA_ERR_ARG;
+  if (cfg->ema_span < 1) return KDA_ERR_ARG;
+  if (!std::isfinite(cfg->mean_bits)) return KDA_ERR_ARG;
+  const long long N = cfg->scope == KDA_SCOPE_SEQUENCE ? (long long)cfg->H * cfg->d_k : cfg->d_k;
+  if (N > 4096) return KDA_ERR_UNSUPPORTED;
+  const long long K = (long long)std::floor(cfg->mean_bits * (double)N + 0.5);
+  if (K < N * cfg->b_min || K > N * cfg->b_max) return KDA_ERR_ARG;
+  if (need) *need = (int)(K - N * cfg->b_min);
+  return KDA_OK;
+}
+
+KParams make_params(const kda_config* cfg, int need) {
+  KParams p;
+  std::memset(&p, 0, sizeof(p));
+  p.B = cfg->B;
+  p.H = cfg->H;
+  p.dk = cfg->d_k;
+  p.dv = cfg->d_v;
+  p.G = cfg->group_rows;
+  p.scope = cfg->scope;
+  p.bmin = cfg->b_min;
+  p.bmax = cfg->b_max;
+  p.per_head = cfg->decay_per_head;
+  p.state32 = cfg->state32;
+  p.need = need;
+  p.alpha = 2.0 / (double)(cfg->ema_span + 1);
+  p.one_minus_alpha = 1.0 - p.alpha;
+  p.L = kda::make_layout(cfg->d_k, cfg->d_v, cfg->b_max < 1 ? 1 : cfg->b_max);
+  for (int b = 0; b <= kda::MAX_B; ++b)
+    for (int m = 0; m < kda::N_FIT; ++m) {
+      const int n = b >= 2 ? (1 << (b - 1)) - 1 : 0;
+      p.phi[b][m] = n > 0 ? (float)((double)(5 + m) / (double)(20 * n)) : 0.f;
+    }
+  return p;
+}
+
+void set_ws(KParams& p, const kda_config* cfg, void* ws) {
+  const WsLayout w = ws_layout(cfg);
+  uint8_t* base = (uint8_t*)ws;
+  p.ws_c = (double*)(base + w.c_off);
+  p.ws_zr = (uint32_t*)(base + w.zr_off);
+  p.ws_bits = base + w.bits_off;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? KDA_OK : KDA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+size_t kda_record_bytes(const kda_config* cfg) {
+  if (check_cfg(cfg, nullptr) != KDA_OK) return 0;
+  if (cfg->state32) return (size_t)cfg->d_k * cfg->d_v * sizeof(float);
+  return (size_t)kda::make_layout(cfg->d_k, cfg->d_v, cfg->b_max).slot;
+}
+
+size_t kda_workspace_bytes(const kda_config* cfg) {
+  if (check_cfg(cfg, nullptr) != KDA_OK) return 0;
+  return ws_layout(cfg).total;
+}
+
+const char* kda_status_str(int status) {
+  switch (status) {
+    case KDA_OK: return "ok";
+    case KDA_ERR_ARG: return "invalid argument";
+    case KDA_ERR_SHAPE: return "invalid shape";
+    case KDA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case KDA_ERR_WORKSPACE: return "workspace missing";
+    case KDA_ERR_HIP: return "HIP launch or runtime error";
+    default: return "unknown status";
+  }
+}
+
+int kda_weights(const kda_config* cfg, int32_t W, int32_t C, const float* q, const float* s,
+                const float* beta, const float* k, double* gamma, void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (W < 1 || C < 1) return KDA_ERR_ARG;
+  if (!q || !s || !beta || !k || !gamma) return KDA_ERR_ARG;
+  KParams p = make_params(cfg, need);
+  return hip_status(kda::launch_window_gamma(p, W, C, q, s, beta, k, gamma, (hipStream_t)stream));
+}
+
+int kda_alloc_bits(const kda_config* cfg, const double* gamma, const float* R, uint8_t* bits,
+                   void* ws, void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (cfg->state32) return KDA_ERR_ARG;
+  if (!gamma || !R || !bits) return KDA_ERR_ARG;
+  if (!ws) return KDA_ERR_WORKSPACE;
+  KParams p = make_params(cfg, need);
+  set_ws(p, cfg, ws);
+  return hip_status(kda::launch_alloc_bits(p, gamma, R, bits, (hipStream_t)stream));
+}
+
+int kda_pack_state(const kda_config* cfg, const float* S, const uint8_t* bits, const double* s_hat,
+                   const double* r, uint32_t tokens_seen, void* records, void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (cfg->state32) return KDA_ERR_ARG;
+  if (!S || !bits || !s_hat || !r || !records) return KDA_ERR_ARG;
+  KParams p = make_params(cfg, need);
+  p.records = records;
+  return hip_status(kda::launch_pack(p, S, bits, s_hat, r, tokens_seen, (hipStream_t)stream));
+}
+
+int kda_unpack_state(const kda_config* cfg, const void* records, float* S, uint8_t* bits,
+                     double* s_hat, double* r, void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (!records) return KDA_ERR_ARG;
+  if (cfg->state32 && (bits || s_hat || r)) return KDA_ERR_ARG;
+  KParams p = make_params(cfg, need);
+  p.records = const_cast<void*>(records);
+  return hip_status(kda::launch_unpack(p, S, bits, s_hat, r, (hipStream_t)stream));
+}
+
+int kda_step(const kda_config* cfg, void* records, const float* q, const float* k, const float* v,
+             const float* s, const float* beta, const double* gamma, float* o, void* ws,
+             void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (!records || !q || !k || !v || !s || !beta || !o) return KDA_ERR_ARG;
+  if (!cfg->state32 && !ws) return KDA_ERR_WORKSPACE;
+  KParams p = make_params(cfg, need);
+  p.records = records;
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.s = s;
+  p.beta = beta;
+  p.gamma = gamma;
+  p.o = o;
+  if (!cfg->state32) set_ws(p, cfg, ws);
+  return hip_status(kda::launch_step(p, (hipStream_t)stream));
+}
+
+int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, const uint16_t* q,
+                const uint16_t* k, const uint16_t* v, const float* s, const float* beta,
+                const double* gamma, float* o, void* ws, void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (T < 1 || C < 1) return KDA_ERR_ARG;
+  if (!records || !q || !k || !v || !s || !beta || !o) return KDA_ERR_ARG;
+  if (!ws) return KDA_ERR_WORKSPACE;
+  (void)gamma;
+  (void)stream;
+  return KDA_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

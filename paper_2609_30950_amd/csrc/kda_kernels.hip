@@ -1,0 +1,718 @@
+// HIP kernels of libkda for gfx950 (MI355X), wave64.
+//
+// One workgroup per (sequence, head).  Two thread layouts are used:
+//  * column layout (recurrence, unpack, pack): wave w owns rows
+//    [32w, 32w + 32) and lane l owns columns l + 64c, c < d_v/64.  The row
+//    contractions u = S'^T k and o = S^T q are then sequential fma chains in
+//    registers (one 32-row block per wave) plus a halving combine of the
+//    per-wave partials through LDS; every row's width, offset and scale is
+//    wave-uniform, so bit fields are extracted with uniform shifts.
+//  * row layout (fit): after an LDS transpose, thread t owns one 64-column
+//    segment of one row; the clip-factor fit needs no cross-lane traffic
+//    except the combine of the d_v/64 segment errors of a row.
+//
+// Decode (C = 1) runs three kernels: stats (recurrence, outputs, row ranges,
+// EMA rates, weights), alloc (layer budget per sequence; skipped for the
+// per-head scope, which allocates inside stats) and requant (recompute the
+// recurrence from the record, fit, quantise, pack in place).
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kda_alloc.hpp"
+#include "kda_device.hpp"
+#include "kda_kernels.hpp"
+#include "kda_profile.hpp"
+
+namespace kda {
+
+// ------------------------------------------------------------ helpers ---
+
+__device__ inline const uint8_t* slot_ptr(const void* recs, long long slot, int bh) {
+  return (const uint8_t*)recs + slot * (long long)bh;
+}
+
+template <int DK>
+struct MetaSmem {
+  uint8_t w[DK];      // widths of the stored record
+  int P[DK + 1];      // prefix sums of widths (row bit offsets)
+  float sc[DK];       // stored scales (FP16 -> float)
+  uint16_t z[DK];     // stored rate codes
+  uint16_t r16[DK];   // stored erase rates
+  unsigned ntok;
+};
+
+// Load widths/scales/stat codes of a record and form the row offsets.
+// Widths above b_max (never written by this library) are clamped so that a
+// damaged record cannot address code words outside its slot.
+template <int DK>
+__device__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
+  const int tid = threadIdx.x;
+  if (tid < DK / 2) {
+    const uint8_t byte = rec[L.w_off + tid];
+    m.w[2 * tid] = (uint8_t)min((byte & 15) + 1, bmax);
+    m.w[2 * tid + 1] = (uint8_t)min((byte >> 4) + 1, bmax);
+  }
+  if (tid < DK) {
+    m.sc[tid] = f16_to_f32(((const uint16_t*)(rec + L.sc_off))[tid]);
+    m.z[tid] = ((const uint16_t*)(rec + L.z_off))[tid];
+    m.r16[tid] = ((const uint16_t*)(rec + L.r_off))[tid];
+  }
+  if (tid == 0) m.ntok = *(const unsigned*)rec;
+  __syncthreads();
+  if (tid < WAVE) {
+    constexpr int PER = (DK + WAVE - 1) / WAVE;
+    int loc[PER], sum = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int i = tid * PER + q;
+      loc[q] = i < DK ? m.w[i] : 0;
+      sum += loc[q];
+    }
+    const int incl = wave_incl_scan(sum);
+    int run = incl - sum;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int i = tid * PER + q;
+      if (i < DK) m.P[i] = run;
+      run += loc[q];
+    }
+    if (tid == WAVE - 1) m.P[DK] = incl;
+  }
+  __syncthreads();
+}
+
+// Per-row scalars of one token for the recurrence.
+template <int DK>
+struct RowSmem {
+  float a[DK];   // fl32(exp(-s))
+  float k[DK];
+  float q[DK];
+  float g[DK];   // fl32(beta * k)
+};
+
+template <int DK>
+__device__ void load_rows(RowSmem<DK>& rs, const float* q, const float* k, const float* s,
+                          float beta, bool per_head) {
+  const int t = threadIdx.x;
+  if (t < DK) {
+    const float sv = per_head ? s[0] : s[t];
+    rs.a[t] = (float)exp(-(double)sv);
+    const float kv = k[t];
+    rs.k[t] = kv;
+    rs.q[t] = q[t];
+    rs.g[t] = beta * kv;
+  }
+}
+
+// Decode one record into column-layout registers X[r][c] (row 32w + r,
+// column lane + 64c): x^ = fl32(code * Delta), or +-mu for one-bit rows.
+template <int DK, int DV>
+__device__ void unpack_cols(const uint8_t* rec, const Layout& L, const MetaSmem<DK>& m,
+                            float (&X)[ROW_BLOCK][DV / WAVE]) {
+  constexpr int CPL = DV / WAVE;
+  const int w = threadIdx.x / WAVE, lane = lane_id();
+  const uint32_t* words = (const uint32_t*)(rec + L.codes_off);
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r) {
+    const int i = w * ROW_BLOCK + r;
+    const int b = m.w[i];
+    const int P = m.P[i];
+    const int kw = P >> 5, sh = P & 31;
+    const bool two = sh + b > 32;
+    const float sc = m.sc[i];
+    const uint32_t mask = (b >= 32) ? 0xffffffffu : ((1u << b) - 1u);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int col = lane + WAVE * c;
+      const uint32_t lo = words[kw * DV + col];
+      const uint32_t hi = two ? words[(kw + 1) * DV + col] : 0u;
+      const uint32_t f = (uint32_t)((((uint64_t)hi << 32) | lo) >> sh) & mask;
+      float x;
+      if (b == 1) {
+        x = f ? -sc : sc;
+      } else {
+        const int code = ((int)(f << (32 - b))) >> (32 - b);
+        x = (float)code * sc;
+      }
+      X[r][c] = x;
+    }
+  }
+}
+
+template <int DK, int DV>
+struct RecSmem {
+  float up[DK / ROW_BLOCK][DV];
+  float op[DK / ROW_BLOCK][DV];
+};
+
+// Halving combine of the per-wave partials of column col.
+template <int DK, int DV>
+__device__ inline float combine_col(const float (&P)[DK / ROW_BLOCK][DV], int col) {
+  constexpr int NWV = DK / ROW_BLOCK;
+  float v[NWV];
+#pragma unroll
+  for (int p = 0; p < NWV; ++p) v[p] = P[p][col];
+#pragma unroll
+  for (int Lh = NWV / 2; Lh >= 1; Lh >>= 1) {
+#pragma unroll
+    for (int p = 0; p < Lh; ++p) v[p] = v[p] + v[p + Lh];
+  }
+  return v[0];
+}
+
+// One token of the gated delta rule on column-layout registers (eq. rule,
+// KDA erase/write): S' = a S; u = S'^T k; S = S' + (beta k)(v - u)^T;
+// o = S^T q.  Writes o to o_out (if non-null).  All threads must call.
+template <int DK, int DV>
+__device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
+                            RecSmem<DK, DV>& sm, const float* v, float* o_out) {
+  constexpr int CPL = DV / WAVE;
+  const int w = threadIdx.x / WAVE, lane = lane_id();
+  float acc[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r) {
+    const int i = w * ROW_BLOCK + r;
+    const float a = rs.a[i], kk = rs.k[i];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      X[r][c] = a * X[r][c];
+      acc[c] = __builtin_fmaf(kk, X[r][c], acc[c]);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) sm.up[w][lane + WAVE * c] = acc[c];
+  __syncthreads();
+  float wv[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int col = lane + WAVE * c;
+    const float u = combine_col<DK, DV>(sm.up, col);
+    wv[c] = v[col] - u;
+    acc[c] = 0.f;
+  }
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r) {
+    const int i = w * ROW_BLOCK + r;
+    const float g = rs.g[i], qq = rs.q[i];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      X[r][c] = __builtin_fmaf(g, wv[c], X[r][c]);
+      acc[c] = __builtin_fmaf(qq, X[r][c], acc[c]);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) sm.op[w][lane + WAVE * c] = acc[c];
+  __syncthreads();
+  if (o_out != nullptr && w == 0) {
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int col = lane + WAVE * c;
+      o_out[col] = combine_col<DK, DV>(sm.op, col);
+    }
+  }
+}
+
+// Row absolute maxima of column-layout registers into R[DK].
+template <int DK, int DV>
+__device__ void row_max(const float (&X)[ROW_BLOCK][DV / WAVE], float* R) {
+  constexpr int CPL = DV / WAVE;
+  const int w = threadIdx.x / WAVE, lane = lane_id();
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r) {
+    float mx = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) mx = fmaxf(mx, fabsf(X[r][c]));
+    mx = wave_max(mx);
+    if (lane == 0) R[w * ROW_BLOCK + r] = mx;
+  }
+}
+
+// ----------------------------------------------------- row-layout fit ---
+
+// Quantise rows held row-major in LDS (float S[DK][ld]) with widths b[] and
+// write int16 codes into C[DK][DV] (may alias S once every thread has loaded
+// its segment: an internal barrier separates the two) and FP16 scales.
+// Contract: see include/kda.h and the method description at the top.
+template <int DK, int DV>
+__device__ void fit_rows(const float* S, int ld, const uint8_t* bits, const float (*phi)[N_FIT],
+                         int16_t* C, uint16_t* scale_out) {
+  constexpr int SEGS = DV / SEG;
+  constexpr int ITEMS = DK * SEGS;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  // codes overwrite S after the (single) load pass: one item per thread
+  static_assert(ITEMS <= 2 * DK, "one fit item per thread");
+  // all threads run the same number of item iterations (barrier inside)
+  const int iters = (ITEMS + nt - 1) / nt;
+  for (int it = 0; it < iters; ++it) {
+    const int item = it * nt + tid;
+    const bool valid = item < ITEMS;
+    const int i = valid ? item / SEGS : 0;
+    const int sg = item % SEGS;
+    float x[SEG];
+    const float* src = S + (size_t)i * ld + sg * SEG;
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) x[j] = src[j];
+    __syncthreads();  // codes may overwrite S below
+    float mx = 0.f;
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) mx = fmaxf(mx, fabsf(x[j]));
+#pragma unroll
+    for (int o = 1; o < SEGS; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, WAVE));
+    const int b = bits[i];
+    int16_t* dst = C + (size_t)i * DV + sg * SEG;
+    if (b == 1) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) acc = acc + fabsf(x[j]);
+      // halving over segments: lanes differing in the top segment bit first
+#pragma unroll
+      for (int o = SEGS >> 1; o >= 1; o >>= 1) acc = acc + __shfl_xor(acc, o, WAVE);
+      const uint16_t mu = f32_to_f16_sat(acc * (1.0f / (float)DV));
+      if (valid) {
+#pragma unroll
+        for (int j = 0; j < SEG; ++j) dst[j] = (int16_t)(x[j] < 0.f ? 1 : 0);
+        if (sg == 0) scale_out[i] = mu;
+      }
+    } else {
+      const float nf = (float)((1 << (b - 1)) - 1);
+      float best = __builtin_inff();
+      int mb = 0;
+      for (int m = 0; m < N_FIT; ++m) {
+        const float d = f16_to_f32(f32_to_f16_sat(mx * phi[b][m]));
+        const float inv = d > 0.f ? 1.0f / d : 0.f;
+        float err = 0.f;
+#pragma unroll
+        for (int j = 0; j < SEG; ++j) {
+          float c = __builtin_rintf(x[j] * inv);
+          c = fminf(fmaxf(c, -nf), nf);
+          const float e = __builtin_fmaf(-c, d, x[j]);
+          err = __builtin_fmaf(e, e, err);
+        }
+#pragma unroll
+        for (int o = SEGS >> 1; o >= 1; o >>= 1) err = err + __shfl_xor(err, o, WAVE);
+        if (err < best) { best = err; mb = m; }
+      }
+      const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
+      const float d = f16_to_f32(dh);
+      const float inv = d > 0.f ? 1.0f / d : 0.f;
+      if (valid) {
+#pragma unroll
+        for (int j = 0; j < SEG; ++j) {
+          float c = __builtin_rintf(x[j] * inv);
+          c = fminf(fmaxf(c, -nf), nf);
+          dst[j] = (int16_t)c;
+        }
+        if (sg == 0) scale_out[i] = dh;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Pack int16 codes C[DK][DV] with widths b[] into column bit streams (one
+// thread per column, rows in order).
+template <int DK, int DV>
+__device__ void pack_cols(const int16_t* C, const uint8_t* bits, uint32_t* words) {
+  const int tid = threadIdx.x;
+  for (int col = tid; col < DV; col += blockDim.x) {
+    uint64_t acc = 0;
+    int nb = 0, wi = 0;
+    for (int i = 0; i < DK; ++i) {
+      const int b = bits[i];
+      const uint32_t f = (uint32_t)(int)C[(size_t)i * DV + col] & ((b >= 32) ? 0xffffffffu : ((1u << b) - 1u));
+      acc |= (uint64_t)f << nb;
+      nb += b;
+      if (nb >= 32) {
+        words[wi * DV + col] = (uint32_t)acc;
+        ++wi;
+        acc >>= 32;
+        nb -= 32;
+      }
+    }
+    if (nb > 0) words[wi * DV + col] = (uint32_t)acc;
+  }
+}
+
+// Write a record's metadata (header, widths, scales, stat codes).
+template <int DK>
+__device__ void store_meta(uint8_t* rec, const Layout& L, unsigned ntok, const uint8_t* bits,
+                           const uint16_t* scale16, const uint16_t* z, const uint16_t* r16) {
+  const int tid = threadIdx.x;
+  if (tid < 4) ((unsigned*)rec)[tid] = tid == 0 ? ntok : 0u;
+  if (tid < DK / 2)
+    rec[L.w_off + tid] = (uint8_t)((bits[2 * tid] - 1) | ((bits[2 * tid + 1] - 1) << 4));
+  if (tid < DK) {
+    ((uint16_t*)(rec + L.sc_off))[tid] = scale16[tid];
+    ((uint16_t*)(rec + L.z_off))[tid] = z[tid];
+    ((uint16_t*)(rec + L.r_off))[tid] = r16[tid];
+  }
+}
+
+// ---------------------------------------------------------- kernels ---
+
+// Row statistics of one write-back for one head (threads t < DK own row t).
+template <int DK>
+struct StatSmem {
+  float R[DK];
+  double gam[DK];
+  double rms[DK];
+  double c[DK];
+};
+
+template <int DK>
+__device__ void row_weights(const KParams& p, int bh, const MetaSmem<DK>& meta,
+                            StatSmem<DK>& st, double m_run, double e_run, int t) {
+  // m_run/e_run: EMA states of row t after the last token (thread t < DK)
+  if (t < DK) {
+    const double s_hat = -0.5 * log(m_run);
+    const double r = 0.5 * e_run;
+    st.gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
+  }
+  __syncthreads();
+  if (t < DK && t % p.G == 0) {
+    double acc = 0.0;
+    for (int j = t; j < t + p.G; ++j) {
+      const double R = (double)st.R[j];
+      acc = acc + R * R;
+    }
+    st.rms[t / p.G] = sqrt(acc / (double)p.G);
+  }
+  __syncthreads();
+  if (t < DK) {
+    const double rms = st.rms[t / p.G];
+    const double Rt = rms > 0.0 ? (double)st.R[t] / rms : 0.0;
+    const double c = st.gam[t] * (Rt * Rt);
+    st.c[t] = c;
+    p.ws_c[(size_t)bh * DK + t] = c;
+  }
+  __syncthreads();
+}
+
+template <int DK, int DV, bool HEAD>
+__global__ void __launch_bounds__(2 * DK) k_stats(KParams p) {
+  const int bh = blockIdx.x;
+  const int t = threadIdx.x;
+  const Layout L = p.L;
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ RowSmem<DK> rs;
+  __shared__ RecSmem<DK, DV> rsm;
+  __shared__ StatSmem<DK> st;
+  load_meta<DK>(rec, L, p.bmax, meta);
+  const float beta = p.beta[bh];
+  load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
+                p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), beta, p.per_head);
+  __syncthreads();
+  float X[ROW_BLOCK][DV / WAVE];
+  unpack_cols<DK, DV>(rec, L, meta, X);
+  recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, p.o + (size_t)bh * DV);
+  row_max<DK, DV>(X, st.R);
+  // EMA of the rates (first token of a fresh state initialises)
+  double m_run = 0.0, e_run = 0.0;
+  if (t < DK) {
+    const float sv = p.per_head ? p.s[bh] : p.s[(size_t)bh * DK + t];
+    const float kv = p.k[(size_t)bh * DK + t];
+    const double zs = decay_sample(sv), ys = erase_sample(kv, beta);
+    if (meta.ntok == 0) {
+      m_run = zs;
+      e_run = ys;
+    } else {
+      const double m0 = exp(-2.0 * logq_decode(meta.z[t]));
+      const double e0 = 2.0 * (double)f16_to_f32(meta.r16[t]);
+      m_run = p.one_minus_alpha * m0 + p.alpha * zs;
+      e_run = p.one_minus_alpha * e0 + p.alpha * ys;
+    }
+  }
+  __syncthreads();
+  row_weights<DK>(p, bh, meta, st, m_run, e_run, t);
+  if constexpr (HEAD) {
+    // per-head budget: allocate here (c of this head is in LDS)
+    __shared__ AllocSmem asm_;
+    block_allocate([&](int n) { return st.c[n]; }, DK, p.need, p.bmin, p.bmax,
+                   p.ws_bits + (size_t)bh * DK, asm_);
+  }
+}
+
+// Layer budget: one block per scope unit of N rows (contiguous in ws_c).
+__global__ void __launch_bounds__(1024) k_alloc(const double* c, int N, int need, int bmin,
+                                                int bmax, uint8_t* bits) {
+  __shared__ AllocSmem sm;
+  const double* cu = c + (size_t)blockIdx.x * N;
+  block_allocate([&](int n) { return cu[n]; }, N, need, bmin, bmax,
+                 bits + (size_t)blockIdx.x * N, sm);
+}
+
+// Recompute the token from the record, fit, quantise and pack in place.
+template <int DK, int DV>
+__global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
+  const int bh = blockIdx.x;
+  const Layout L = p.L;
+  uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ RowSmem<DK> rs;
+  __shared__ RecSmem<DK, DV> rsm;
+  __shared__ float Sx[DK * (DV + 4)];
+  __shared__ uint8_t nb[DK];
+  __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
+  __shared__ float phi[MAX_B + 1][N_FIT];
+  const int t = threadIdx.x;
+  load_meta<DK>(rec, L, p.bmax, meta);
+  const float beta = p.beta[bh];
+  load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
+                p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), beta, p.per_head);
+  if (t < DK) {
+    nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
+    const uint32_t zr = p.ws_zr[(size_t)bh * DK + t];
+    zz[t] = (uint16_t)(zr & 0xffffu);
+    rr[t] = (uint16_t)(zr >> 16);
+  }
+  for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
+  __syncthreads();
+  float X[ROW_BLOCK][DV / WAVE];
+  unpack_cols<DK, DV>(rec, L, meta, X);
+  recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, nullptr);
+  // transpose to row layout
+  {
+    constexpr int CPL = DV / WAVE;
+    const int w = t / WAVE, lane = lane_id();
+#pragma unroll
+    for (int r = 0; r < ROW_BLOCK; ++r)
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) Sx[(w * ROW_BLOCK + r) * (DV + 4) + lane + WAVE * c] = X[r][c];
+  }
+  __syncthreads();
+  int16_t* C = (int16_t*)Sx;
+  fit_rows<DK, DV>(Sx, DV + 4, nb, phi, C, sc16);
+  __syncthreads();
+  pack_cols<DK, DV>(C, nb, (uint32_t*)(rec + L.codes_off));
+  store_meta<DK>(rec, L, meta.ntok + 1u, nb, sc16, zz, rr);
+}
+
+// Unquantised ("32-bit") state: load, one token, store.
+template <int DK, int DV>
+__global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
+  constexpr int CPL = DV / WAVE;
+  const int bh = blockIdx.x;
+  const int w = threadIdx.x / WAVE, lane = lane_id();
+  float* S = (float*)((uint8_t*)p.records + (long long)bh * DK * DV * 4);
+  __shared__ RowSmem<DK> rs;
+  __shared__ RecSmem<DK, DV> rsm;
+  load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
+                p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), p.beta[bh], p.per_head);
+  float X[ROW_BLOCK][CPL];
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) X[r][c] = S[(w * ROW_BLOCK + r) * DV + lane + WAVE * c];
+  __syncthreads();
+  recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, p.o + (size_t)bh * DV);
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) S[(w * ROW_BLOCK + r) * DV + lane + WAVE * c] = X[r][c];
+}
+
+// Standalone codec: quantise given states.
+template <int DK, int DV>
+__global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, const uint8_t* bits,
+                                                 const double* s_hat, const double* r,
+                                                 unsigned ntok) {
+  const int bh = blockIdx.x;
+  const Layout L = p.L;
+  uint8_t* rec = (uint8_t*)p.records + L.slot * (long long)bh;
+  __shared__ float Sx[DK * (DV + 4)];
+  __shared__ uint8_t nb[DK];
+  __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
+  __shared__ float phi[MAX_B + 1][N_FIT];
+  const int t = threadIdx.x;
+  const float* src = S + (size_t)bh * DK * DV;
+  for (int e = t; e < DK * DV; e += blockDim.x) Sx[(e / DV) * (DV + 4) + e % DV] = src[e];
+  if (t < DK) {
+    nb[t] = (uint8_t)min(max((int)bits[(size_t)bh * DK + t], 1), p.bmax);
+    zz[t] = logq_encode(s_hat[(size_t)bh * DK + t]);
+    rr[t] = r_encode(r[(size_t)bh * DK + t]);
+  }
+  for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
+  __syncthreads();
+  int16_t* C = (int16_t*)Sx;
+  fit_rows<DK, DV>(Sx, DV + 4, nb, phi, C, sc16);
+  __syncthreads();
+  pack_cols<DK, DV>(C, nb, (uint32_t*)(rec + L.codes_off));
+  store_meta<DK>(rec, L, ntok, nb, sc16, zz, rr);
+}
+
+// Standalone codec: decode records.
+template <int DK, int DV>
+__global__ void __launch_bounds__(2 * DK) k_unpack(KParams p, float* S, uint8_t* bits,
+                                                   double* s_hat, double* r) {
+  constexpr int CPL = DV / WAVE;
+  const int bh = blockIdx.x;
+  const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
+  const Layout L = p.L;
+  if (p.state32) {
+    if (S) {
+      const float* src = (const float*)((const uint8_t*)p.records + (long long)bh * DK * DV * 4);
+      for (int e = t; e < DK * DV; e += blockDim.x) S[(size_t)bh * DK * DV + e] = src[e];
+    }
+    return;
+  }
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  load_meta<DK>(rec, L, p.bmax, meta);
+  if (S) {
+    float X[ROW_BLOCK][CPL];
+    unpack_cols<DK, DV>(rec, L, meta, X);
+#pragma unroll
+    for (int rr_ = 0; rr_ < ROW_BLOCK; ++rr_)
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+        S[((size_t)bh * DK + w * ROW_BLOCK + rr_) * DV + lane + WAVE * c] = X[rr_][c];
+  }
+  if (t < DK) {
+    if (bits) bits[(size_t)bh * DK + t] = meta.w[t];
+    if (s_hat) s_hat[(size_t)bh * DK + t] = logq_decode(meta.z[t]);
+    if (r) r[(size_t)bh * DK + t] = (double)f16_to_f32(meta.r16[t]);
+  }
+}
+
+// Weights c = gamma * R~^2 from given gamma and R (kda_alloc_bits).
+template <int DK>
+__global__ void __launch_bounds__(DK) k_weights_from_ranges(KParams p, const double* gamma,
+                                                            const float* R) {
+  const int bh = blockIdx.x;
+  const int t = threadIdx.x;
+  __shared__ StatSmem<DK> st;
+  st.R[t] = R[(size_t)bh * DK + t];
+  st.gam[t] = gamma[(size_t)bh * DK + t];
+  __syncthreads();
+  if (t % p.G == 0) {
+    double acc = 0.0;
+    for (int j = t; j < t + p.G; ++j) {
+      const double v = (double)st.R[j];
+      acc = acc + v * v;
+    }
+    st.rms[t / p.G] = sqrt(acc / (double)p.G);
+  }
+  __syncthreads();
+  const double rms = st.rms[t / p.G];
+  const double Rt = rms > 0.0 ? (double)st.R[t] / rms : 0.0;
+  p.ws_c[(size_t)bh * DK + t] = st.gam[t] * (Rt * Rt);
+}
+
+// Windowed Gramian weights: one thread per (b, h, row), sequential in time.
+__global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head,
+                               const float* q, const float* s, const float* beta,
+                               const float* k, double* gamma) {
+  const long long id = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long total = (long long)B * H * DKr;
+  if (id >= total) return;
+  const int i = (int)(id % DKr);
+  const int h = (int)((id / DKr) % H);
+  const int b = (int)(id / ((long long)DKr * H));
+  double A = 0.0, acc = 0.0;
+  for (int t = 0; t < W; ++t) {
+    const size_t tok = ((size_t)b * W + t) * H + h;
+    const float sv = per_head ? s[tok] : s[tok * DKr + i];
+    const double y = erase_sample(k[tok * DKr + i], beta[tok]);
+    const double lam = exp(-2.0 * (double)sv - y);
+    if (t >= 1) {
+      const double chi = (t % C == 0) ? 1.0 : 0.0;  // write-back after token t-1
+      A = lam * (chi + A);
+      const double qq = (double)q[tok * DKr + i];
+      acc = acc + (qq * qq) * A;
+    }
+  }
+  gamma[id] = acc / (double)W;
+}
+
+// ------------------------------------------------------- launchers ---
+
+template <int DK, int DV>
+static hipError_t launch_step_t(const KParams& p, hipStream_t st) {
+  const int nbh = p.B * p.H;
+  if (p.state32) {
+    ProfScope ps("step32", st);
+    k_step32<DK, DV><<<nbh, 2 * DK, 0, st>>>(p);
+    return hipGetLastError();
+  }
+  hipError_t e;
+  {
+    ProfScope ps("stats", st);
+    if (p.scope == 1)
+      k_stats<DK, DV, true><<<nbh, 2 * DK, 0, st>>>(p);
+    else
+      k_stats<DK, DV, false><<<nbh, 2 * DK, 0, st>>>(p);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  if (p.scope == 0) {
+    ProfScope ps("alloc", st);
+    k_alloc<<<p.B, 1024, 0, st>>>(p.ws_c, p.H * DK, p.need, p.bmin, p.bmax, p.ws_bits);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  ProfScope ps("requant", st);
+  k_requant<DK, DV><<<nbh, 2 * DK, 0, st>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_step(const KParams& p, hipStream_t st) {
+  if (p.dk == 64) return launch_step_t<64, 64>(p, st);
+  return launch_step_t<128, 128>(p, st);
+}
+
+template <int DK, int DV>
+static hipError_t launch_pack_t(const KParams& p, const float* S, const uint8_t* bits,
+                                const double* s_hat, const double* r, unsigned ntok,
+                                hipStream_t st) {
+  ProfScope ps("pack", st);
+  k_pack<DK, DV><<<p.B * p.H, 2 * DK, 0, st>>>(p, S, bits, s_hat, r, ntok);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
+                       const double* r, unsigned ntok, hipStream_t st) {
+  if (p.dk == 64) return launch_pack_t<64, 64>(p, S, bits, s_hat, r, ntok, st);
+  return launch_pack_t<128, 128>(p, S, bits, s_hat, r, ntok, st);
+}
+
+hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,
+                         hipStream_t st) {
+  ProfScope ps("unpack", st);
+  if (p.dk == 64)
+    k_unpack<64, 64><<<p.B * p.H, 128, 0, st>>>(p, S, bits, s_hat, r);
+  else
+    k_unpack<128, 128><<<p.B * p.H, 256, 0, st>>>(p, S, bits, s_hat, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_alloc_bits(const KParams& p, const double* gamma, const float* R, uint8_t* bits,
+                             hipStream_t st) {
+  if (p.dk == 64)
+    k_weights_from_ranges<64><<<p.B * p.H, 64, 0, st>>>(p, gamma, R);
+  else
+    k_weights_from_ranges<128><<<p.B * p.H, 128, 0, st>>>(p, gamma, R);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int units = p.scope == 0 ? p.B : p.B * p.H;
+  const int N = p.scope == 0 ? p.H * p.dk : p.dk;
+  ProfScope ps("alloc", st);
+  k_alloc<<<units, 1024, 0, st>>>(p.ws_c, N, p.need, p.bmin, p.bmax, bits);
+  return hipGetLastError();
+}
+
+hipError_t launch_window_gamma(const KParams& p, int W, int C, const float* q, const float* s,
+                               const float* beta, const float* k, double* gamma, hipStream_t st) {
+  const long long total = (long long)p.B * p.H * p.dk;
+  const int bs = 256;
+  ProfScope ps("weights", st);
+  k_window_gamma<<<(unsigned)((total + bs - 1) / bs), bs, 0, st>>>(p.B, W, p.H, p.dk, C,
+                                                                   p.per_head, q, s, beta, k, gamma);
+  return hipGetLastError();
+}
+
+}  // namespace kda

@@ -1,0 +1,39 @@
+// Host-visible launch interface between the C ABI (kda_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kda_device.hpp"
+
+namespace kda {
+
+// Everything a kernel needs, passed by value.
+struct KParams {
+  int B, H, dk, dv, G, scope, bmin, bmax, per_head, state32;
+  int need;                 // granted slots per scope unit: K - N * b_min
+  double alpha, one_minus_alpha;
+  Layout L;
+  float phi[MAX_B + 1][N_FIT];   // fl32((5 + m) / (20 n_b)), n_b = 2^(b-1) - 1
+  // tensors (device)
+  void* records;
+  const float *q, *k, *v, *s, *beta;
+  const double* gamma;
+  float* o;
+  // workspace views
+  double* ws_c;
+  uint32_t* ws_zr;
+  uint8_t* ws_bits;
+};
+
+hipError_t launch_step(const KParams& p, hipStream_t st);
+hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
+                       const double* r, unsigned ntok, hipStream_t st);
+hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,
+                         hipStream_t st);
+hipError_t launch_alloc_bits(const KParams& p, const double* gamma, const float* R, uint8_t* bits,
+                             hipStream_t st);
+hipError_t launch_window_gamma(const KParams& p, int W, int C, const float* q, const float* s,
+                               const float* beta, const float* k, double* gamma, hipStream_t st);
+
+}  // namespace kda

@@ -1,0 +1,70 @@
+"""CPU-side checks of the C ABI: the library loads, exports every declared
+symbol, sizes records like the oracle's layout and validates arguments
+before launching anything (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_30950_amd as K
+from oracle import record
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "kda.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kda_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_30950_amd", "libkda.so"))
+    names = _declared()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+@pytest.mark.parametrize("d,bmax", [(64, 8), (128, 8), (128, 16)])
+def test_record_bytes_match_layout(d, bmax):
+    cfg = K.Config(B=1, H=1, d_k=d, d_v=d, group_rows=d, b_min=1, b_max=bmax, mean_bits=2)
+    assert K.record_bytes(cfg) == record.record_bytes(d, d, bmax)
+    cfg.state32 = 1
+    assert K.record_bytes(cfg) == record.state32_bytes(d, d)
+
+
+def test_invalid_configs_rejected():
+    lib = K.load()
+    bad = [
+        dict(d_k=96, d_v=96),                  # unsupported width
+        dict(d_k=64, d_v=128),
+        dict(mean_bits=1.5),                   # budget below b_min
+        dict(mean_bits=8.5),
+        dict(b_min=0),
+        dict(b_max=17),
+        dict(group_rows=48),
+        dict(scope=2),
+        dict(ema_span=0),
+        dict(H=64, d_k=128, d_v=128),          # > 4096 rows in one budget
+    ]
+    for kw in bad:
+        base = dict(B=1, H=2, d_k=64, d_v=64, group_rows=64)
+        base.update(kw)
+        cfg = K.Config(**base)
+        assert K.record_bytes(cfg) == 0, kw
+        st = lib.kda_step(ctypes.byref(cfg.c()), None, None, None, None, None, None, None, None,
+                          None, None)
+        assert st != 0, kw
+
+
+def test_null_pointers_rejected_before_launch():
+    lib = K.load()
+    cfg = K.Config(B=1, H=2, d_k=64, d_v=64)
+    assert lib.kda_step(ctypes.byref(cfg.c()), None, None, None, None, None, None, None, None,
+                        None, None) == 1
+    assert lib.kda_pack_state(ctypes.byref(cfg.c()), None, None, None, None, 0, None, None) == 1
+    assert lib.kda_unpack_state(ctypes.byref(cfg.c()), None, None, None, None, None, None) == 1
+    assert lib.kda_weights(ctypes.byref(cfg.c()), 0, 1, None, None, None, None, None, None) == 1
+    assert lib.kda_status_str(3).decode() == "unsupported configuration"

@@ -1,0 +1,75 @@
+"""GPU parity of kda_alloc_bits and kda_weights against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_30950_amd as K
+import workloads as W
+from oracle import alloc, stats
+from tests._gpu import dev, host, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle_bits(gamma, R, G, scope, mean, bmin, bmax):
+    B, H, d = gamma.shape
+    c = alloc.weights(gamma, alloc.normalized_ranges(R, G))
+    if scope == 0:
+        return np.stack([alloc.allocate(c[b].reshape(-1), mean, bmin, bmax).reshape(H, d)
+                         for b in range(B)])
+    return np.stack([[alloc.allocate(c[b, h], mean, bmin, bmax) for h in range(H)]
+                     for b in range(B)])
+
+
+CASES = [
+    (2, 3, 64, 64, 0, 4.0, 2, 8),
+    (2, 32, 128, 64, 0, 4.0, 2, 8),
+    (1, 32, 128, 128, 0, 2.0, 1, 8),
+    (3, 4, 128, 128, 1, 3.0, 1, 8),
+    (1, 8, 64, 32, 0, 5.5, 1, 16),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_alloc_bits_bit_exact(case):
+    B, H, d, G, scope, mean, bmin, bmax = case
+    say("alloc case", case)
+    rng = np.random.default_rng(7 * d + H)
+    gamma = np.exp(rng.normal(0, 3, (B, H, d)))
+    R = np.abs(rng.standard_normal((B, H, d))).astype(np.float32)
+    R[0, 0, :5] = 0.0                       # zero rows
+    gamma[0, 1, :] = 1.0                    # ties inside a head
+    R[0, 1, :] = 0.5
+    if H > 2:
+        R[0, 2, :] = 0.0                    # a whole zero head
+    cfg = K.Config(B=B, H=H, d_k=d, d_v=d, group_rows=G, scope=scope, mean_bits=mean,
+                   b_min=bmin, b_max=bmax)
+    bits = torch.zeros(B * H * d, dtype=torch.uint8, device="cuda")
+    ws = K.new_workspace(cfg)
+    K.kda_alloc_bits(cfg, dev(gamma), dev(R), bits, ws)
+    got = host(bits).reshape(B, H, d).astype(np.int64)
+    want = _oracle_bits(gamma, R, G, scope, mean, bmin, bmax)
+    assert np.array_equal(got, want), f"{np.sum(got != want)} widths differ"
+
+
+def test_alloc_all_zero_weights_fill_in_row_order():
+    B, H, d = 1, 2, 64
+    cfg = K.Config(B=B, H=H, d_k=d, d_v=d, group_rows=64, scope=0, mean_bits=2.3, b_min=2, b_max=8)
+    bits = torch.zeros(B * H * d, dtype=torch.uint8, device="cuda")
+    K.kda_alloc_bits(cfg, dev(np.zeros((B, H, d))), dev(np.zeros((B, H, d), np.float32)), bits,
+                     K.new_workspace(cfg))
+    want = alloc.allocate(np.zeros(H * d), 2.3, 2, 8)
+    assert np.array_equal(host(bits).astype(np.int64), want)
+
+
+@pytest.mark.parametrize("C", [1, 4])
+def test_window_weights_match_oracle(C):
+    w = W.sized(W.WORKLOADS["tiny"], B=2, H=3)
+    x = W.tokens(w, 0, 96)
+    cfg = K.Config(B=2, H=3, d_k=64, d_v=64)
+    g = torch.zeros(2 * 3 * 64, dtype=torch.float64, device="cuda")
+    K.kda_weights(cfg, 96, C, dev(x["q"]), dev(x["s"]), dev(x["beta"]), dev(x["k"]), g)
+    # oracle takes [W, ..., dk] time-major
+    want = stats.window_gamma(np.moveaxis(x["q"], 1, 0), np.moveaxis(x["s"], 1, 0),
+                              np.moveaxis(x["k"], 1, 0), np.moveaxis(x["beta"], 1, 0), C)
+    np.testing.assert_allclose(host(g).reshape(2, 3, 64), want, rtol=1e-12)

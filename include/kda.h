@@ -32,9 +32,11 @@
  * - Records: one fixed-size slot of kda_record_bytes() per (sequence, head),
  *   slots ordered [B][H].  A zero-filled slot is the zero state (fresh EMA).
  *   kda_step / kda_prefill update records in place.
- * - Workspace: kda_workspace_bytes() bytes, 256-byte aligned, ZERO-FILLED by
- *   the caller before its first use; calls leave its counters at zero again.
- *   Concurrent calls must not share a workspace.
+ * - Records, workspace and state arrays must be 16-byte aligned (device
+ *   allocations are); misaligned pointers give KDA_ERR_ARG.
+ * - Workspace: kda_workspace_bytes() bytes, used as scratch by one call at a
+ *   time (per-row weights, widths, rate codes and the float32 state between
+ *   the passes of a write-back).  Concurrent calls must not share one.
  */
 #ifndef KDA_H_
 #define KDA_H_
@@ -114,7 +116,7 @@ int kda_weights(const kda_config* cfg, int32_t W, int32_t C, const float* q,
  * minimising sum c_i 2^(-2 b_i) with sum b_i = floor(mean_bits*N + 0.5) over
  * each scope unit of N rows; ties to the lower row index.
  * In:  gamma [B][H][d_k] f64 (>= 0); R [B][H][d_k] f32 row absolute maxima.
- * Out: bits [B][H][d_k] u8.  ws: workspace (only its counters are used). */
+ * Out: bits [B][H][d_k] u8.  ws: workspace (scratch for the weights). */
 int kda_alloc_bits(const kda_config* cfg, const double* gamma, const float* R,
                    uint8_t* bits, void* ws, void* stream);
 

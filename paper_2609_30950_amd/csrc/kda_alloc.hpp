@@ -6,12 +6,16 @@
 // are granted, ties to the lower row index (then lower l).
 //
 // Slot keys are compared exactly as (E_i - 2 l, M_i) with c_i = M_i 2^E_i,
-// M_i in [0.5, 1) (frexp).  The search runs in two exact stages:
-//  1. bisection on the integer bucket E - 2 l: the largest bucket beta* such
-//     that at least `need` slots lie in buckets >= beta*;
-//  2. the rows owning a slot in bucket beta* (at most one slot per row) are
-//     sorted by (M desc, row asc) with an LDS bitonic sort and the first
-//     `need - (slots above beta*)` of them are granted that slot.
+// M_i in [0.5, 1) (frexp).  The selection runs in exact stages:
+//  1. bucket E - 2l: a histogram of the row exponents (wave ballots) gives the
+//     slot count of every bucket; the boundary bucket beta* is the highest one
+//     at which the running count from the top reaches `need`;
+//  2. rows owning a slot in beta* (at most one slot per row) are narrowed by
+//     radix passes over the 52 fraction bits (256-bin LDS histograms), each
+//     keeping the digit bin that contains the boundary, until at most one
+//     wave of candidates remains;
+//  3. one wave ranks those by (fraction desc, row asc) and grants the first
+//     ones.
 // Rows with c_i = 0 own slots below every positive one, granted in row order.
 #pragma once
 
@@ -19,29 +23,35 @@
 
 namespace kda {
 
-constexpr int ALLOC_MAX_N = 4096;  // rows per scope unit (12-bit row field)
-constexpr short E_ZERO = -32768;   // exponent sentinel of c = 0
+constexpr int ALLOC_MAX_N = 4096;     // rows per scope unit
+constexpr int ALLOC_MAX_T = 1024;     // threads per block
+constexpr int ALLOC_RPT = 4;          // rows per thread (N <= 4096 with 1024 threads)
+constexpr int E_ZERO = -100000;       // exponent sentinel of c = 0
+constexpr int EBINS = 2304;           // exponent histogram range (frexp: [-1073, 1024])
+constexpr int EOFF = 1100;
 
 struct AllocSmem {
-  short E[ALLOC_MAX_N];
-  unsigned long long keys[ALLOC_MAX_N];
+  int hist_e[EBINS];
+  int hist_d[256];
+  int red[32];
+  int cand_n;
+  int sel_beta, sel_digit, sel_rem, sel_mode;
+  unsigned long long cand_key[WAVE];
+  int cand_row[WAVE];
   unsigned char extra[ALLOC_MAX_N];
-  int red_i[32];
-  long long red_l[32];
-  int ncand;
 };
 
 __device__ inline int slots_ge(int E, int beta, int bmin, int L) {
   if (E == E_ZERO) return 0;
-  int lmax = (E - beta) >> 1;  // floor division
-  int c = lmax - bmin;
+  const int lmax = (E - beta) >> 1;  // floor division
+  const int c = lmax - bmin;
   return c < 0 ? 0 : (c > L ? L : c);
 }
 
 // Block-wide exclusive scan of one int per thread (row order = thread order).
 __device__ inline int block_excl_scan(int v, int* scratch, int* total) {
   const int w = threadIdx.x / WAVE, nw = (blockDim.x + WAVE - 1) / WAVE;
-  int incl = wave_incl_scan(v);
+  const int incl = wave_incl_scan(v);
   __syncthreads();
   if (lane_id() == WAVE - 1) scratch[w] = incl;
   __syncthreads();
@@ -54,30 +64,56 @@ __device__ inline int block_excl_scan(int v, int* scratch, int* total) {
   return off + incl - v;
 }
 
-// c: N weights (any address space readable by the block); out: N widths.
+// c_at(n): weight of row n (any address space); out: N widths.
 template <typename Load>
-__device__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax,
-                               uint8_t* out, AllocSmem& sm) {
-  const int tid = threadIdx.x, nt = blockDim.x;
+__device__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax, uint8_t* out,
+                               AllocSmem& sm) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id();
   const int L = bmax - bmin;
-  int emin = 0x7fffffff, emax = -0x7fffffff, npos = 0;
-  for (int n = tid; n < N; n += nt) {
-    const double cv = c_at(n);
-    short e = E_ZERO;
-    if (cv > 0.0) {
-      int ei;
-      (void)frexp(cv, &ei);
-      e = (short)ei;
-      emin = min(emin, ei);
-      emax = max(emax, ei);
-      ++npos;
+  // rows n = tid + k * nt, k < ALLOC_RPT
+  int E[ALLOC_RPT];
+  unsigned long long F[ALLOC_RPT];   // 52-bit fraction of the frexp mantissa
+  for (int e = tid; e < EBINS; e += nt) sm.hist_e[e] = 0;
+  for (int n = tid; n < N; n += nt) sm.extra[n] = 0;
+  if (tid == 0) sm.cand_n = 0;
+  int npos = 0;
+#pragma unroll
+  for (int k = 0; k < ALLOC_RPT; ++k) {
+    const int n = tid + k * nt;
+    E[k] = E_ZERO;
+    F[k] = 0;
+    if (n < N) {
+      const double cv = c_at(n);
+      if (cv > 0.0) {
+        int ei;
+        const double m = frexp(cv, &ei);
+        E[k] = ei;
+        F[k] = (unsigned long long)ldexp(m, 53) - (1ull << 52);
+        ++npos;
+      }
     }
-    sm.E[n] = e;
-    sm.extra[n] = 0;
   }
-  emin = block_reduce(emin, sm.red_i, [](int a, int b) { return a < b ? a : b; });
-  emax = block_reduce(emax, sm.red_i, [](int a, int b) { return a > b ? a : b; });
-  npos = block_reduce(npos, sm.red_i, [](int a, int b) { return a + b; });
+  __syncthreads();
+  // histogram of exponents: one LDS atomic per distinct value in a wave
+#pragma unroll
+  for (int k = 0; k < ALLOC_RPT; ++k) {
+    bool pending = E[k] != E_ZERO;
+    while (__ballot(pending)) {
+      const unsigned long long act = __ballot(pending);
+      const int leader = __ffsll((long long)act) - 1;
+      const int e0 = __builtin_amdgcn_readlane(E[k], leader);
+      const unsigned long long same = __ballot(pending && E[k] == e0);
+      if (lane == leader) atomicAdd(&sm.hist_e[e0 + EOFF], __popcll(same));
+      if (pending && E[k] == e0) pending = false;
+    }
+  }
+  int emin = 0x7fffffff, emax = -0x7fffffff;
+#pragma unroll
+  for (int k = 0; k < ALLOC_RPT; ++k)
+    if (E[k] != E_ZERO) { emin = min(emin, E[k]); emax = max(emax, E[k]); }
+  npos = block_reduce(npos, sm.red, [](int a, int b) { return a + b; });
+  emin = block_reduce(emin, sm.red, [](int a, int b) { return a < b ? a : b; });
+  emax = block_reduce(emax, sm.red, [](int a, int b) { return a > b ? a : b; });
   __syncthreads();
   const long long ptot = (long long)npos * L;
 
@@ -89,11 +125,12 @@ __device__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax,
     // every positive slot, then zero rows in row order
     const long long rem0 = need - ptot;
     int carry = 0;
-    for (int base = 0; base < N; base += nt) {
-      const int n = base + tid;
-      const int isz = (n < N && sm.E[n] == E_ZERO) ? 1 : 0;
+#pragma unroll
+    for (int k = 0; k < ALLOC_RPT; ++k) {
+      const int n = tid + k * nt;
+      const int isz = (n < N && E[k] == E_ZERO) ? 1 : 0;
       int tot;
-      const int z = carry + block_excl_scan(isz, sm.red_i, &tot);
+      const int z = carry + block_excl_scan(isz, sm.red, &tot);
       if (n < N) {
         int b;
         if (!isz) {
@@ -111,78 +148,155 @@ __device__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax,
     return;
   }
 
-  // stage 1: bucket bisection
-  int lo = emin - 2 * bmax, hi = emax - 2 * (bmin + 1);
-  while (lo < hi) {
-    const int mid = lo + ((hi - lo + 1) >> 1);
-    long long cnt = 0;
-    for (int n = tid; n < N; n += nt) cnt += slots_ge(sm.E[n], mid, bmin, L);
-    cnt = block_reduce(cnt, sm.red_l, [](long long a, long long b) { return a + b; });
-    if (cnt >= need) lo = mid; else hi = mid - 1;
+  // stage 1: boundary bucket from the exponent histogram.  Bucket bb holds
+  // sum_l hist[bb + 2l] slots; wave 0 examines 64 buckets at a time from the
+  // top and finds the first at which the running count reaches `need`.
+  if (tid < WAVE) {
+    const int top = emax - 2 * (bmin + 1);
+    const int bot = emin - 2 * bmax;
+    long long run = 0;
+    for (int b0 = top; b0 >= bot; b0 -= WAVE) {
+      const int bb = b0 - lane;
+      long long cnt = 0;
+      if (bb >= bot)
+        for (int l = bmin + 1; l <= bmax; ++l) {
+          const int e = bb + 2 * l + EOFF;
+          if (e >= 0 && e < EBINS) cnt += sm.hist_e[e];
+        }
+      // inclusive prefix over lanes (lane order = descending bucket)
+      long long incl = cnt;
+      for (int o = 1; o < WAVE; o <<= 1) {
+        const long long v = __shfl_up(incl, o, WAVE);
+        if (lane >= o) incl += v;
+      }
+      const unsigned long long hit = __ballot(run + incl >= need);
+      if (hit) {
+        const int f = __ffsll((long long)hit) - 1;
+        if (lane == f) {
+          sm.sel_beta = bb;
+          sm.sel_rem = (int)(need - (run + incl - cnt));
+        }
+        break;
+      }
+      run += __shfl(incl, WAVE - 1, WAVE);
+    }
   }
-  const int beta = lo;
-  long long ngt = 0;
-  for (int n = tid; n < N; n += nt) ngt += slots_ge(sm.E[n], beta + 1, bmin, L);
-  ngt = block_reduce(ngt, sm.red_l, [](long long a, long long b) { return a + b; });
-  const long long rem = need - ngt;  // >= 1 slots taken inside bucket beta
+  __syncthreads();
+  const int beta = sm.sel_beta;
+  int rem = sm.sel_rem;
 
-  // stage 2: candidates of bucket beta
-  if (tid == 0) sm.ncand = 0;
-  __syncthreads();
-  for (int base = 0; base < N; base += nt) {
-    const int n = base + tid;
-    bool cand = false;
-    unsigned long long key = 0;
-    if (n < N) {
-      const int e = sm.E[n];
-      if (e != E_ZERO && ((e - beta) & 1) == 0) {
-        const int l = (e - beta) >> 1;
-        if (l >= bmin + 1 && l <= bmax) {
-          int ei;
-          const double m = frexp(c_at(n), &ei);           // [0.5, 1)
-          const unsigned long long m53 = (unsigned long long)ldexp(m, 53);
-          key = ((m53 - (1ull << 52)) << 12) | (unsigned long long)(ALLOC_MAX_N - 1 - n);
-          cand = true;
-        }
-      }
-    }
-    const unsigned long long mask = __ballot(cand);
-    int wbase = 0;
-    if (lane_id() == 0 && mask) wbase = atomicAdd(&sm.ncand, __popcll(mask));
-    wbase = __shfl(wbase, 0, WAVE);
-    if (cand) {
-      const int pos = wbase + __popcll(mask & ((1ull << lane_id()) - 1ull));
-      sm.keys[pos] = key;
+  // stage 2: radix narrowing of the candidates of bucket beta
+  bool cand[ALLOC_RPT];
+#pragma unroll
+  for (int k = 0; k < ALLOC_RPT; ++k) {
+    cand[k] = false;
+    if (E[k] != E_ZERO && ((E[k] - beta) & 1) == 0) {
+      const int l = (E[k] - beta) >> 1;
+      cand[k] = l >= bmin + 1 && l <= bmax;
     }
   }
-  __syncthreads();
-  const int nc = sm.ncand;
-  if (rem >= nc) {
-    for (int p = tid; p < nc; p += nt)
-      sm.extra[ALLOC_MAX_N - 1 - (int)(sm.keys[p] & 4095ull)] = 1;
-  } else {
-    int p2 = 1;
-    while (p2 < nc) p2 <<= 1;
-    for (int p = nc + tid; p < p2; p += nt) sm.keys[p] = 0ull;
+  bool many = true;
+  for (int pass = 0; pass < 7; ++pass) {
+    const int shift = pass < 6 ? 44 - 8 * pass : 0;
+    const unsigned long long dmask = pass < 6 ? 255ull : 15ull;
+    int live = 0;
+#pragma unroll
+    for (int k = 0; k < ALLOC_RPT; ++k) live += cand[k];
+    live = block_reduce(live, sm.red, [](int a, int b) { return a + b; });
+    if (live <= WAVE) { many = false; break; }
+    // candidates above the boundary digit are granted; keep the boundary bin
+    for (int e = tid; e < 256; e += nt) sm.hist_d[e] = 0;
     __syncthreads();
-    for (int k = 2; k <= p2; k <<= 1) {
-      for (int j = k >> 1; j > 0; j >>= 1) {
-        for (int t = tid; t < (p2 >> 1); t += nt) {
-          const int i = (t / j) * 2 * j + (t % j);
-          const int l = i + j;
-          const bool up = (i & k) == 0;
-          const unsigned long long a = sm.keys[i], b = sm.keys[l];
-          if ((a < b) == up) { sm.keys[i] = b; sm.keys[l] = a; }
+#pragma unroll
+    for (int k = 0; k < ALLOC_RPT; ++k)
+      if (cand[k]) atomicAdd(&sm.hist_d[(F[k] >> shift) & dmask], 1);
+    __syncthreads();
+    if (tid < WAVE) {
+      // lane j covers bins 4j+3..4j of the descending order dmask..0
+      const int nb = (int)dmask + 1;
+      int h[4], tot = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int d = (int)dmask - (4 * lane + u);
+        h[u] = d >= 0 ? sm.hist_d[d] : 0;
+        tot += h[u];
+      }
+      (void)nb;
+      const int incl = wave_incl_scan(tot);
+      const unsigned long long hit = __ballot(incl >= rem);
+      const int f = __ffsll((long long)hit) - 1;
+      if (lane == f) {
+        int run = incl - tot;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (run + h[u] >= rem) {
+            sm.sel_digit = (int)dmask - (4 * lane + u);
+            sm.sel_rem = rem - run;
+            break;
+          }
+          run += h[u];
         }
-        __syncthreads();
       }
     }
-    for (int p = tid; p < (int)rem; p += nt)
-      sm.extra[ALLOC_MAX_N - 1 - (int)(sm.keys[p] & 4095ull)] = 1;
+    __syncthreads();
+    const unsigned long long dg = (unsigned long long)sm.sel_digit;
+#pragma unroll
+    for (int k = 0; k < ALLOC_RPT; ++k) {
+      if (!cand[k]) continue;
+      const unsigned long long d = (F[k] >> shift) & dmask;
+      if (d > dg) {
+        sm.extra[tid + k * nt] = 1;   // above the boundary digit: granted
+        cand[k] = false;
+      } else if (d < dg) {
+        cand[k] = false;
+      }
+    }
+    rem = sm.sel_rem;
+    __syncthreads();
+  }
+  if (many) {
+    // more than a wave of candidates with identical keys: lowest rows first
+    int carry = 0;
+#pragma unroll
+    for (int k = 0; k < ALLOC_RPT; ++k) {
+      int tot;
+      const int z = carry + block_excl_scan(cand[k] ? 1 : 0, sm.red, &tot);
+      if (cand[k] && z < rem) sm.extra[tid + k * nt] = 1;
+      cand[k] = false;
+      carry += tot;
+      __syncthreads();
+    }
+  }
+  // stage 3: at most one wave of candidates left; rank them in wave 0
+#pragma unroll
+  for (int k = 0; k < ALLOC_RPT; ++k) {
+    if (cand[k]) {
+      const int pos = atomicAdd(&sm.cand_n, 1);
+      sm.cand_key[pos] = F[k];
+      sm.cand_row[pos] = tid + k * nt;
+    }
   }
   __syncthreads();
-  for (int n = tid; n < N; n += nt)
-    out[n] = (uint8_t)(bmin + slots_ge(sm.E[n], beta + 1, bmin, L) + sm.extra[n]);
+  if (tid < WAVE) {
+    const int nc = sm.cand_n;
+    if (lane < nc) {
+      const unsigned long long my = sm.cand_key[lane];
+      const int myr = sm.cand_row[lane];
+      int rank = 0;
+      for (int j = 0; j < nc; ++j) {
+        const unsigned long long o = sm.cand_key[j];
+        const int orow = sm.cand_row[j];
+        rank += (o > my) || (o == my && orow < myr);
+      }
+      if (rank < rem) sm.extra[myr] = 1;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < ALLOC_RPT; ++k) {
+    const int n = tid + k * nt;
+    if (n < N) out[n] = (uint8_t)(bmin + slots_ge(E[k], beta + 1, bmin, L) + sm.extra[n]);
+  }
 }
 
 }  // namespace kda

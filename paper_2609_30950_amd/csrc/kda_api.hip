@@ -86,9 +86,13 @@ void set_ws(KParams& p, const kda_config* cfg, void* ws) {
   p.ws_c = (double*)(base + w.c_off);
   p.ws_zr = (uint32_t*)(base + w.zr_off);
   p.ws_bits = base + w.bits_off;
+  p.ws_s32 = (float*)(base + w.s32_off);
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KDA_OK : KDA_ERR_HIP; }
+
+// Kernels use 16-byte vector accesses on records, workspace and states.
+bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
 }  // namespace
 
@@ -148,6 +152,7 @@ int kda_pack_state(const kda_config* cfg, const float* S, const uint8_t* bits, c
   if (st != KDA_OK) return st;
   if (cfg->state32) return KDA_ERR_ARG;
   if (!S || !bits || !s_hat || !r || !records) return KDA_ERR_ARG;
+  if (!aligned16(S) || !aligned16(records)) return KDA_ERR_ARG;
   KParams p = make_params(cfg, need);
   p.records = records;
   return hip_status(kda::launch_pack(p, S, bits, s_hat, r, tokens_seen, (hipStream_t)stream));
@@ -158,7 +163,7 @@ int kda_unpack_state(const kda_config* cfg, const void* records, float* S, uint8
   int need = 0;
   int st = check_cfg(cfg, &need);
   if (st != KDA_OK) return st;
-  if (!records) return KDA_ERR_ARG;
+  if (!records || !aligned16(records)) return KDA_ERR_ARG;
   if (cfg->state32 && (bits || s_hat || r)) return KDA_ERR_ARG;
   KParams p = make_params(cfg, need);
   p.records = const_cast<void*>(records);
@@ -173,6 +178,7 @@ int kda_step(const kda_config* cfg, void* records, const float* q, const float* 
   if (st != KDA_OK) return st;
   if (!records || !q || !k || !v || !s || !beta || !o) return KDA_ERR_ARG;
   if (!cfg->state32 && !ws) return KDA_ERR_WORKSPACE;
+  if (!aligned16(records) || (ws && !aligned16(ws))) return KDA_ERR_ARG;
   KParams p = make_params(cfg, need);
   p.records = records;
   p.q = q;

@@ -60,33 +60,32 @@ __device__ inline float f16_to_f32(uint16_t u) {
 // ----------------------------------------------------- wave primitives ---
 __device__ inline int lane_id() { return __lane_id(); }
 
-__device__ inline float wave_max(float v) {
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
-  return v;
+// DPP lane exchange within 16-lane rows (quad permutes and mirrors).
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
 
-template <typename T>
-__device__ inline T wave_sum(T v) {
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
-  return v;
+// Broadcast lane `l` of v to the wave (scalar register).
+__device__ inline int bcast_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ inline float bcast_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
 }
 
-template <typename T>
-__device__ inline T wave_min_t(T v) {
-  for (int o = 32; o >= 1; o >>= 1) {
-    T w = __shfl_xor(v, o, WAVE);
-    v = w < v ? w : v;
-  }
-  return v;
-}
-
-template <typename T>
-__device__ inline T wave_max_t(T v) {
-  for (int o = 32; o >= 1; o >>= 1) {
-    T w = __shfl_xor(v, o, WAVE);
-    v = w > v ? w : v;
-  }
-  return v;
+// Maximum over the 64 lanes of a wave, returned wave-uniform.  DPP steps
+// (xor 1, xor 2, half-row mirror, row mirror) leave every lane with its
+// 16-lane row maximum; the four row maxima are then read as scalars.
+__device__ inline float wave_max_uniform(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));    // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_f<0x4E>(v));    // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_f<0x141>(v));   // row_half_mirror
+  v = fmaxf(v, dpp_f<0x140>(v));   // row_mirror
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
 // inclusive prefix sum over the wave
@@ -99,16 +98,35 @@ __device__ inline int wave_incl_scan(int v) {
   return v;
 }
 
-// Block-wide reductions through a small shared scratch of one slot per wave.
-// Every thread of the block must call them; all receive the result.
-template <typename T, typename Op>
-__device__ inline T block_reduce(T v, T* scratch, Op op) {
+// DPP exchange for 32-bit integers.
+template <int CTRL>
+__device__ inline int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+
+// Wave-wide reduction of a 32-bit int, returned wave-uniform: four DPP steps
+// reduce within 16-lane rows, then the four row results are read as scalars.
+template <typename Op>
+__device__ inline int wave_reduce_i(int v, Op op) {
+  v = op(v, dpp_i<0xB1>(v));
+  v = op(v, dpp_i<0x4E>(v));
+  v = op(v, dpp_i<0x141>(v));
+  v = op(v, dpp_i<0x140>(v));
+  return op(op(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+            op(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
+
+// Block-wide reductions of a 32-bit int through a small shared scratch of one
+// slot per wave.  Every thread of the block must call them; all receive the
+// result.
+template <typename Op>
+__device__ inline int block_reduce(int v, int* scratch, Op op) {
   const int w = threadIdx.x / WAVE, nw = (blockDim.x + WAVE - 1) / WAVE;
-  for (int o = 32; o >= 1; o >>= 1) v = op(v, __shfl_xor(v, o, WAVE));
+  v = wave_reduce_i(v, op);
   __syncthreads();
   if (lane_id() == 0) scratch[w] = v;
   __syncthreads();
-  T r = scratch[0];
+  int r = scratch[0];
   for (int i = 1; i < nw; ++i) r = op(r, scratch[i]);
   return r;
 }

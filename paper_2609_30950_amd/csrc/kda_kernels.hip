@@ -105,37 +105,50 @@ __device__ void load_rows(RowSmem<DK>& rs, const float* q, const float* k, const
   }
 }
 
-// Decode one record into column-layout registers X[r][c] (row 32w + r,
-// column lane + 64c): x^ = fl32(code * Delta), or +-mu for one-bit rows.
+// Copy the meaningful code words of a record (ceil(sum b / 32) words per
+// column) into LDS with coalesced 16-byte loads.  All threads must call.
+template <int DV>
+__device__ void stage_words(const uint8_t* rec, const Layout& L, int total_bits, uint32_t* lds) {
+  const int nw = (total_bits + 31) >> 5;
+  const int n4 = nw * DV / 4;
+  const uint4* src = (const uint4*)(rec + L.codes_off);
+  uint4* dst = (uint4*)lds;
+  for (int e = threadIdx.x; e < n4; e += blockDim.x) dst[e] = src[e];
+  __syncthreads();
+}
+
+// Decode staged code words into column-layout registers X[r][c] (row
+// 32w + r, column lane + 64c): x^ = fl32(code * Delta), or +-mu for one-bit
+// rows.  Row offsets and widths are wave-uniform.
 template <int DK, int DV>
-__device__ void unpack_cols(const uint8_t* rec, const Layout& L, const MetaSmem<DK>& m,
+__device__ void unpack_cols(const uint32_t* words, const MetaSmem<DK>& m,
                             float (&X)[ROW_BLOCK][DV / WAVE]) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
-  const uint32_t* words = (const uint32_t*)(rec + L.codes_off);
+  // lane r holds row 32w + r's width, offset and scale; rows are broadcast.
+  // One expression covers every width: the field is sign-extended, then
+  // x^ = fma(code, mul, add) with (mul, add) = (Delta, 0) for b >= 2, which
+  // is fl32(code Delta), and (2 mu, mu) for one-bit rows (code 0 or -1),
+  // which gives mu or -mu exactly.
+  const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
+  const int vb = m.w[myrow], vP = m.P[myrow];
+  const float vsc = m.sc[myrow];
+  const float vmul = vb == 1 ? 2.0f * vsc : vsc;
+  const float vadd = vb == 1 ? vsc : 0.0f;
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    const int i = w * ROW_BLOCK + r;
-    const int b = m.w[i];
-    const int P = m.P[i];
+    const int b = bcast_i(vb, r);
+    const int P = bcast_i(vP, r);
+    const float mul = bcast_f(vmul, r), add = bcast_f(vadd, r);
     const int kw = P >> 5, sh = P & 31;
-    const bool two = sh + b > 32;
-    const float sc = m.sc[i];
-    const uint32_t mask = (b >= 32) ? 0xffffffffu : ((1u << b) - 1u);
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int col = lane + WAVE * c;
       const uint32_t lo = words[kw * DV + col];
-      const uint32_t hi = two ? words[(kw + 1) * DV + col] : 0u;
-      const uint32_t f = (uint32_t)((((uint64_t)hi << 32) | lo) >> sh) & mask;
-      float x;
-      if (b == 1) {
-        x = f ? -sc : sc;
-      } else {
-        const int code = ((int)(f << (32 - b))) >> (32 - b);
-        x = (float)code * sc;
-      }
-      X[r][c] = x;
+      const uint32_t hi = words[(kw + 1) * DV + col];   // staged; masked off unless straddling
+      const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
+      const int code = __builtin_amdgcn_sbfe((int)f, 0, b);
+      X[r][c] = __builtin_fmaf((float)code, mul, add);
     }
   }
 }
@@ -169,13 +182,14 @@ __device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>&
                             RecSmem<DK, DV>& sm, const float* v, float* o_out) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
+  const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
+  const float va = rs.a[myrow], vk = rs.k[myrow], vg = rs.g[myrow], vq = rs.q[myrow];
   float acc[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    const int i = w * ROW_BLOCK + r;
-    const float a = rs.a[i], kk = rs.k[i];
+    const float a = bcast_f(va, r), kk = bcast_f(vk, r);
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       X[r][c] = a * X[r][c];
@@ -195,8 +209,7 @@ __device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>&
   }
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    const int i = w * ROW_BLOCK + r;
-    const float g = rs.g[i], qq = rs.q[i];
+    const float g = bcast_f(vg, r), qq = bcast_f(vq, r);
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       X[r][c] = __builtin_fmaf(g, wv[c], X[r][c]);
@@ -225,111 +238,161 @@ __device__ void row_max(const float (&X)[ROW_BLOCK][DV / WAVE], float* R) {
     float mx = 0.f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) mx = fmaxf(mx, fabsf(X[r][c]));
-    mx = wave_max(mx);
+    mx = wave_max_uniform(mx);
     if (lane == 0) R[w * ROW_BLOCK + r] = mx;
   }
 }
 
 // ----------------------------------------------------- row-layout fit ---
 
-// Quantise rows held row-major in LDS (float S[DK][ld]) with widths b[] and
-// write int16 codes into C[DK][DV] (may alias S once every thread has loaded
-// its segment: an internal barrier separates the two) and FP16 scales.
-// Contract: see include/kda.h and the method description at the top.
+// Column stride (int16 elements) of the column-major code buffer: padded by
+// 8 so that the 16-byte reads of consecutive columns hit distinct LDS banks.
+template <int DK>
+constexpr int CT_LD = DK + 8;
+
+// Sum of the per-segment partials of one row held by SEGS adjacent lanes, in
+// the halving order (p[s] + p[s + SEGS/2] first), via DPP quad permutes.
+template <int SEGS>
+__device__ inline float seg_combine(float v) {
+  static_assert(SEGS == 1 || SEGS == 2 || SEGS == 4, "segments per row");
+  if constexpr (SEGS == 4) v = v + dpp_f<0x4E>(v);   // lanes differing in bit 1
+  if constexpr (SEGS >= 2) v = v + dpp_f<0xB1>(v);   // lanes differing in bit 0
+  return v;
+}
+
+// Order rows by width, widest first (ties by row index), so that each wave of
+// the fit holds rows of similar width and similar pruning depth.
+template <int DK>
+__device__ void width_order(const uint8_t* bits, uint8_t* perm) {
+  const int t = threadIdx.x;
+  if (t < DK) {
+    const int b = bits[t];
+    int pos = 0;
+    for (int u = 0; u < DK; ++u) {
+      const int bu = bits[u];
+      pos += (bu > b) || (bu == b && u < t);
+    }
+    perm[pos] = (uint8_t)t;
+  }
+  __syncthreads();
+}
+
+// Quantise the rows of a row-major float32 state S[DK][DV] (device memory)
+// with widths bits[] (method: see the top of this file and include/kda.h).
+// Thread t handles the 64-column segment t % (DV/64) of row
+// perm[t / (DV/64)].  Writes int16 codes column-major into Ct[DV][CT_LD]
+// (LDS) and FP16 scales.
+//
+// Exact pruning: candidates are scanned from f = 1 downwards.  For m with
+// n Delta_m <= R the row maximum is coded as +-n, so its squared residual
+// fl(e_max^2), e_max = fl(R - n Delta_m), is a lower bound of err_m (the error
+// is a float32 sum of non-negative terms that contains it), and e_max only
+// grows as m falls.  Once that bound exceeds the best error no smaller f can
+// reach the minimum, so the scan stops; the result equals the exhaustive
+// first strict minimum over all 16 candidates.
 template <int DK, int DV>
-__device__ void fit_rows(const float* S, int ld, const uint8_t* bits, const float (*phi)[N_FIT],
-                         int16_t* C, uint16_t* scale_out) {
+__device__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* perm,
+                         const float (*phi)[N_FIT], int16_t* Ct, uint16_t* scale_out) {
   constexpr int SEGS = DV / SEG;
   constexpr int ITEMS = DK * SEGS;
-  const int tid = threadIdx.x, nt = blockDim.x;
-  // codes overwrite S after the (single) load pass: one item per thread
+  const int tid = threadIdx.x;
   static_assert(ITEMS <= 2 * DK, "one fit item per thread");
-  // all threads run the same number of item iterations (barrier inside)
-  const int iters = (ITEMS + nt - 1) / nt;
-  for (int it = 0; it < iters; ++it) {
-    const int item = it * nt + tid;
-    const bool valid = item < ITEMS;
-    const int i = valid ? item / SEGS : 0;
-    const int sg = item % SEGS;
-    float x[SEG];
-    const float* src = S + (size_t)i * ld + sg * SEG;
+  const bool valid = tid < ITEMS;
+  const int i = valid ? perm[tid / SEGS] : 0;
+  const int sg = tid % SEGS;
+  float x[SEG];
+  const float4* src = (const float4*)(S + (size_t)i * DV + sg * SEG);
 #pragma unroll
-    for (int j = 0; j < SEG; ++j) x[j] = src[j];
-    __syncthreads();  // codes may overwrite S below
-    float mx = 0.f;
+  for (int q = 0; q < SEG / 4; ++q) {
+    const float4 v = src[q];
+    x[4 * q] = v.x;
+    x[4 * q + 1] = v.y;
+    x[4 * q + 2] = v.z;
+    x[4 * q + 3] = v.w;
+  }
+  float mx = 0.f;
 #pragma unroll
-    for (int j = 0; j < SEG; ++j) mx = fmaxf(mx, fabsf(x[j]));
+  for (int j = 0; j < SEG; ++j) mx = fmaxf(mx, fabsf(x[j]));
+  if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0xB1>(mx));
+  if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
+  const int b = bits[i];
+  int16_t* dst = Ct + (size_t)(sg * SEG) * CT_LD<DK> + i;
+  if (b == 1) {
+    float acc = 0.f;
 #pragma unroll
-    for (int o = 1; o < SEGS; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, WAVE));
-    const int b = bits[i];
-    int16_t* dst = C + (size_t)i * DV + sg * SEG;
-    if (b == 1) {
-      float acc = 0.f;
+    for (int j = 0; j < SEG; ++j) acc = acc + fabsf(x[j]);
+    // halving over segments: lanes differing in the top segment bit first
+    acc = seg_combine<SEGS>(acc);
+    const uint16_t mu = f32_to_f16_sat(acc * (1.0f / (float)DV));
+    if (valid) {
 #pragma unroll
-      for (int j = 0; j < SEG; ++j) acc = acc + fabsf(x[j]);
-      // halving over segments: lanes differing in the top segment bit first
-#pragma unroll
-      for (int o = SEGS >> 1; o >= 1; o >>= 1) acc = acc + __shfl_xor(acc, o, WAVE);
-      const uint16_t mu = f32_to_f16_sat(acc * (1.0f / (float)DV));
-      if (valid) {
-#pragma unroll
-        for (int j = 0; j < SEG; ++j) dst[j] = (int16_t)(x[j] < 0.f ? 1 : 0);
-        if (sg == 0) scale_out[i] = mu;
-      }
-    } else {
-      const float nf = (float)((1 << (b - 1)) - 1);
-      float best = __builtin_inff();
-      int mb = 0;
-      for (int m = 0; m < N_FIT; ++m) {
-        const float d = f16_to_f32(f32_to_f16_sat(mx * phi[b][m]));
-        const float inv = d > 0.f ? 1.0f / d : 0.f;
-        float err = 0.f;
-#pragma unroll
-        for (int j = 0; j < SEG; ++j) {
-          float c = __builtin_rintf(x[j] * inv);
-          c = fminf(fmaxf(c, -nf), nf);
-          const float e = __builtin_fmaf(-c, d, x[j]);
-          err = __builtin_fmaf(e, e, err);
-        }
-#pragma unroll
-        for (int o = SEGS >> 1; o >= 1; o >>= 1) err = err + __shfl_xor(err, o, WAVE);
-        if (err < best) { best = err; mb = m; }
-      }
-      const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
-      const float d = f16_to_f32(dh);
-      const float inv = d > 0.f ? 1.0f / d : 0.f;
-      if (valid) {
-#pragma unroll
-        for (int j = 0; j < SEG; ++j) {
-          float c = __builtin_rintf(x[j] * inv);
-          c = fminf(fmaxf(c, -nf), nf);
-          dst[j] = (int16_t)c;
-        }
-        if (sg == 0) scale_out[i] = dh;
-      }
+      for (int j = 0; j < SEG; ++j) dst[(size_t)j * CT_LD<DK>] = (int16_t)(x[j] < 0.f ? 1 : 0);
+      if (sg == 0) scale_out[i] = mu;
     }
-    __syncthreads();
+    return;
+  }
+  const float nf = (float)((1 << (b - 1)) - 1);
+  float best = __builtin_inff();
+  int mb = N_FIT - 1;
+  for (int m = N_FIT - 1; m >= 0; --m) {
+    const float d = f16_to_f32(f32_to_f16_sat(mx * phi[b][m]));
+    const float emax = __builtin_fmaf(-nf, d, mx);
+    if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
+    const float inv = d > 0.f ? 1.0f / d : 0.f;
+    float err = 0.f;
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) {
+      const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+      const float e = __builtin_fmaf(-c, d, x[j]);
+      err = __builtin_fmaf(e, e, err);
+    }
+    err = seg_combine<SEGS>(err);
+    if (err <= best) { best = err; mb = m; }
+  }
+  const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
+  const float d = f16_to_f32(dh);
+  const float inv = d > 0.f ? 1.0f / d : 0.f;
+  if (valid) {
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) {
+      const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+      dst[(size_t)j * CT_LD<DK>] = (int16_t)c;
+    }
+    if (sg == 0) scale_out[i] = dh;
   }
 }
 
-// Pack int16 codes C[DK][DV] with widths b[] into column bit streams (one
-// thread per column, rows in order).
+// Pack int16 codes Ct[DV][CT_LD] (column-major) with widths bits[] into column
+// bit streams: one thread per column, rows in order, widths wave-uniform.
 template <int DK, int DV>
-__device__ void pack_cols(const int16_t* C, const uint8_t* bits, uint32_t* words) {
-  const int tid = threadIdx.x;
+__device__ void pack_cols(const int16_t* Ct, const uint8_t* bits, uint32_t* words) {
+  const int tid = threadIdx.x, lane = lane_id();
+  constexpr int RPL = (DK + WAVE - 1) / WAVE;
+  int vb[RPL];
+#pragma unroll
+  for (int q = 0; q < RPL; ++q) vb[q] = (lane + WAVE * q < DK) ? bits[lane + WAVE * q] : 0;
   for (int col = tid; col < DV; col += blockDim.x) {
+    const int16_t* cc = Ct + (size_t)col * CT_LD<DK>;
     uint64_t acc = 0;
     int nb = 0, wi = 0;
-    for (int i = 0; i < DK; ++i) {
-      const int b = bits[i];
-      const uint32_t f = (uint32_t)(int)C[(size_t)i * DV + col] & ((b >= 32) ? 0xffffffffu : ((1u << b) - 1u));
-      acc |= (uint64_t)f << nb;
-      nb += b;
-      if (nb >= 32) {
-        words[wi * DV + col] = (uint32_t)acc;
-        ++wi;
-        acc >>= 32;
-        nb -= 32;
+#pragma unroll
+    for (int i0 = 0; i0 < DK; i0 += 8) {
+      const uint4 raw = *(const uint4*)(cc + i0);
+      const uint32_t pr[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u;
+        const int b = bcast_i(vb[i / WAVE], i % WAVE);
+        const uint32_t code = (pr[u >> 1] >> (16 * (u & 1))) & 0xffffu;
+        const uint32_t f = code & ((1u << b) - 1u);
+        acc |= (uint64_t)f << nb;
+        nb += b;
+        if (nb >= 32) {
+          words[wi * DV + col] = (uint32_t)acc;
+          ++wi;
+          acc >>= 32;
+          nb -= 32;
+        }
       }
     }
     if (nb > 0) words[wi * DV + col] = (uint32_t)acc;
@@ -406,10 +469,21 @@ __global__ void __launch_bounds__(2 * DK) k_stats(KParams p) {
   const float beta = p.beta[bh];
   load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
                 p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), beta, p.per_head);
-  __syncthreads();
+  extern __shared__ uint4 dyn_lds[];
+  uint32_t* words = (uint32_t*)dyn_lds;
+  stage_words<DV>(rec, L, meta.P[DK], words);
   float X[ROW_BLOCK][DV / WAVE];
-  unpack_cols<DK, DV>(rec, L, meta, X);
+  unpack_cols<DK, DV>(words, meta, X);
   recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, p.o + (size_t)bh * DV);
+  {
+    // float32 state after the token, row-major, for the requantisation pass
+    const int w = t / WAVE, lane = lane_id();
+    float* dstS = p.ws_s32 + (size_t)bh * DK * DV;
+#pragma unroll
+    for (int r = 0; r < ROW_BLOCK; ++r)
+#pragma unroll
+      for (int c = 0; c < DV / WAVE; ++c) dstS[(w * ROW_BLOCK + r) * DV + lane + WAVE * c] = X[r][c];
+  }
   row_max<DK, DV>(X, st.R);
   // EMA of the rates (first token of a fresh state initialises)
   double m_run = 0.0, e_run = 0.0;
@@ -446,24 +520,19 @@ __global__ void __launch_bounds__(1024) k_alloc(const double* c, int N, int need
                  bits + (size_t)blockIdx.x * N, sm);
 }
 
-// Recompute the token from the record, fit, quantise and pack in place.
+// Quantise the float32 state the stats pass left in the workspace with the
+// allocated widths and pack it into the record in place.
 template <int DK, int DV>
 __global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
   const int bh = blockIdx.x;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
-  __shared__ MetaSmem<DK> meta;
-  __shared__ RowSmem<DK> rs;
-  __shared__ RecSmem<DK, DV> rsm;
-  __shared__ float Sx[DK * (DV + 4)];
-  __shared__ uint8_t nb[DK];
+  __shared__ __align__(16) int16_t Ct[DV * CT_LD<DK>];
+  __shared__ uint8_t nb[DK], perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
   const int t = threadIdx.x;
-  load_meta<DK>(rec, L, p.bmax, meta);
-  const float beta = p.beta[bh];
-  load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
-                p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), beta, p.per_head);
+  const unsigned ntok = *(const unsigned*)rec;
   if (t < DK) {
     nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
     const uint32_t zr = p.ws_zr[(size_t)bh * DK + t];
@@ -472,24 +541,11 @@ __global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
   }
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
-  float X[ROW_BLOCK][DV / WAVE];
-  unpack_cols<DK, DV>(rec, L, meta, X);
-  recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, nullptr);
-  // transpose to row layout
-  {
-    constexpr int CPL = DV / WAVE;
-    const int w = t / WAVE, lane = lane_id();
-#pragma unroll
-    for (int r = 0; r < ROW_BLOCK; ++r)
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) Sx[(w * ROW_BLOCK + r) * (DV + 4) + lane + WAVE * c] = X[r][c];
-  }
+  width_order<DK>(nb, perm);
+  fit_rows<DK, DV>(p.ws_s32 + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
   __syncthreads();
-  int16_t* C = (int16_t*)Sx;
-  fit_rows<DK, DV>(Sx, DV + 4, nb, phi, C, sc16);
-  __syncthreads();
-  pack_cols<DK, DV>(C, nb, (uint32_t*)(rec + L.codes_off));
-  store_meta<DK>(rec, L, meta.ntok + 1u, nb, sc16, zz, rr);
+  pack_cols<DK, DV>(Ct, nb, (uint32_t*)(rec + L.codes_off));
+  store_meta<DK>(rec, L, ntok + 1u, nb, sc16, zz, rr);
 }
 
 // Unquantised ("32-bit") state: load, one token, store.
@@ -524,13 +580,11 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   const int bh = blockIdx.x;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)p.records + L.slot * (long long)bh;
-  __shared__ float Sx[DK * (DV + 4)];
-  __shared__ uint8_t nb[DK];
+  __shared__ __align__(16) int16_t Ct[DV * CT_LD<DK>];
+  __shared__ uint8_t nb[DK], perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
   const int t = threadIdx.x;
-  const float* src = S + (size_t)bh * DK * DV;
-  for (int e = t; e < DK * DV; e += blockDim.x) Sx[(e / DV) * (DV + 4) + e % DV] = src[e];
   if (t < DK) {
     nb[t] = (uint8_t)min(max((int)bits[(size_t)bh * DK + t], 1), p.bmax);
     zz[t] = logq_encode(s_hat[(size_t)bh * DK + t]);
@@ -538,10 +592,10 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   }
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
-  int16_t* C = (int16_t*)Sx;
-  fit_rows<DK, DV>(Sx, DV + 4, nb, phi, C, sc16);
+  width_order<DK>(nb, perm);
+  fit_rows<DK, DV>(S + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
   __syncthreads();
-  pack_cols<DK, DV>(C, nb, (uint32_t*)(rec + L.codes_off));
+  pack_cols<DK, DV>(Ct, nb, (uint32_t*)(rec + L.codes_off));
   store_meta<DK>(rec, L, ntok, nb, sc16, zz, rr);
 }
 
@@ -563,9 +617,11 @@ __global__ void __launch_bounds__(2 * DK) k_unpack(KParams p, float* S, uint8_t*
   const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
   __shared__ MetaSmem<DK> meta;
   load_meta<DK>(rec, L, p.bmax, meta);
+  extern __shared__ uint4 dyn_lds[];
+  stage_words<DV>(rec, L, meta.P[DK], (uint32_t*)dyn_lds);
   if (S) {
     float X[ROW_BLOCK][CPL];
-    unpack_cols<DK, DV>(rec, L, meta, X);
+    unpack_cols<DK, DV>((const uint32_t*)dyn_lds, meta, X);
 #pragma unroll
     for (int rr_ = 0; rr_ < ROW_BLOCK; ++rr_)
 #pragma unroll
@@ -642,10 +698,11 @@ static hipError_t launch_step_t(const KParams& p, hipStream_t st) {
   hipError_t e;
   {
     ProfScope ps("stats", st);
+    const size_t dyn = (size_t)(p.L.wc + 1) * DV * 4;
     if (p.scope == 1)
-      k_stats<DK, DV, true><<<nbh, 2 * DK, 0, st>>>(p);
+      k_stats<DK, DV, true><<<nbh, 2 * DK, dyn, st>>>(p);
     else
-      k_stats<DK, DV, false><<<nbh, 2 * DK, 0, st>>>(p);
+      k_stats<DK, DV, false><<<nbh, 2 * DK, dyn, st>>>(p);
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
@@ -683,10 +740,11 @@ hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, co
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,
                          hipStream_t st) {
   ProfScope ps("unpack", st);
+  const size_t dyn = p.state32 ? 0 : (size_t)(p.L.wc + 1) * p.dv * 4;
   if (p.dk == 64)
-    k_unpack<64, 64><<<p.B * p.H, 128, 0, st>>>(p, S, bits, s_hat, r);
+    k_unpack<64, 64><<<p.B * p.H, 128, dyn, st>>>(p, S, bits, s_hat, r);
   else
-    k_unpack<128, 128><<<p.B * p.H, 256, 0, st>>>(p, S, bits, s_hat, r);
+    k_unpack<128, 128><<<p.B * p.H, 256, dyn, st>>>(p, S, bits, s_hat, r);
   return hipGetLastError();
 }
 

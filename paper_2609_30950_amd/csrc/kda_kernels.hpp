@@ -24,6 +24,7 @@ struct KParams {
   double* ws_c;
   uint32_t* ws_zr;
   uint8_t* ws_bits;
+  float* ws_s32;            // float32 state after the token, [B][H][dk][dv]
 };
 
 hipError_t launch_step(const KParams& p, hipStream_t st);

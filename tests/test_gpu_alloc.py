@@ -73,3 +73,40 @@ def test_window_weights_match_oracle(C):
     want = stats.window_gamma(np.moveaxis(x["q"], 1, 0), np.moveaxis(x["s"], 1, 0),
                               np.moveaxis(x["k"], 1, 0), np.moveaxis(x["beta"], 1, 0), C)
     np.testing.assert_allclose(host(g).reshape(2, 3, 64), want, rtol=1e-12)
+
+
+def _weights_case(kind, rng, B, H, d):
+    gamma = np.exp(rng.normal(0, 3, (B, H, d)))
+    R = np.abs(rng.standard_normal((B, H, d))).astype(np.float32)
+    if kind == "all_equal":                  # one bucket, identical keys everywhere
+        gamma[:] = 0.37
+        R[:] = 1.0
+    elif kind == "few_values":               # many exact ties between rows
+        gamma = np.choose(rng.integers(0, 3, (B, H, d)), [0.5, 1.0, 2.0]).astype(np.float64)
+        R[:] = np.choose(rng.integers(0, 2, (B, H, d)), [1.0, 2.0]).astype(np.float32)
+    elif kind == "powers_of_two":            # fraction bits all zero
+        gamma = np.exp2(rng.integers(-20, 20, (B, H, d))).astype(np.float64)
+        R[:] = 1.0
+    elif kind == "wide_range":
+        gamma = np.exp(rng.uniform(-600, 600, (B, H, d)))
+    elif kind == "near_ties":                # keys differing in the last fraction bits
+        base = 1.2345678
+        gamma = base * (1 + rng.integers(0, 8, (B, H, d)) * 2.0 ** -50)
+        R[:] = 1.0
+    return gamma, R
+
+
+@pytest.mark.parametrize("kind", ["all_equal", "few_values", "powers_of_two", "wide_range",
+                                  "near_ties"])
+@pytest.mark.parametrize("mean", [2.5, 4.0, 6.25])
+def test_alloc_ties_and_ranges(kind, mean):
+    B, H, d = 2, 32, 128
+    rng = np.random.default_rng(hash((kind, mean)) % 2 ** 32)
+    gamma, R = _weights_case(kind, rng, B, H, d)
+    say("alloc ties", kind, mean)
+    cfg = K.Config(B=B, H=H, d_k=d, d_v=d, group_rows=64, scope=0, mean_bits=mean, b_min=2, b_max=8)
+    bits = torch.zeros(B * H * d, dtype=torch.uint8, device="cuda")
+    K.kda_alloc_bits(cfg, dev(gamma), dev(R), bits, K.new_workspace(cfg))
+    got = host(bits).reshape(B, H, d).astype(np.int64)
+    want = _oracle_bits(gamma, R, 64, 0, mean, 2, 8)
+    assert np.array_equal(got, want), f"{kind}: {np.sum(got != want)} widths differ"

@@ -39,7 +39,8 @@ def _ptr(t, dtype=None, numel=None, name="tensor"):
         raise KdaError(f"{name}: expected a device tensor")
     if not t.is_contiguous():
         raise KdaError(f"{name}: expected a contiguous tensor")
-    if dtype is not None and t.dtype != dtype:
+    dtypes = dtype if isinstance(dtype, tuple) else (dtype,)
+    if dtype is not None and t.dtype not in dtypes:
         raise KdaError(f"{name}: expected {dtype}, got {t.dtype}")
     if numel is not None and t.numel() != numel:
         raise KdaError(f"{name}: expected {numel} elements, got {t.numel()}")
@@ -127,14 +128,17 @@ def kda_step(cfg, records, q, k, v, s, beta, o, ws, gamma=None):
         _stream()))
 
 
+_BF16 = (torch.bfloat16, torch.int16)   # bf16 values or their raw bit patterns
+
+
 def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None):
     n_s = cfg.B * T * cfg.H * (1 if cfg.decay_per_head else cfg.d_k)
     n_qk = cfg.B * T * cfg.H * cfg.d_k
     _check(load().kda_prefill(
         ctypes.byref(cfg.c()), int(T), int(C),
         _ptr(records, torch.uint8, cfg.B * cfg.H * record_bytes(cfg), "records"),
-        _ptr(q, torch.int16, n_qk, "q"), _ptr(k, torch.int16, n_qk, "k"),
-        _ptr(v, torch.int16, cfg.B * T * cfg.H * cfg.d_v, "v"), _ptr(s, torch.float32, n_s, "s"),
+        _ptr(q, _BF16, n_qk, "q"), _ptr(k, _BF16, n_qk, "k"),
+        _ptr(v, _BF16, cfg.B * T * cfg.H * cfg.d_v, "v"), _ptr(s, torch.float32, n_s, "s"),
         _ptr(beta, torch.float32, cfg.B * T * cfg.H, "beta"),
         _ptr(gamma, torch.float64, _rows(cfg), "gamma"),
         _ptr(o, torch.float32, cfg.B * T * cfg.H * cfg.d_v, "o"), _ptr(ws, torch.uint8, None, "ws"),

@@ -188,6 +188,10 @@ int kda_step(const kda_config* cfg, void* records, const float* q, const float* 
   p.beta = beta;
   p.gamma = gamma;
   p.o = o;
+  p.T = 1;
+  p.tok0 = 0;
+  p.ntk = 1;
+  p.in_bf16 = 0;
   if (!cfg->state32) set_ws(p, cfg, ws);
   return hip_status(kda::launch_step(p, (hipStream_t)stream));
 }
@@ -200,10 +204,21 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, cons
   if (st != KDA_OK) return st;
   if (T < 1 || C < 1) return KDA_ERR_ARG;
   if (!records || !q || !k || !v || !s || !beta || !o) return KDA_ERR_ARG;
-  if (!ws) return KDA_ERR_WORKSPACE;
-  (void)gamma;
-  (void)stream;
-  return KDA_ERR_UNSUPPORTED;
+  if (!cfg->state32 && !ws) return KDA_ERR_WORKSPACE;
+  if (!aligned16(records) || (ws && !aligned16(ws))) return KDA_ERR_ARG;
+  KParams p = make_params(cfg, need);
+  p.records = records;
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.s = s;
+  p.beta = beta;
+  p.gamma = gamma;
+  p.o = o;
+  p.T = T;
+  p.in_bf16 = 1;
+  if (!cfg->state32) set_ws(p, cfg, ws);
+  return hip_status(kda::launch_prefill(p, C, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -91,16 +91,24 @@ struct RowSmem {
   float g[DK];   // fl32(beta * k)
 };
 
+__device__ inline float in_f32(const void* base, size_t idx, bool bf16) {
+  if (bf16) return __builtin_bit_cast(float, (uint32_t)((const uint16_t*)base)[idx] << 16);
+  return ((const float*)base)[idx];
+}
+
+// Per-row scalars of token `tok` of head bh into LDS (threads t < DK).
 template <int DK>
-__device__ void load_rows(RowSmem<DK>& rs, const float* q, const float* k, const float* s,
-                          float beta, bool per_head) {
+__device__ void load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
   const int t = threadIdx.x;
   if (t < DK) {
-    const float sv = per_head ? s[0] : s[t];
+    const int b = bh / p.H, h = bh % p.H;
+    const size_t th = ((size_t)b * p.T + tok) * p.H + h;       // (b, tok, h)
+    const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
+    const float beta = p.beta[th];
     rs.a[t] = (float)exp(-(double)sv);
-    const float kv = k[t];
+    const float kv = in_f32(p.k, th * DK + t, p.in_bf16);
     rs.k[t] = kv;
-    rs.q[t] = q[t];
+    rs.q[t] = in_f32(p.q, th * DK + t, p.in_bf16);
     rs.g[t] = beta * kv;
   }
 }
@@ -179,7 +187,8 @@ __device__ inline float combine_col(const float (&P)[DK / ROW_BLOCK][DV], int co
 // o = S^T q.  Writes o to o_out (if non-null).  All threads must call.
 template <int DK, int DV>
 __device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
-                            RecSmem<DK, DV>& sm, const float* v, float* o_out) {
+                            RecSmem<DK, DV>& sm, const void* v, size_t v_off, bool v_bf16,
+                            float* o_out) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
   const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
@@ -204,7 +213,7 @@ __device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>&
   for (int c = 0; c < CPL; ++c) {
     const int col = lane + WAVE * c;
     const float u = combine_col<DK, DV>(sm.up, col);
-    wv[c] = v[col] - u;
+    wv[c] = in_f32(v, v_off + col, v_bf16) - u;
     acc[c] = 0.f;
   }
 #pragma unroll
@@ -455,10 +464,15 @@ __device__ void row_weights(const KParams& p, int bh, const MetaSmem<DK>& meta,
   __syncthreads();
 }
 
+// Tokens [tok0, tok0 + ntk) of one head with the state resident in registers,
+// starting from the record: outputs o for every token, the float32 state after
+// the last token (to the workspace), row ranges and EMA rates, weights c and,
+// for the per-head scope, the widths.  Decode is the one-token case.
 template <int DK, int DV, bool HEAD>
-__global__ void __launch_bounds__(2 * DK) k_stats(KParams p) {
+__global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   const int bh = blockIdx.x;
   const int t = threadIdx.x;
+  const int b = bh / p.H, h = bh % p.H;
   const Layout L = p.L;
   const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
   __shared__ MetaSmem<DK> meta;
@@ -466,17 +480,41 @@ __global__ void __launch_bounds__(2 * DK) k_stats(KParams p) {
   __shared__ RecSmem<DK, DV> rsm;
   __shared__ StatSmem<DK> st;
   load_meta<DK>(rec, L, p.bmax, meta);
-  const float beta = p.beta[bh];
-  load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
-                p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), beta, p.per_head);
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
   stage_words<DV>(rec, L, meta.P[DK], words);
   float X[ROW_BLOCK][DV / WAVE];
   unpack_cols<DK, DV>(words, meta, X);
-  recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, p.o + (size_t)bh * DV);
+  // EMA states of row t (threads t < DK): from the record, or fresh
+  bool fresh = meta.ntok == 0;
+  double m_run = 0.0, e_run = 0.0;
+  if (t < DK && !fresh) {
+    m_run = exp(-2.0 * logq_decode(meta.z[t]));
+    e_run = 2.0 * (double)f16_to_f32(meta.r16[t]);
+  }
+  for (int j = 0; j < p.ntk; ++j) {
+    const int tok = p.tok0 + j;
+    load_rows<DK>(rs, p, bh, tok);
+    __syncthreads();
+    const size_t th = ((size_t)b * p.T + tok) * p.H + h;
+    recur_token<DK, DV>(X, rs, rsm, p.v, th * DV, p.in_bf16, p.o + th * DV);
+    if (t < DK) {
+      const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
+      const float kv = in_f32(p.k, th * DK + t, p.in_bf16);
+      const float beta = p.beta[th];
+      const double zs = decay_sample(sv), ys = erase_sample(kv, beta);
+      if (fresh) {
+        m_run = zs;
+        e_run = ys;
+      } else {
+        m_run = p.one_minus_alpha * m_run + p.alpha * zs;
+        e_run = p.one_minus_alpha * e_run + p.alpha * ys;
+      }
+    }
+    fresh = false;
+  }
   {
-    // float32 state after the token, row-major, for the requantisation pass
+    // float32 state after the last token, row-major, for the requantisation
     const int w = t / WAVE, lane = lane_id();
     float* dstS = p.ws_s32 + (size_t)bh * DK * DV;
 #pragma unroll
@@ -485,22 +523,6 @@ __global__ void __launch_bounds__(2 * DK) k_stats(KParams p) {
       for (int c = 0; c < DV / WAVE; ++c) dstS[(w * ROW_BLOCK + r) * DV + lane + WAVE * c] = X[r][c];
   }
   row_max<DK, DV>(X, st.R);
-  // EMA of the rates (first token of a fresh state initialises)
-  double m_run = 0.0, e_run = 0.0;
-  if (t < DK) {
-    const float sv = p.per_head ? p.s[bh] : p.s[(size_t)bh * DK + t];
-    const float kv = p.k[(size_t)bh * DK + t];
-    const double zs = decay_sample(sv), ys = erase_sample(kv, beta);
-    if (meta.ntok == 0) {
-      m_run = zs;
-      e_run = ys;
-    } else {
-      const double m0 = exp(-2.0 * logq_decode(meta.z[t]));
-      const double e0 = 2.0 * (double)f16_to_f32(meta.r16[t]);
-      m_run = p.one_minus_alpha * m0 + p.alpha * zs;
-      e_run = p.one_minus_alpha * e0 + p.alpha * ys;
-    }
-  }
   __syncthreads();
   row_weights<DK>(p, bh, meta, st, m_run, e_run, t);
   if constexpr (HEAD) {
@@ -545,7 +567,7 @@ __global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
   fit_rows<DK, DV>(p.ws_s32 + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
   __syncthreads();
   pack_cols<DK, DV>(Ct, nb, (uint32_t*)(rec + L.codes_off));
-  store_meta<DK>(rec, L, ntok + 1u, nb, sc16, zz, rr);
+  store_meta<DK>(rec, L, ntok + (unsigned)p.ntk, nb, sc16, zz, rr);
 }
 
 // Unquantised ("32-bit") state: load, one token, store.
@@ -553,19 +575,23 @@ template <int DK, int DV>
 __global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
   constexpr int CPL = DV / WAVE;
   const int bh = blockIdx.x;
+  const int b = bh / p.H, h = bh % p.H;
   const int w = threadIdx.x / WAVE, lane = lane_id();
   float* S = (float*)((uint8_t*)p.records + (long long)bh * DK * DV * 4);
   __shared__ RowSmem<DK> rs;
   __shared__ RecSmem<DK, DV> rsm;
-  load_rows<DK>(rs, p.q + (size_t)bh * DK, p.k + (size_t)bh * DK,
-                p.s + (p.per_head ? (size_t)bh : (size_t)bh * DK), p.beta[bh], p.per_head);
   float X[ROW_BLOCK][CPL];
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r)
 #pragma unroll
     for (int c = 0; c < CPL; ++c) X[r][c] = S[(w * ROW_BLOCK + r) * DV + lane + WAVE * c];
-  __syncthreads();
-  recur_token<DK, DV>(X, rs, rsm, p.v + (size_t)bh * DV, p.o + (size_t)bh * DV);
+  for (int j = 0; j < p.ntk; ++j) {
+    const int tok = p.tok0 + j;
+    load_rows<DK>(rs, p, bh, tok);
+    __syncthreads();
+    const size_t th = ((size_t)b * p.T + tok) * p.H + h;
+    recur_token<DK, DV>(X, rs, rsm, p.v, th * DV, p.in_bf16, p.o + th * DV);
+  }
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r)
 #pragma unroll
@@ -687,8 +713,9 @@ __global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head
 
 // ------------------------------------------------------- launchers ---
 
+// One write-back interval: tokens [p.tok0, p.tok0 + p.ntk), then quantise.
 template <int DK, int DV>
-static hipError_t launch_step_t(const KParams& p, hipStream_t st) {
+static hipError_t launch_interval_t(const KParams& p, hipStream_t st) {
   const int nbh = p.B * p.H;
   if (p.state32) {
     ProfScope ps("step32", st);
@@ -700,9 +727,9 @@ static hipError_t launch_step_t(const KParams& p, hipStream_t st) {
     ProfScope ps("stats", st);
     const size_t dyn = (size_t)(p.L.wc + 1) * DV * 4;
     if (p.scope == 1)
-      k_stats<DK, DV, true><<<nbh, 2 * DK, dyn, st>>>(p);
+      k_chunk<DK, DV, true><<<nbh, 2 * DK, dyn, st>>>(p);
     else
-      k_stats<DK, DV, false><<<nbh, 2 * DK, dyn, st>>>(p);
+      k_chunk<DK, DV, false><<<nbh, 2 * DK, dyn, st>>>(p);
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
@@ -717,9 +744,26 @@ static hipError_t launch_step_t(const KParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_step(const KParams& p, hipStream_t st) {
-  if (p.dk == 64) return launch_step_t<64, 64>(p, st);
-  return launch_step_t<128, 128>(p, st);
+static hipError_t launch_interval(const KParams& p, hipStream_t st) {
+  if (p.dk == 64) return launch_interval_t<64, 64>(p, st);
+  return launch_interval_t<128, 128>(p, st);
+}
+
+hipError_t launch_step(const KParams& p, hipStream_t st) { return launch_interval(p, st); }
+
+hipError_t launch_prefill(KParams p, int C, hipStream_t st) {
+  if (p.state32) {
+    p.tok0 = 0;
+    p.ntk = p.T;
+    return launch_interval(p, st);
+  }
+  for (int t0 = 0; t0 < p.T; t0 += C) {
+    p.tok0 = t0;
+    p.ntk = (p.T - t0) < C ? (p.T - t0) : C;
+    hipError_t e = launch_interval(p, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <int DK, int DV>

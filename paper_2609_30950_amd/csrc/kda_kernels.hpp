@@ -15,9 +15,14 @@ struct KParams {
   double alpha, one_minus_alpha;
   Layout L;
   float phi[MAX_B + 1][N_FIT];   // fl32((5 + m) / (20 n_b)), n_b = 2^(b-1) - 1
-  // tensors (device)
+  // tensors (device).  Token inputs are [B][T][H][.] with T = 1 for decode;
+  // q/k/v are float32 (decode) or bf16 bit patterns (prefill).
   void* records;
-  const float *q, *k, *v, *s, *beta;
+  const void *q, *k, *v;
+  const float *s, *beta;
+  int T;                    // tokens in the input arrays
+  int tok0, ntk;            // chunk: tokens [tok0, tok0 + ntk)
+  int in_bf16;              // q/k/v element type
   const double* gamma;
   float* o;
   // workspace views
@@ -28,6 +33,7 @@ struct KParams {
 };
 
 hipError_t launch_step(const KParams& p, hipStream_t st);
+hipError_t launch_prefill(KParams p, int C, hipStream_t st);
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st);
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,

@@ -41,7 +41,7 @@ struct AllocSmem {
   unsigned char extra[ALLOC_MAX_N];
 };
 
-__device__ inline int slots_ge(int E, int beta, int bmin, int L) {
+__device__ __forceinline__ int slots_ge(int E, int beta, int bmin, int L) {
   if (E == E_ZERO) return 0;
   const int lmax = (E - beta) >> 1;  // floor division
   const int c = lmax - bmin;
@@ -49,7 +49,7 @@ __device__ inline int slots_ge(int E, int beta, int bmin, int L) {
 }
 
 // Block-wide exclusive scan of one int per thread (row order = thread order).
-__device__ inline int block_excl_scan(int v, int* scratch, int* total) {
+__device__ __forceinline__ int block_excl_scan(int v, int* scratch, int* total) {
   const int w = threadIdx.x / WAVE, nw = (blockDim.x + WAVE - 1) / WAVE;
   const int incl = wave_incl_scan(v);
   __syncthreads();
@@ -66,7 +66,7 @@ __device__ inline int block_excl_scan(int v, int* scratch, int* total) {
 
 // c_at(n): weight of row n (any address space); out: N widths.
 template <typename Load>
-__device__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax, uint8_t* out,
+__device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax, uint8_t* out,
                                AllocSmem& sm) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id();
   const int L = bmax - bmin;

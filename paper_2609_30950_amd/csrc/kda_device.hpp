@@ -45,7 +45,7 @@ __host__ __device__ inline Layout make_layout(int dk, int dv, int bmax) {
 // preceding float multiply with this conversion into v_fma_mix*_f16, which
 // rounds the exact product to FP16 once instead of rounding it to float32
 // first, and so differs on FP16 midpoints.
-__device__ inline uint16_t f32_to_f16_sat(float x) {
+__device__ __forceinline__ uint16_t f32_to_f16_sat(float x) {
   asm volatile("" : "+v"(x));
   _Float16 h = (_Float16)x;
   uint16_t u = __builtin_bit_cast(uint16_t, h);
@@ -53,30 +53,30 @@ __device__ inline uint16_t f32_to_f16_sat(float x) {
   return u;
 }
 
-__device__ inline float f16_to_f32(uint16_t u) {
+__device__ __forceinline__ float f16_to_f32(uint16_t u) {
   return (float)__builtin_bit_cast(_Float16, u);
 }
 
 // ----------------------------------------------------- wave primitives ---
-__device__ inline int lane_id() { return __lane_id(); }
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 // DPP lane exchange within 16-lane rows (quad permutes and mirrors).
 template <int CTRL>
-__device__ inline float dpp_f(float v) {
+__device__ __forceinline__ float dpp_f(float v) {
   return __builtin_bit_cast(
       float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
 
 // Broadcast lane `l` of v to the wave (scalar register).
-__device__ inline int bcast_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ inline float bcast_f(float v, int l) {
+__device__ __forceinline__ int bcast_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ float bcast_f(float v, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
 }
 
 // Maximum over the 64 lanes of a wave, returned wave-uniform.  DPP steps
 // (xor 1, xor 2, half-row mirror, row mirror) leave every lane with its
 // 16-lane row maximum; the four row maxima are then read as scalars.
-__device__ inline float wave_max_uniform(float v) {
+__device__ __forceinline__ float wave_max_uniform(float v) {
   v = fmaxf(v, dpp_f<0xB1>(v));    // quad_perm [1,0,3,2]
   v = fmaxf(v, dpp_f<0x4E>(v));    // quad_perm [2,3,0,1]
   v = fmaxf(v, dpp_f<0x141>(v));   // row_half_mirror
@@ -89,7 +89,7 @@ __device__ inline float wave_max_uniform(float v) {
 }
 
 // inclusive prefix sum over the wave
-__device__ inline int wave_incl_scan(int v) {
+__device__ __forceinline__ int wave_incl_scan(int v) {
   const int l = lane_id();
   for (int o = 1; o < WAVE; o <<= 1) {
     int w = __shfl_up(v, o, WAVE);
@@ -100,14 +100,14 @@ __device__ inline int wave_incl_scan(int v) {
 
 // DPP exchange for 32-bit integers.
 template <int CTRL>
-__device__ inline int dpp_i(int v) {
+__device__ __forceinline__ int dpp_i(int v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
 }
 
 // Wave-wide reduction of a 32-bit int, returned wave-uniform: four DPP steps
 // reduce within 16-lane rows, then the four row results are read as scalars.
 template <typename Op>
-__device__ inline int wave_reduce_i(int v, Op op) {
+__device__ __forceinline__ int wave_reduce_i(int v, Op op) {
   v = op(v, dpp_i<0xB1>(v));
   v = op(v, dpp_i<0x4E>(v));
   v = op(v, dpp_i<0x141>(v));
@@ -120,7 +120,7 @@ __device__ inline int wave_reduce_i(int v, Op op) {
 // slot per wave.  Every thread of the block must call them; all receive the
 // result.
 template <typename Op>
-__device__ inline int block_reduce(int v, int* scratch, Op op) {
+__device__ __forceinline__ int block_reduce(int v, int* scratch, Op op) {
   const int w = threadIdx.x / WAVE, nw = (blockDim.x + WAVE - 1) / WAVE;
   v = wave_reduce_i(v, op);
   __syncthreads();
@@ -137,14 +137,14 @@ constexpr double LOGQ_LO = -20.0;
 constexpr double LOGQ_HI = 5.0;
 constexpr double LOGQ_LEVELS = 65535.0;
 
-__device__ inline double decay_sample(float s) { return exp(-2.0 * (double)s); }
+__device__ __forceinline__ double decay_sample(float s) { return exp(-2.0 * (double)s); }
 
-__device__ inline double erase_sample(float k, float beta) {
+__device__ __forceinline__ double erase_sample(float k, float beta) {
   const double b = (double)beta, kk = (double)k;
   return (b * (2.0 - b)) * (kk * kk);
 }
 
-__device__ inline uint16_t logq_encode(double s_hat) {
+__device__ __forceinline__ uint16_t logq_encode(double s_hat) {
   if (!(s_hat > 0.0)) return 0;
   const double inv_step = LOGQ_LEVELS / (LOGQ_HI - LOGQ_LO);
   double u = (log2(s_hat) - LOGQ_LO) * inv_step;
@@ -154,14 +154,14 @@ __device__ inline uint16_t logq_encode(double s_hat) {
   return (uint16_t)u;
 }
 
-__device__ inline double logq_decode(uint16_t z) {
+__device__ __forceinline__ double logq_decode(uint16_t z) {
   const double step = (LOGQ_HI - LOGQ_LO) / LOGQ_LEVELS;
   return exp2((double)z * step + LOGQ_LO);
 }
 
-__device__ inline uint16_t r_encode(double r) { return f32_to_f16_sat((float)r); }
+__device__ __forceinline__ uint16_t r_encode(double r) { return f32_to_f16_sat((float)r); }
 
-__device__ inline double gamma_hat(double s_hat, double r) {
+__device__ __forceinline__ double gamma_hat(double s_hat, double r) {
   double t = s_hat + r;
   t = t < 1e-12 ? 1e-12 : t;
   return 1.0 / expm1(2.0 * t);

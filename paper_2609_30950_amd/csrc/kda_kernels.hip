@@ -28,7 +28,7 @@ namespace kda {
 
 // ------------------------------------------------------------ helpers ---
 
-__device__ inline const uint8_t* slot_ptr(const void* recs, long long slot, int bh) {
+__device__ __forceinline__ const uint8_t* slot_ptr(const void* recs, long long slot, int bh) {
   return (const uint8_t*)recs + slot * (long long)bh;
 }
 
@@ -46,7 +46,7 @@ struct MetaSmem {
 // Widths above b_max (never written by this library) are clamped so that a
 // damaged record cannot address code words outside its slot.
 template <int DK>
-__device__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
+__device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
   const int tid = threadIdx.x;
   if (tid < DK / 2) {
     const uint8_t byte = rec[L.w_off + tid];
@@ -91,14 +91,15 @@ struct RowSmem {
   float g[DK];   // fl32(beta * k)
 };
 
-__device__ inline float in_f32(const void* base, size_t idx, bool bf16) {
-  if (bf16) return __builtin_bit_cast(float, (uint32_t)((const uint16_t*)base)[idx] << 16);
+template <bool BF16>
+__device__ __forceinline__ float in_f32(const void* base, size_t idx) {
+  if constexpr (BF16) return __builtin_bit_cast(float, (uint32_t)((const uint16_t*)base)[idx] << 16);
   return ((const float*)base)[idx];
 }
 
 // Per-row scalars of token `tok` of head bh into LDS (threads t < DK).
-template <int DK>
-__device__ void load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
+template <int DK, bool BF16>
+__device__ __forceinline__ void load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
   const int t = threadIdx.x;
   if (t < DK) {
     const int b = bh / p.H, h = bh % p.H;
@@ -106,30 +107,30 @@ __device__ void load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
     const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
     const float beta = p.beta[th];
     rs.a[t] = (float)exp(-(double)sv);
-    const float kv = in_f32(p.k, th * DK + t, p.in_bf16);
+    const float kv = in_f32<BF16>(p.k, th * DK + t);
     rs.k[t] = kv;
-    rs.q[t] = in_f32(p.q, th * DK + t, p.in_bf16);
+    rs.q[t] = in_f32<BF16>(p.q, th * DK + t);
     rs.g[t] = beta * kv;
   }
 }
 
 // Copy the meaningful code words of a record (ceil(sum b / 32) words per
 // column) into LDS with coalesced 16-byte loads.  All threads must call.
-template <int DV>
-__device__ void stage_words(const uint8_t* rec, const Layout& L, int total_bits, uint32_t* lds) {
+template <int DV, bool SYNC = true>
+__device__ __forceinline__ void stage_words(const uint8_t* rec, const Layout& L, int total_bits, uint32_t* lds) {
   const int nw = (total_bits + 31) >> 5;
   const int n4 = nw * DV / 4;
   const uint4* src = (const uint4*)(rec + L.codes_off);
   uint4* dst = (uint4*)lds;
   for (int e = threadIdx.x; e < n4; e += blockDim.x) dst[e] = src[e];
-  __syncthreads();
+  if constexpr (SYNC) __syncthreads();
 }
 
 // Decode staged code words into column-layout registers X[r][c] (row
 // 32w + r, column lane + 64c): x^ = fl32(code * Delta), or +-mu for one-bit
 // rows.  Row offsets and widths are wave-uniform.
 template <int DK, int DV>
-__device__ void unpack_cols(const uint32_t* words, const MetaSmem<DK>& m,
+__device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSmem<DK>& m,
                             float (&X)[ROW_BLOCK][DV / WAVE]) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
@@ -169,7 +170,7 @@ struct RecSmem {
 
 // Halving combine of the per-wave partials of column col.
 template <int DK, int DV>
-__device__ inline float combine_col(const float (&P)[DK / ROW_BLOCK][DV], int col) {
+__device__ __forceinline__ float combine_col(const float (&P)[DK / ROW_BLOCK][DV], int col) {
   constexpr int NWV = DK / ROW_BLOCK;
   float v[NWV];
 #pragma unroll
@@ -185,14 +186,16 @@ __device__ inline float combine_col(const float (&P)[DK / ROW_BLOCK][DV], int co
 // One token of the gated delta rule on column-layout registers (eq. rule,
 // KDA erase/write): S' = a S; u = S'^T k; S = S' + (beta k)(v - u)^T;
 // o = S^T q.  Writes o to o_out (if non-null).  All threads must call.
-template <int DK, int DV>
-__device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
-                            RecSmem<DK, DV>& sm, const void* v, size_t v_off, bool v_bf16,
-                            float* o_out) {
+template <int DK, int DV, bool BF16>
+__device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
+                            RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
   const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
   const float va = rs.a[myrow], vk = rs.k[myrow], vg = rs.g[myrow], vq = rs.q[myrow];
+  float vin[CPL];   // this lane's columns of v, loaded before the row sweep
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) vin[c] = in_f32<BF16>(v, v_off + lane + WAVE * c);
   float acc[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
@@ -213,7 +216,7 @@ __device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>&
   for (int c = 0; c < CPL; ++c) {
     const int col = lane + WAVE * c;
     const float u = combine_col<DK, DV>(sm.up, col);
-    wv[c] = in_f32(v, v_off + col, v_bf16) - u;
+    wv[c] = vin[c] - u;
     acc[c] = 0.f;
   }
 #pragma unroll
@@ -237,19 +240,66 @@ __device__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>&
   }
 }
 
-// Row absolute maxima of column-layout registers into R[DK].
+// Row absolute maxima of column-layout registers into R[DK].  Reduce-scatter
+// over the 64 lanes: each step halves the number of row values per lane by
+// pairing lanes that differ in one bit (permlane32/16 swaps for bits 5 and 4,
+// DPP rotates within 16-lane rows for bits 3 and 2, quad permutes for bits 1
+// and 0).  Afterwards lanes 2r and 2r+1 of wave w hold row 32w + r.
+template <int CTRL>
+__device__ __forceinline__ float fmax_dpp(float v) { return fmaxf(v, dpp_f<CTRL>(v)); }
+
+__device__ __forceinline__ float swap_max32(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, a), __builtin_bit_cast(int, b),
+                                                  false, false);
+  return fmaxf(__builtin_bit_cast(float, (int)r[0]), __builtin_bit_cast(float, (int)r[1]));
+}
+
+__device__ __forceinline__ float swap_max16(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, a), __builtin_bit_cast(int, b),
+                                                  false, false);
+  return fmaxf(__builtin_bit_cast(float, (int)r[0]), __builtin_bit_cast(float, (int)r[1]));
+}
+
 template <int DK, int DV>
-__device__ void row_max(const float (&X)[ROW_BLOCK][DV / WAVE], float* R) {
+__device__ __forceinline__ void row_max(const float (&X)[ROW_BLOCK][DV / WAVE], float* R) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
+  float v[ROW_BLOCK];
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    float mx = 0.f;
+    float mx = fabsf(X[r][0]);
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) mx = fmaxf(mx, fabsf(X[r][c]));
-    mx = wave_max_uniform(mx);
-    if (lane == 0) R[w * ROW_BLOCK + r] = mx;
+    for (int c = 1; c < CPL; ++c) mx = fmaxf(mx, fabsf(X[r][c]));
+    v[r] = mx;
   }
+  // lane bit 5: rows r and r + 16
+#pragma unroll
+  for (int r = 0; r < 16; ++r) v[r] = swap_max32(v[r], v[r + 16]);
+  // lane bit 4: rows r and r + 8
+#pragma unroll
+  for (int r = 0; r < 8; ++r) v[r] = swap_max16(v[r], v[r + 8]);
+  const bool b3 = (lane >> 3) & 1, b2 = (lane >> 2) & 1, b1 = (lane >> 1) & 1;
+  // lane bit 3 (rotate by 8 inside 16-lane rows is its own inverse)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float x0 = fmax_dpp<0x128>(v[r]), x1 = fmax_dpp<0x128>(v[r + 4]);
+    v[r] = b3 ? x1 : x0;
+  }
+  // lane bit 2: row_ror:N delivers lane (i - N) mod 16, so the partner i + 4
+  // of a lane with bit 2 clear comes from rotate 12 and i - 4 from rotate 4
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const float x0 = fmax_dpp<0x12C>(v[r]), x1 = fmax_dpp<0x124>(v[r + 2]);
+    v[r] = b2 ? x1 : x0;
+  }
+  // lane bit 1 (quad permute [2,3,0,1])
+  {
+    const float x0 = fmax_dpp<0x4E>(v[0]), x1 = fmax_dpp<0x4E>(v[1]);
+    v[0] = b1 ? x1 : x0;
+  }
+  // lane bit 0 (quad permute [1,0,3,2])
+  v[0] = fmax_dpp<0xB1>(v[0]);
+  if ((lane & 1) == 0) R[w * ROW_BLOCK + (lane >> 1)] = v[0];
 }
 
 // ----------------------------------------------------- row-layout fit ---
@@ -262,7 +312,7 @@ constexpr int CT_LD = DK + 8;
 // Sum of the per-segment partials of one row held by SEGS adjacent lanes, in
 // the halving order (p[s] + p[s + SEGS/2] first), via DPP quad permutes.
 template <int SEGS>
-__device__ inline float seg_combine(float v) {
+__device__ __forceinline__ float seg_combine(float v) {
   static_assert(SEGS == 1 || SEGS == 2 || SEGS == 4, "segments per row");
   if constexpr (SEGS == 4) v = v + dpp_f<0x4E>(v);   // lanes differing in bit 1
   if constexpr (SEGS >= 2) v = v + dpp_f<0xB1>(v);   // lanes differing in bit 0
@@ -270,19 +320,46 @@ __device__ inline float seg_combine(float v) {
 }
 
 // Order rows by width, widest first (ties by row index), so that each wave of
-// the fit holds rows of similar width and similar pruning depth.
+// the fit holds rows of similar width and similar pruning depth.  Also forms
+// the prefix sums P[i] of the new widths (row bit offsets of the packed
+// streams).  Wave-ballot counting; threads t < DK own row t.
 template <int DK>
-__device__ void width_order(const uint8_t* bits, uint8_t* perm) {
-  const int t = threadIdx.x;
+struct OrderSmem {
+  int cnt[DK / WAVE][MAX_B + 1];
+  int P[DK + 1];
+};
+
+template <int DK>
+__device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, OrderSmem<DK>& os) {
+  const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
+  int b = 0, below = 0;
   if (t < DK) {
-    const int b = bits[t];
-    int pos = 0;
-    for (int u = 0; u < DK; ++u) {
-      const int bu = bits[u];
-      pos += (bu > b) || (bu == b && u < t);
+    b = bits[t];
+    const unsigned long long lt = (1ull << lane) - 1ull;
+    for (int v = 1; v <= MAX_B; ++v) {
+      const unsigned long long m = __ballot(b == v);
+      if (lane == 0) os.cnt[w][v] = __popcll(m);
+      if (b == v) below = __popcll(m & lt);
     }
+    // prefix sums of widths in row order
+    const int incl = wave_incl_scan(b);
+    os.P[t + 1] = incl;          // per-wave inclusive; fixed up below
+  }
+  __syncthreads();
+  if (t < DK) {
+    int pos = below;
+    for (int v = b + 1; v <= MAX_B; ++v)
+      for (int q = 0; q < DK / WAVE; ++q) pos += os.cnt[q][v];
+    for (int q = 0; q < w; ++q) pos += os.cnt[q][b];
     perm[pos] = (uint8_t)t;
   }
+  // wave totals of widths -> global prefix
+  int carry = 0;
+  if (t < DK)
+    for (int q = 0; q < w; ++q) carry += os.P[(q + 1) * WAVE];
+  __syncthreads();
+  if (t < DK) os.P[t + 1] += carry;
+  if (t == 0) os.P[0] = 0;
   __syncthreads();
 }
 
@@ -300,7 +377,7 @@ __device__ void width_order(const uint8_t* bits, uint8_t* perm) {
 // reach the minimum, so the scan stops; the result equals the exhaustive
 // first strict minimum over all 16 candidates.
 template <int DK, int DV>
-__device__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* perm,
+__device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* perm,
                          const float (*phi)[N_FIT], int16_t* Ct, uint16_t* scale_out) {
   constexpr int SEGS = DV / SEG;
   constexpr int ITEMS = DK * SEGS;
@@ -343,8 +420,10 @@ __device__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* per
   const float nf = (float)((1 << (b - 1)) - 1);
   float best = __builtin_inff();
   int mb = N_FIT - 1;
+  float ph = phi[b][N_FIT - 1];
   for (int m = N_FIT - 1; m >= 0; --m) {
-    const float d = f16_to_f32(f32_to_f16_sat(mx * phi[b][m]));
+    const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
+    ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
     const float emax = __builtin_fmaf(-nf, d, mx);
     if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
     const float inv = d > 0.f ? 1.0f / d : 0.f;
@@ -372,20 +451,36 @@ __device__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* per
 }
 
 // Pack int16 codes Ct[DV][CT_LD] (column-major) with widths bits[] into column
-// bit streams: one thread per column, rows in order, widths wave-uniform.
+// bit streams.  Thread (column, half) packs rows [half*DK/2, (half+1)*DK/2)
+// starting at bit P[half*DK/2]; the word both halves share (if the boundary is
+// not word aligned) is merged through LDS.  Widths are wave-uniform.
 template <int DK, int DV>
-__device__ void pack_cols(const int16_t* Ct, const uint8_t* bits, uint32_t* words) {
+__device__ __forceinline__ void pack_cols(const int16_t* Ct, const uint8_t* bits, const int* P,
+                                          uint32_t* words, uint32_t* tail) {
+  constexpr int HALF = DK / 2;
+  static_assert(2 * DV <= 2 * DK, "one (column, half) per thread");
   const int tid = threadIdx.x, lane = lane_id();
-  constexpr int RPL = (DK + WAVE - 1) / WAVE;
+  const int col = tid % DV, half = tid / DV;
+  const bool active = tid < 2 * DV;
+  const int r0 = half * HALF;
+  const int start = active ? P[r0] : 0;
+  const int split = P[HALF];
+  constexpr int RPL = (HALF + WAVE - 1) / WAVE;
   int vb[RPL];
 #pragma unroll
-  for (int q = 0; q < RPL; ++q) vb[q] = (lane + WAVE * q < DK) ? bits[lane + WAVE * q] : 0;
-  for (int col = tid; col < DV; col += blockDim.x) {
-    const int16_t* cc = Ct + (size_t)col * CT_LD<DK>;
-    uint64_t acc = 0;
-    int nb = 0, wi = 0;
+  for (int q = 0; q < RPL; ++q) {
+    const int i = lane + WAVE * q;
+    vb[q] = (i < HALF && active) ? bits[r0 + i] : 0;
+  }
+  uint64_t acc = 0;
+  int nb = start & 31;      // bits already in the first word (owned by the lower half)
+  int wi = start >> 5;
+  uint32_t first = 0;       // upper half: its first word, merged after the barrier
+  bool first_pending = half == 1 && (split & 31) != 0;
+  const int16_t* cc = Ct + (size_t)col * CT_LD<DK> + r0;
+  if (active) {
 #pragma unroll
-    for (int i0 = 0; i0 < DK; i0 += 8) {
+    for (int i0 = 0; i0 < HALF; i0 += 8) {
       const uint4 raw = *(const uint4*)(cc + i0);
       const uint32_t pr[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
@@ -393,24 +488,44 @@ __device__ void pack_cols(const int16_t* Ct, const uint8_t* bits, uint32_t* word
         const int i = i0 + u;
         const int b = bcast_i(vb[i / WAVE], i % WAVE);
         const uint32_t code = (pr[u >> 1] >> (16 * (u & 1))) & 0xffffu;
-        const uint32_t f = code & ((1u << b) - 1u);
-        acc |= (uint64_t)f << nb;
+        acc |= (uint64_t)(code & ((1u << b) - 1u)) << nb;
         nb += b;
         if (nb >= 32) {
-          words[wi * DV + col] = (uint32_t)acc;
+          if (first_pending) {
+            first = (uint32_t)acc;
+            first_pending = false;
+          } else {
+            words[wi * DV + col] = (uint32_t)acc;
+          }
           ++wi;
           acc >>= 32;
           nb -= 32;
         }
       }
     }
-    if (nb > 0) words[wi * DV + col] = (uint32_t)acc;
+  }
+  // the lower half's last partial word goes to LDS when the upper half shares it
+  const bool shared = (split & 31) != 0;
+  if (active && half == 0 && nb > 0) {
+    if (shared) tail[col] = (uint32_t)acc;
+    else words[wi * DV + col] = (uint32_t)acc;
+  }
+  __syncthreads();
+  if (active && half == 1) {
+    if (shared) {
+      // first word of the upper half (complete, or still in acc if short)
+      const uint32_t mine = first_pending ? (uint32_t)acc : first;
+      words[(split >> 5) * DV + col] = mine | tail[col];
+      if (!first_pending && nb > 0) words[wi * DV + col] = (uint32_t)acc;
+    } else if (nb > 0) {
+      words[wi * DV + col] = (uint32_t)acc;
+    }
   }
 }
 
 // Write a record's metadata (header, widths, scales, stat codes).
 template <int DK>
-__device__ void store_meta(uint8_t* rec, const Layout& L, unsigned ntok, const uint8_t* bits,
+__device__ __forceinline__ void store_meta(uint8_t* rec, const Layout& L, unsigned ntok, const uint8_t* bits,
                            const uint16_t* scale16, const uint16_t* z, const uint16_t* r16) {
   const int tid = threadIdx.x;
   if (tid < 4) ((unsigned*)rec)[tid] = tid == 0 ? ntok : 0u;
@@ -435,7 +550,7 @@ struct StatSmem {
 };
 
 template <int DK>
-__device__ void row_weights(const KParams& p, int bh, const MetaSmem<DK>& meta,
+__device__ __forceinline__ void row_weights(const KParams& p, int bh, const MetaSmem<DK>& meta,
                             StatSmem<DK>& st, double m_run, double e_run, int t) {
   // m_run/e_run: EMA states of row t after the last token (thread t < DK)
   if (t < DK) {
@@ -468,7 +583,7 @@ __device__ void row_weights(const KParams& p, int bh, const MetaSmem<DK>& meta,
 // starting from the record: outputs o for every token, the float32 state after
 // the last token (to the workspace), row ranges and EMA rates, weights c and,
 // for the per-head scope, the widths.  Decode is the one-token case.
-template <int DK, int DV, bool HEAD>
+template <int DK, int DV, bool HEAD, bool BF16>
 __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   const int bh = blockIdx.x;
   const int t = threadIdx.x;
@@ -479,10 +594,13 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   __shared__ RowSmem<DK> rs;
   __shared__ RecSmem<DK, DV> rsm;
   __shared__ StatSmem<DK> st;
-  load_meta<DK>(rec, L, p.bmax, meta);
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
-  stage_words<DV>(rec, L, meta.P[DK], words);
+  // the first token's row scalars and the whole code-word capacity of the
+  // record are requested together with the metadata (one memory round trip)
+  load_rows<DK, BF16>(rs, p, bh, p.tok0);
+  stage_words<DV, false>(rec, L, L.wc * 32, words);   // the barrier in load_meta covers it
+  load_meta<DK>(rec, L, p.bmax, meta);
   float X[ROW_BLOCK][DV / WAVE];
   unpack_cols<DK, DV>(words, meta, X);
   // EMA states of row t (threads t < DK): from the record, or fresh
@@ -494,13 +612,13 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   }
   for (int j = 0; j < p.ntk; ++j) {
     const int tok = p.tok0 + j;
-    load_rows<DK>(rs, p, bh, tok);
+    if (j > 0) load_rows<DK, BF16>(rs, p, bh, tok);
     __syncthreads();
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV>(X, rs, rsm, p.v, th * DV, p.in_bf16, p.o + th * DV);
+    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV);
     if (t < DK) {
       const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
-      const float kv = in_f32(p.k, th * DK + t, p.in_bf16);
+      const float kv = in_f32<BF16>(p.k, th * DK + t);
       const float beta = p.beta[th];
       const double zs = decay_sample(sv), ys = erase_sample(kv, beta);
       if (fresh) {
@@ -545,7 +663,8 @@ __global__ void __launch_bounds__(1024) k_alloc(const double* c, int N, int need
 // Quantise the float32 state the stats pass left in the workspace with the
 // allocated widths and pack it into the record in place.
 template <int DK, int DV>
-__global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
+__global__ void __launch_bounds__(2 * DK) __attribute__((amdgpu_waves_per_eu(4)))
+k_requant(KParams p) {
   const int bh = blockIdx.x;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
@@ -553,6 +672,8 @@ __global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
   __shared__ uint8_t nb[DK], perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
+  __shared__ OrderSmem<DK> os;
+  __shared__ uint32_t tail[DV];
   const int t = threadIdx.x;
   const unsigned ntok = *(const unsigned*)rec;
   if (t < DK) {
@@ -563,15 +684,15 @@ __global__ void __launch_bounds__(2 * DK) k_requant(KParams p) {
   }
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
-  width_order<DK>(nb, perm);
+  width_order<DK>(nb, perm, os);
   fit_rows<DK, DV>(p.ws_s32 + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
   __syncthreads();
-  pack_cols<DK, DV>(Ct, nb, (uint32_t*)(rec + L.codes_off));
+  pack_cols<DK, DV>(Ct, nb, os.P, (uint32_t*)(rec + L.codes_off), tail);
   store_meta<DK>(rec, L, ntok + (unsigned)p.ntk, nb, sc16, zz, rr);
 }
 
 // Unquantised ("32-bit") state: load, one token, store.
-template <int DK, int DV>
+template <int DK, int DV, bool BF16>
 __global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
   constexpr int CPL = DV / WAVE;
   const int bh = blockIdx.x;
@@ -587,10 +708,10 @@ __global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
     for (int c = 0; c < CPL; ++c) X[r][c] = S[(w * ROW_BLOCK + r) * DV + lane + WAVE * c];
   for (int j = 0; j < p.ntk; ++j) {
     const int tok = p.tok0 + j;
-    load_rows<DK>(rs, p, bh, tok);
+    load_rows<DK, BF16>(rs, p, bh, tok);
     __syncthreads();
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV>(X, rs, rsm, p.v, th * DV, p.in_bf16, p.o + th * DV);
+    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV);
   }
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r)
@@ -610,6 +731,8 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   __shared__ uint8_t nb[DK], perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
+  __shared__ OrderSmem<DK> os;
+  __shared__ uint32_t tail[DV];
   const int t = threadIdx.x;
   if (t < DK) {
     nb[t] = (uint8_t)min(max((int)bits[(size_t)bh * DK + t], 1), p.bmax);
@@ -618,10 +741,10 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   }
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
-  width_order<DK>(nb, perm);
+  width_order<DK>(nb, perm, os);
   fit_rows<DK, DV>(S + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
   __syncthreads();
-  pack_cols<DK, DV>(Ct, nb, (uint32_t*)(rec + L.codes_off));
+  pack_cols<DK, DV>(Ct, nb, os.P, (uint32_t*)(rec + L.codes_off), tail);
   store_meta<DK>(rec, L, ntok, nb, sc16, zz, rr);
 }
 
@@ -719,17 +842,27 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st) {
   const int nbh = p.B * p.H;
   if (p.state32) {
     ProfScope ps("step32", st);
-    k_step32<DK, DV><<<nbh, 2 * DK, 0, st>>>(p);
+    if (p.in_bf16)
+      k_step32<DK, DV, true><<<nbh, 2 * DK, 0, st>>>(p);
+    else
+      k_step32<DK, DV, false><<<nbh, 2 * DK, 0, st>>>(p);
     return hipGetLastError();
   }
   hipError_t e;
   {
     ProfScope ps("stats", st);
     const size_t dyn = (size_t)(p.L.wc + 1) * DV * 4;
-    if (p.scope == 1)
-      k_chunk<DK, DV, true><<<nbh, 2 * DK, dyn, st>>>(p);
-    else
-      k_chunk<DK, DV, false><<<nbh, 2 * DK, dyn, st>>>(p);
+    if (p.scope == 1) {
+      if (p.in_bf16)
+        k_chunk<DK, DV, true, true><<<nbh, 2 * DK, dyn, st>>>(p);
+      else
+        k_chunk<DK, DV, true, false><<<nbh, 2 * DK, dyn, st>>>(p);
+    } else {
+      if (p.in_bf16)
+        k_chunk<DK, DV, false, true><<<nbh, 2 * DK, dyn, st>>>(p);
+      else
+        k_chunk<DK, DV, false, false><<<nbh, 2 * DK, dyn, st>>>(p);
+    }
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;

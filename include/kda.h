@@ -156,11 +156,21 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records,
                 const float* s, const float* beta, const double* gamma,
                 float* o, void* ws, void* stream);
 
-/* Diagnostics: per-kernel timing.  While enabled (on != 0), every kernel a
- * call enqueues is bracketed by two hipEvents recorded on the call's stream
- * (host-side runtime objects from a reusable pool; no device memory).  Not
+/* Diagnostics: per-kernel timing and work counts.  With KDA_PROFILE_EVENTS,
+ * every kernel a call enqueues is bracketed by two hipEvents recorded on the
+ * call's stream (host-side runtime objects from a reusable pool).  With
+ * KDA_PROFILE_COUNTERS, the quantiser counts its clip-factor evaluations into
+ * an 8-byte device counter that the first such call allocates (the only
+ * device allocation the library makes; it lives until the process ends; the
+ * counting itself slows the quantiser down).  flags = 0 turns both off.  Not
  * thread safe; meant for single-threaded benchmark drivers. */
-int kda_profile_enable(int on);
+enum { KDA_PROFILE_EVENTS = 1, KDA_PROFILE_COUNTERS = 2 };
+int kda_profile_enable(int flags);
+
+/* Synchronise the device, then report and clear the number of (row segment of
+ * 64 columns) x (clip-factor candidate) evaluations counted while profiling
+ * was enabled.  Host pointer. */
+int kda_profile_counters(unsigned long long* fit_evals);
 
 /* Wait for the last recorded event, then report per kernel kind (static
  * strings such as "stats", "alloc", "requant") the summed milliseconds and

@@ -145,8 +145,13 @@ def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None):
         _stream()))
 
 
-def kda_profile_enable(on=True):
-    _check(load().kda_profile_enable(1 if on else 0))
+PROFILE_EVENTS = 1
+PROFILE_COUNTERS = 2
+
+
+def kda_profile_enable(flags=PROFILE_EVENTS):
+    """flags: PROFILE_EVENTS | PROFILE_COUNTERS, or 0 to disable."""
+    _check(load().kda_profile_enable(int(flags)))
 
 
 def kda_profile_read(max_kinds=16):
@@ -157,3 +162,11 @@ def kda_profile_read(max_kinds=16):
     n = ctypes.c_int(0)
     _check(load().kda_profile_read(max_kinds, kinds, ms, cnt, ctypes.byref(n)))
     return {kinds[i].decode(): (ms[i], cnt[i]) for i in range(min(n.value, max_kinds))}
+
+
+def kda_profile_counters():
+    """Clip-factor evaluations (row segment x candidate) counted while
+    profiling was enabled since the previous call (synchronises)."""
+    n = ctypes.c_ulonglong(0)
+    _check(load().kda_profile_counters(ctypes.byref(n)))
+    return int(n.value)

@@ -33,7 +33,7 @@ constexpr int EOFF = 1100;
 struct AllocSmem {
   int hist_e[EBINS];
   int hist_d[256];
-  int red[32];
+  int red[48];
   int cand_n;
   int sel_beta, sel_digit, sel_rem, sel_mode;
   unsigned long long cand_key[WAVE];
@@ -94,26 +94,15 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     }
   }
   __syncthreads();
-  // histogram of exponents: one LDS atomic per distinct value in a wave
+  // histogram of exponents (few distinct values: LDS atomics conflict little)
 #pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k) {
-    bool pending = E[k] != E_ZERO;
-    while (__ballot(pending)) {
-      const unsigned long long act = __ballot(pending);
-      const int leader = __ffsll((long long)act) - 1;
-      const int e0 = __builtin_amdgcn_readlane(E[k], leader);
-      const unsigned long long same = __ballot(pending && E[k] == e0);
-      if (lane == leader) atomicAdd(&sm.hist_e[e0 + EOFF], __popcll(same));
-      if (pending && E[k] == e0) pending = false;
-    }
-  }
+  for (int k = 0; k < ALLOC_RPT; ++k)
+    if (E[k] != E_ZERO) atomicAdd(&sm.hist_e[E[k] + EOFF], 1);
   int emin = 0x7fffffff, emax = -0x7fffffff;
 #pragma unroll
   for (int k = 0; k < ALLOC_RPT; ++k)
     if (E[k] != E_ZERO) { emin = min(emin, E[k]); emax = max(emax, E[k]); }
-  npos = block_reduce(npos, sm.red, [](int a, int b) { return a + b; });
-  emin = block_reduce(emin, sm.red, [](int a, int b) { return a < b ? a : b; });
-  emax = block_reduce(emax, sm.red, [](int a, int b) { return a > b ? a : b; });
+  block_sum_min_max(npos, emin, emax, sm.red);
   __syncthreads();
   const long long ptot = (long long)npos * L;
 
@@ -154,21 +143,17 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   if (tid < WAVE) {
     const int top = emax - 2 * (bmin + 1);
     const int bot = emin - 2 * bmax;
-    long long run = 0;
+    int run = 0;
     for (int b0 = top; b0 >= bot; b0 -= WAVE) {
       const int bb = b0 - lane;
-      long long cnt = 0;
+      int cnt = 0;
       if (bb >= bot)
         for (int l = bmin + 1; l <= bmax; ++l) {
           const int e = bb + 2 * l + EOFF;
           if (e >= 0 && e < EBINS) cnt += sm.hist_e[e];
         }
       // inclusive prefix over lanes (lane order = descending bucket)
-      long long incl = cnt;
-      for (int o = 1; o < WAVE; o <<= 1) {
-        const long long v = __shfl_up(incl, o, WAVE);
-        if (lane >= o) incl += v;
-      }
+      const int incl = wave_incl_scan(cnt);
       const unsigned long long hit = __ballot(run + incl >= need);
       if (hit) {
         const int f = __ffsll((long long)hit) - 1;
@@ -178,7 +163,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
         }
         break;
       }
-      run += __shfl(incl, WAVE - 1, WAVE);
+      run += __builtin_amdgcn_readlane(incl, WAVE - 1);
     }
   }
   __syncthreads();

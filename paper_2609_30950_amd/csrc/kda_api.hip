@@ -8,6 +8,7 @@
 
 #include "../../include/kda.h"
 #include "kda_kernels.hpp"
+#include "kda_profile.hpp"
 
 namespace {
 
@@ -72,6 +73,7 @@ KParams make_params(const kda_config* cfg, int need) {
   p.alpha = 2.0 / (double)(cfg->ema_span + 1);
   p.one_minus_alpha = 1.0 - p.alpha;
   p.L = kda::make_layout(cfg->d_k, cfg->d_v, cfg->b_max < 1 ? 1 : cfg->b_max);
+  p.diag_fit = kda::prof_counter();
   for (int b = 0; b <= kda::MAX_B; ++b)
     for (int m = 0; m < kda::N_FIT; ++m) {
       const int n = b >= 2 ? (1 << (b - 1)) - 1 : 0;

@@ -88,13 +88,21 @@ __device__ __forceinline__ float wave_max_uniform(float v) {
   return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
-// inclusive prefix sum over the wave
+// Inclusive prefix sum over the wave: Hillis-Steele within 16-lane rows
+// (row shifts by 1, 2, 4, 8; lanes without a source add 0), then the row
+// totals are carried across rows with row_bcast:15 and row_bcast:31.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_add_src(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, false);
+}
+
 __device__ __forceinline__ int wave_incl_scan(int v) {
-  const int l = lane_id();
-  for (int o = 1; o < WAVE; o <<= 1) {
-    int w = __shfl_up(v, o, WAVE);
-    if (l >= o) v += w;
-  }
+  v += dpp_add_src<0x111, 0xF>(v);
+  v += dpp_add_src<0x112, 0xF>(v);
+  v += dpp_add_src<0x114, 0xF>(v);
+  v += dpp_add_src<0x118, 0xF>(v);
+  v += dpp_add_src<0x142, 0xA>(v);
+  v += dpp_add_src<0x143, 0xC>(v);
   return v;
 }
 
@@ -129,6 +137,29 @@ __device__ __forceinline__ int block_reduce(int v, int* scratch, Op op) {
   int r = scratch[0];
   for (int i = 1; i < nw; ++i) r = op(r, scratch[i]);
   return r;
+}
+
+// Block-wide (sum, min, max) of three ints in one pass (two barriers).
+__device__ __forceinline__ void block_sum_min_max(int& sum, int& mn, int& mx, int* scratch) {
+  const int w = threadIdx.x / WAVE, nw = (blockDim.x + WAVE - 1) / WAVE;
+  sum = wave_reduce_i(sum, [](int a, int b) { return a + b; });
+  mn = wave_reduce_i(mn, [](int a, int b) { return a < b ? a : b; });
+  mx = wave_reduce_i(mx, [](int a, int b) { return a > b ? a : b; });
+  __syncthreads();
+  if (lane_id() == 0) {
+    scratch[3 * w] = sum;
+    scratch[3 * w + 1] = mn;
+    scratch[3 * w + 2] = mx;
+  }
+  __syncthreads();
+  sum = scratch[0];
+  mn = scratch[1];
+  mx = scratch[2];
+  for (int i = 1; i < nw; ++i) {
+    sum += scratch[3 * i];
+    mn = scratch[3 * i + 1] < mn ? scratch[3 * i + 1] : mn;
+    mx = scratch[3 * i + 2] > mx ? scratch[3 * i + 2] : mx;
+  }
 }
 
 // ------------------------------------------------ EMA and rate coding ---

@@ -378,7 +378,8 @@ __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, 
 // first strict minimum over all 16 candidates.
 template <int DK, int DV>
 __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* perm,
-                         const float (*phi)[N_FIT], int16_t* Ct, uint16_t* scale_out) {
+                         const float (*phi)[N_FIT], int16_t* Ct, uint16_t* scale_out,
+                         unsigned long long* diag) {
   constexpr int SEGS = DV / SEG;
   constexpr int ITEMS = DK * SEGS;
   const int tid = threadIdx.x;
@@ -403,6 +404,7 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
   if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
   const int b = bits[i];
   int16_t* dst = Ct + (size_t)(sg * SEG) * CT_LD<DK> + i;
+  int evals = 0;
   if (b == 1) {
     float acc = 0.f;
 #pragma unroll
@@ -415,38 +417,44 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
       for (int j = 0; j < SEG; ++j) dst[(size_t)j * CT_LD<DK>] = (int16_t)(x[j] < 0.f ? 1 : 0);
       if (sg == 0) scale_out[i] = mu;
     }
-    return;
-  }
-  const float nf = (float)((1 << (b - 1)) - 1);
-  float best = __builtin_inff();
-  int mb = N_FIT - 1;
-  float ph = phi[b][N_FIT - 1];
-  for (int m = N_FIT - 1; m >= 0; --m) {
-    const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
-    ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
-    const float emax = __builtin_fmaf(-nf, d, mx);
-    if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
+  } else {
+    const float nf = (float)((1 << (b - 1)) - 1);
+    float best = __builtin_inff();
+    int mb = N_FIT - 1;
+    float ph = phi[b][N_FIT - 1];
+    for (int m = N_FIT - 1; m >= 0; --m) {
+      const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
+      ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
+      const float emax = __builtin_fmaf(-nf, d, mx);
+      if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
+      ++evals;
+      const float inv = d > 0.f ? 1.0f / d : 0.f;
+      float err = 0.f;
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+        const float e = __builtin_fmaf(-c, d, x[j]);
+        err = __builtin_fmaf(e, e, err);
+      }
+      err = seg_combine<SEGS>(err);
+      if (err <= best) { best = err; mb = m; }
+    }
+    const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
+    const float d = f16_to_f32(dh);
     const float inv = d > 0.f ? 1.0f / d : 0.f;
-    float err = 0.f;
+    if (valid) {
 #pragma unroll
-    for (int j = 0; j < SEG; ++j) {
-      const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-      const float e = __builtin_fmaf(-c, d, x[j]);
-      err = __builtin_fmaf(e, e, err);
+      for (int j = 0; j < SEG; ++j) {
+        const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+        dst[(size_t)j * CT_LD<DK>] = (int16_t)c;
+      }
+      if (sg == 0) scale_out[i] = dh;
     }
-    err = seg_combine<SEGS>(err);
-    if (err <= best) { best = err; mb = m; }
   }
-  const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
-  const float d = f16_to_f32(dh);
-  const float inv = d > 0.f ? 1.0f / d : 0.f;
-  if (valid) {
-#pragma unroll
-    for (int j = 0; j < SEG; ++j) {
-      const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-      dst[(size_t)j * CT_LD<DK>] = (int16_t)c;
-    }
-    if (sg == 0) scale_out[i] = dh;
+  if (diag != nullptr) {
+    // all lanes have reconverged here
+    const int tot = wave_reduce_i(valid ? evals : 0, [](int a, int c) { return a + c; });
+    if (lane_id() == 0) atomicAdd(diag, (unsigned long long)tot);
   }
 }
 
@@ -685,7 +693,7 @@ k_requant(KParams p) {
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
   width_order<DK>(nb, perm, os);
-  fit_rows<DK, DV>(p.ws_s32 + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
+  fit_rows<DK, DV>(p.ws_s32 + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16, p.diag_fit);
   __syncthreads();
   pack_cols<DK, DV>(Ct, nb, os.P, (uint32_t*)(rec + L.codes_off), tail);
   store_meta<DK>(rec, L, ntok + (unsigned)p.ntk, nb, sc16, zz, rr);
@@ -742,7 +750,7 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
   width_order<DK>(nb, perm, os);
-  fit_rows<DK, DV>(S + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16);
+  fit_rows<DK, DV>(S + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16, p.diag_fit);
   __syncthreads();
   pack_cols<DK, DV>(Ct, nb, os.P, (uint32_t*)(rec + L.codes_off), tail);
   store_meta<DK>(rec, L, ntok, nb, sc16, zz, rr);

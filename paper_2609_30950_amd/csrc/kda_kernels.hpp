@@ -30,6 +30,7 @@ struct KParams {
   uint32_t* ws_zr;
   uint8_t* ws_bits;
   float* ws_s32;            // float32 state after the token, [B][H][dk][dv]
+  unsigned long long* diag_fit;  // profiling: candidate evaluations (or null)
 };
 
 hipError_t launch_step(const KParams& p, hipStream_t st);

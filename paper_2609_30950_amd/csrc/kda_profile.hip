@@ -15,11 +15,13 @@ struct Mark {
   hipEvent_t start, stop;
 };
 
-bool g_on = false;
+bool g_on = false;          // per-kernel events
+bool g_count = false;       // quantiser work counter
 std::vector<Mark> g_marks;      // recorded since the last read
 std::vector<hipEvent_t> g_pool; // spare events
 const char* g_pending = nullptr;
 hipEvent_t g_pending_start = nullptr;
+unsigned long long* g_counter = nullptr;   // device memory, 8 bytes
 
 hipEvent_t take() {
   if (!g_pool.empty()) {
@@ -41,6 +43,8 @@ void prof_begin(const char* kind, hipStream_t st) {
   if (g_pending_start) (void)hipEventRecord(g_pending_start, st);
 }
 
+unsigned long long* prof_counter() { return g_count ? g_counter : nullptr; }
+
 void prof_end(hipStream_t st) {
   if (!g_on || !g_pending_start) return;
   hipEvent_t stop = take();
@@ -54,8 +58,24 @@ void prof_end(hipStream_t st) {
 
 extern "C" {
 
-int kda_profile_enable(int on) {
-  kda::g_on = on != 0;
+int kda_profile_enable(int flags) {
+  if ((flags & KDA_PROFILE_COUNTERS) && kda::g_counter == nullptr) {
+    if (hipMalloc(&kda::g_counter, sizeof(unsigned long long)) != hipSuccess) return KDA_ERR_HIP;
+    if (hipMemset(kda::g_counter, 0, sizeof(unsigned long long)) != hipSuccess) return KDA_ERR_HIP;
+  }
+  kda::g_on = (flags & KDA_PROFILE_EVENTS) != 0;
+  kda::g_count = (flags & KDA_PROFILE_COUNTERS) != 0;
+  return KDA_OK;
+}
+
+int kda_profile_counters(unsigned long long* fit_evals) {
+  if (!fit_evals) return KDA_ERR_ARG;
+  *fit_evals = 0;
+  if (kda::g_counter == nullptr) return KDA_OK;
+  if (hipDeviceSynchronize() != hipSuccess) return KDA_ERR_HIP;
+  if (hipMemcpy(fit_evals, kda::g_counter, sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess)
+    return KDA_ERR_HIP;
+  if (hipMemset(kda::g_counter, 0, sizeof(unsigned long long)) != hipSuccess) return KDA_ERR_HIP;
   return KDA_OK;
 }
 

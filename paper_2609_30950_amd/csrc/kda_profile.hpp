@@ -14,6 +14,10 @@ namespace kda {
 void prof_begin(const char* kind, hipStream_t st);
 void prof_end(hipStream_t st);
 
+// Device counter of fit work (row-segment x candidate evaluations) while
+// profiling is enabled, else nullptr.
+unsigned long long* prof_counter();
+
 struct ProfScope {
   hipStream_t st;
   ProfScope(const char* kind, hipStream_t s) : st(s) { prof_begin(kind, s); }

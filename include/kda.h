@@ -63,7 +63,8 @@ enum { KDA_SCOPE_SEQUENCE = 0, KDA_SCOPE_HEAD = 1 };
 typedef struct {
   int32_t B;              /* sequences                                        */
   int32_t H;              /* heads per layer                                  */
-  int32_t d_k;            /* rows (key channels): 64 or 128                   */
+  int32_t d_k;            /* rows (key channels): 64, 128 or 256 (256 needs
+                             b_max <= 8)                                      */
   int32_t d_v;            /* columns (value channels): equal to d_k           */
   int32_t group_rows;     /* G: rows per output-normalisation group (Sec. 2,
                              Range normalization); divides d_k                */

@@ -36,7 +36,7 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg == nullptr) return KDA_ERR_ARG;
   if (cfg->B < 1 || cfg->H < 1) return KDA_ERR_SHAPE;
   if (cfg->d_k != cfg->d_v) return KDA_ERR_UNSUPPORTED;
-  if (cfg->d_k != 64 && cfg->d_k != 128) return KDA_ERR_UNSUPPORTED;
+  if (cfg->d_k != 64 && cfg->d_k != 128 && cfg->d_k != 256) return KDA_ERR_UNSUPPORTED;
   if (cfg->decay_per_head != 0 && cfg->decay_per_head != 1) return KDA_ERR_ARG;
   if (cfg->state32 != 0 && cfg->state32 != 1) return KDA_ERR_ARG;
   if (cfg->state32) {
@@ -46,6 +46,7 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg->group_rows < 1 || cfg->d_k % cfg->group_rows != 0) return KDA_ERR_ARG;
   if (cfg->scope != KDA_SCOPE_SEQUENCE && cfg->scope != KDA_SCOPE_HEAD) return KDA_ERR_ARG;
   if (cfg->b_min < 1 || cfg->b_max < cfg->b_min || cfg->b_max > 16) return KDA_ERR_ARG;
+  if (cfg->d_k == 256 && cfg->b_max > 8) return KDA_ERR_UNSUPPORTED;   // LDS code tile
   if (cfg->ema_span < 1) return KDA_ERR_ARG;
   if (!std::isfinite(cfg->mean_bits)) return KDA_ERR_ARG;
   const long long N = cfg->scope == KDA_SCOPE_SEQUENCE ? (long long)cfg->H * cfg->d_k : cfg->d_k;

@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kda_alloc.hpp"
 #include "kda_device.hpp"
 #include "kda_kernels.hpp"
@@ -136,14 +138,14 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
   const int w = threadIdx.x / WAVE, lane = lane_id();
   // lane r holds row 32w + r's width, offset and scale; rows are broadcast.
   // One expression covers every width: the field is sign-extended, then
-  // x^ = fma(code, mul, add) with (mul, add) = (Delta, 0) for b >= 2, which
-  // is fl32(code Delta), and (2 mu, mu) for one-bit rows (code 0 or -1),
-  // which gives mu or -mu exactly.
+  // x^ = (code + add) mul with (mul, add) = (Delta, 0) for b >= 2, which is
+  // fl32(code Delta), and (2 mu, 1/2) for one-bit rows (code 0 or -1), which
+  // gives mu or -mu exactly, signed zeros included.
   const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
   const int vb = m.w[myrow], vP = m.P[myrow];
   const float vsc = m.sc[myrow];
   const float vmul = vb == 1 ? 2.0f * vsc : vsc;
-  const float vadd = vb == 1 ? vsc : 0.0f;
+  const float vadd = vb == 1 ? 0.5f : 0.0f;
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
     const int b = bcast_i(vb, r);
@@ -157,7 +159,7 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
       const uint32_t hi = words[(kw + 1) * DV + col];   // staged; masked off unless straddling
       const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
       const int code = __builtin_amdgcn_sbfe((int)f, 0, b);
-      X[r][c] = __builtin_fmaf((float)code, mul, add);
+      X[r][c] = ((float)code + add) * mul;
     }
   }
 }
@@ -304,10 +306,15 @@ __device__ __forceinline__ void row_max(const float (&X)[ROW_BLOCK][DV / WAVE], 
 
 // ----------------------------------------------------- row-layout fit ---
 
-// Column stride (int16 elements) of the column-major code buffer: padded by
-// 8 so that the 16-byte reads of consecutive columns hit distinct LDS banks.
+// Codes in LDS: int16 (widths up to 16) for d_k <= 128, int8 for d_k = 256
+// (widths up to 8), so that the column-major code tile fits in LDS.
 template <int DK>
-constexpr int CT_LD = DK + 8;
+using CodeT = typename std::conditional<(DK > 128), int8_t, int16_t>::type;
+
+// Column stride (elements) of the column-major code buffer: padded by 16 bytes
+// so that the 16-byte reads of consecutive columns hit distinct LDS banks.
+template <int DK>
+constexpr int CT_LD = DK + 16 / (int)sizeof(CodeT<DK>);
 
 // Sum of the per-segment partials of one row held by SEGS adjacent lanes, in
 // the halving order (p[s] + p[s + SEGS/2] first), via DPP quad permutes.
@@ -378,15 +385,17 @@ __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, 
 // first strict minimum over all 16 candidates.
 template <int DK, int DV>
 __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* perm,
-                         const float (*phi)[N_FIT], int16_t* Ct, uint16_t* scale_out,
+                         const float (*phi)[N_FIT], CodeT<DK>* Ct, uint16_t* scale_out,
                          unsigned long long* diag) {
   constexpr int SEGS = DV / SEG;
   constexpr int ITEMS = DK * SEGS;
-  const int tid = threadIdx.x;
-  static_assert(ITEMS <= 2 * DK, "one fit item per thread");
-  const bool valid = tid < ITEMS;
-  const int i = valid ? perm[tid / SEGS] : 0;
-  const int sg = tid % SEGS;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int iters = (ITEMS + nt - 1) / nt;   // same count for every thread
+  for (int rep = 0; rep < iters; ++rep) {
+  const int item = rep * nt + tid;
+  const bool valid = item < ITEMS;
+  const int i = valid ? perm[item / SEGS] : 0;
+  const int sg = item % SEGS;
   float x[SEG];
   const float4* src = (const float4*)(S + (size_t)i * DV + sg * SEG);
 #pragma unroll
@@ -403,7 +412,7 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
   if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0xB1>(mx));
   if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
   const int b = bits[i];
-  int16_t* dst = Ct + (size_t)(sg * SEG) * CT_LD<DK> + i;
+  CodeT<DK>* dst = Ct + (size_t)(sg * SEG) * CT_LD<DK> + i;
   int evals = 0;
   if (b == 1) {
     float acc = 0.f;
@@ -414,7 +423,7 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
     const uint16_t mu = f32_to_f16_sat(acc * (1.0f / (float)DV));
     if (valid) {
 #pragma unroll
-      for (int j = 0; j < SEG; ++j) dst[(size_t)j * CT_LD<DK>] = (int16_t)(x[j] < 0.f ? 1 : 0);
+      for (int j = 0; j < SEG; ++j) dst[(size_t)j * CT_LD<DK>] = (CodeT<DK>)(x[j] < 0.f ? 1 : 0);
       if (sg == 0) scale_out[i] = mu;
     }
   } else {
@@ -446,7 +455,7 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
         const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-        dst[(size_t)j * CT_LD<DK>] = (int16_t)c;
+        dst[(size_t)j * CT_LD<DK>] = (CodeT<DK>)c;
       }
       if (sg == 0) scale_out[i] = dh;
     }
@@ -456,14 +465,15 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
     const int tot = wave_reduce_i(valid ? evals : 0, [](int a, int c) { return a + c; });
     if (lane_id() == 0) atomicAdd(diag, (unsigned long long)tot);
   }
+  }
 }
 
-// Pack int16 codes Ct[DV][CT_LD] (column-major) with widths bits[] into column
+// Pack codes Ct[DV][CT_LD] (column-major) with widths bits[] into column
 // bit streams.  Thread (column, half) packs rows [half*DK/2, (half+1)*DK/2)
 // starting at bit P[half*DK/2]; the word both halves share (if the boundary is
 // not word aligned) is merged through LDS.  Widths are wave-uniform.
 template <int DK, int DV>
-__device__ __forceinline__ void pack_cols(const int16_t* Ct, const uint8_t* bits, const int* P,
+__device__ __forceinline__ void pack_cols(const CodeT<DK>* Ct, const uint8_t* bits, const int* P,
                                           uint32_t* words, uint32_t* tail) {
   constexpr int HALF = DK / 2;
   static_assert(2 * DV <= 2 * DK, "one (column, half) per thread");
@@ -485,17 +495,19 @@ __device__ __forceinline__ void pack_cols(const int16_t* Ct, const uint8_t* bits
   int wi = start >> 5;
   uint32_t first = 0;       // upper half: its first word, merged after the barrier
   bool first_pending = half == 1 && (split & 31) != 0;
-  const int16_t* cc = Ct + (size_t)col * CT_LD<DK> + r0;
+  constexpr int CB = (int)sizeof(CodeT<DK>);   // bytes per code
+  constexpr int CPR = 16 / CB;                  // codes per 16-byte read
+  const CodeT<DK>* cc = Ct + (size_t)col * CT_LD<DK> + r0;
   if (active) {
 #pragma unroll
-    for (int i0 = 0; i0 < HALF; i0 += 8) {
+    for (int i0 = 0; i0 < HALF; i0 += CPR) {
       const uint4 raw = *(const uint4*)(cc + i0);
       const uint32_t pr[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < CPR; ++u) {
         const int i = i0 + u;
         const int b = bcast_i(vb[i / WAVE], i % WAVE);
-        const uint32_t code = (pr[u >> 1] >> (16 * (u & 1))) & 0xffffu;
+        const uint32_t code = (pr[u / (4 / CB)] >> (8 * CB * (u % (4 / CB)))) & ((1u << (8 * CB)) - 1u);
         acc |= (uint64_t)(code & ((1u << b) - 1u)) << nb;
         nb += b;
         if (nb >= 32) {
@@ -676,7 +688,7 @@ k_requant(KParams p) {
   const int bh = blockIdx.x;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
-  __shared__ __align__(16) int16_t Ct[DV * CT_LD<DK>];
+  __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD<DK>];
   __shared__ uint8_t nb[DK], perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
@@ -735,7 +747,7 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   const int bh = blockIdx.x;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)p.records + L.slot * (long long)bh;
-  __shared__ __align__(16) int16_t Ct[DV * CT_LD<DK>];
+  __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD<DK>];
   __shared__ uint8_t nb[DK], perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
@@ -887,6 +899,7 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st) {
 
 static hipError_t launch_interval(const KParams& p, hipStream_t st) {
   if (p.dk == 64) return launch_interval_t<64, 64>(p, st);
+  if (p.dk == 256) return launch_interval_t<256, 256>(p, st);
   return launch_interval_t<128, 128>(p, st);
 }
 
@@ -919,6 +932,7 @@ static hipError_t launch_pack_t(const KParams& p, const float* S, const uint8_t*
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st) {
   if (p.dk == 64) return launch_pack_t<64, 64>(p, S, bits, s_hat, r, ntok, st);
+  if (p.dk == 256) return launch_pack_t<256, 256>(p, S, bits, s_hat, r, ntok, st);
   return launch_pack_t<128, 128>(p, S, bits, s_hat, r, ntok, st);
 }
 
@@ -928,6 +942,8 @@ hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_ha
   const size_t dyn = p.state32 ? 0 : (size_t)(p.L.wc + 1) * p.dv * 4;
   if (p.dk == 64)
     k_unpack<64, 64><<<p.B * p.H, 128, dyn, st>>>(p, S, bits, s_hat, r);
+  else if (p.dk == 256)
+    k_unpack<256, 256><<<p.B * p.H, 512, dyn, st>>>(p, S, bits, s_hat, r);
   else
     k_unpack<128, 128><<<p.B * p.H, 256, dyn, st>>>(p, S, bits, s_hat, r);
   return hipGetLastError();
@@ -937,6 +953,8 @@ hipError_t launch_alloc_bits(const KParams& p, const double* gamma, const float*
                              hipStream_t st) {
   if (p.dk == 64)
     k_weights_from_ranges<64><<<p.B * p.H, 64, 0, st>>>(p, gamma, R);
+  else if (p.dk == 256)
+    k_weights_from_ranges<256><<<p.B * p.H, 256, 0, st>>>(p, gamma, R);
   else
     k_weights_from_ranges<128><<<p.B * p.H, 128, 0, st>>>(p, gamma, R);
   hipError_t e = hipGetLastError();

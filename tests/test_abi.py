@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
-@pytest.mark.parametrize("d,bmax", [(64, 8), (128, 8), (128, 16)])
+@pytest.mark.parametrize("d,bmax", [(64, 8), (128, 8), (128, 16), (256, 8), (256, 4)])
 def test_record_bytes_match_layout(d, bmax):
     cfg = K.Config(B=1, H=1, d_k=d, d_v=d, group_rows=d, b_min=1, b_max=bmax, mean_bits=2)
     assert K.record_bytes(cfg) == record.record_bytes(d, d, bmax)
@@ -48,6 +48,8 @@ def test_invalid_configs_rejected():
         dict(scope=2),
         dict(ema_span=0),
         dict(H=64, d_k=128, d_v=128),          # > 4096 rows in one budget
+        dict(H=17, d_k=256, d_v=256, group_rows=256),
+        dict(d_k=256, d_v=256, group_rows=256, b_max=16),   # 256 rows: widths up to 8
     ]
     for kw in bad:
         base = dict(B=1, H=2, d_k=64, d_v=64, group_rows=64)

@@ -101,6 +101,23 @@ def test_zero_records_unpack_to_zero_state():
     assert torch.count_nonzero(Sg).item() == 0
 
 
+def test_one_bit_rows_with_zero_mean_keep_signs():
+    """A one-bit row whose mean |x| rounds to an FP16 zero decodes to +-0
+    with the sign of each code (the oracle's -mu for negative codes)."""
+    d = 64
+    rng = np.random.default_rng(11)
+    S = (np.where(rng.random((1, 1, d, d)) < 0.5, -1.0, 1.0) * 1e-30).astype(np.float32)
+    bits = np.ones((1, 1, d), np.uint8)
+    cfg = K.Config(B=1, H=1, d_k=d, d_v=d, group_rows=d, b_min=1, b_max=8, mean_bits=4)
+    want = _oracle_pack(S, bits, np.full((1, 1, d), 0.01), np.zeros((1, 1, d)), 1, d, d, 8)
+    f = record.unpack(want, d, d, 8)
+    X = quant.dequantize_rows(f["codes"], f["scale"], f["widths"])
+    assert np.all(X == 0) and np.any(np.signbit(X))
+    Sg = torch.empty(d * d, dtype=torch.float32, device="cuda")
+    K.kda_unpack_state(cfg, dev(want), Sg)
+    assert np.array_equal(host(Sg).view(np.uint32), X.reshape(-1).view(np.uint32))
+
+
 def _midpoint_ranges(b, m, count, rng):
     """float32 ranges R whose float32 product R*phi lands exactly on an FP16
     midpoint while the exact product does not (single vs double rounding

@@ -471,74 +471,73 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
 // Pack codes Ct[DV][CT_LD] (column-major) with widths bits[] into column
 // bit streams.  Thread (column, half) packs rows [half*DK/2, (half+1)*DK/2)
 // starting at bit P[half*DK/2]; the word both halves share (if the boundary is
-// not word aligned) is merged through LDS.  Widths are wave-uniform.
+// not word aligned) is merged through LDS.  A wave holds one half, so the
+// widths, the bit position and every word boundary are wave-uniform (scalar
+// registers and branches): each code costs one field extract and one
+// shift-or into the current word.
 template <int DK, int DV>
 __device__ __forceinline__ void pack_cols(const CodeT<DK>* Ct, const uint8_t* bits, const int* P,
                                           uint32_t* words, uint32_t* tail) {
   constexpr int HALF = DK / 2;
-  static_assert(2 * DV <= 2 * DK, "one (column, half) per thread");
-  const int tid = threadIdx.x, lane = lane_id();
-  const int col = tid % DV, half = tid / DV;
-  const bool active = tid < 2 * DV;
+  static_assert(DV == DK && DV % WAVE == 0, "one (column, half) per thread, halves wave-aligned");
+  const int tid = threadIdx.x;
+  const int col = tid % DV;
+  const int half = __builtin_amdgcn_readfirstlane(tid / DV);
   const int r0 = half * HALF;
-  const int start = active ? P[r0] : 0;
-  const int split = P[HALF];
-  constexpr int RPL = (HALF + WAVE - 1) / WAVE;
-  int vb[RPL];
-#pragma unroll
-  for (int q = 0; q < RPL; ++q) {
-    const int i = lane + WAVE * q;
-    vb[q] = (i < HALF && active) ? bits[r0 + i] : 0;
-  }
-  uint64_t acc = 0;
-  int nb = start & 31;      // bits already in the first word (owned by the lower half)
+  const int start = __builtin_amdgcn_readfirstlane(P[r0]);
+  const int split = __builtin_amdgcn_readfirstlane(P[HALF]);
+  // widths, four per LDS word (bits[] is 4-byte aligned), read as broadcasts
+  const uint32_t* bw = (const uint32_t*)(bits + r0);
+  uint32_t cur = 0;         // bits [32 wi, 32 wi + nb) of this column's stream
+  int nb = start & 31;      // bits below nb in the first word belong to the lower half
   int wi = start >> 5;
   uint32_t first = 0;       // upper half: its first word, merged after the barrier
   bool first_pending = half == 1 && (split & 31) != 0;
   constexpr int CB = (int)sizeof(CodeT<DK>);   // bytes per code
   constexpr int CPR = 16 / CB;                  // codes per 16-byte read
   const CodeT<DK>* cc = Ct + (size_t)col * CT_LD<DK> + r0;
-  if (active) {
 #pragma unroll
-    for (int i0 = 0; i0 < HALF; i0 += CPR) {
-      const uint4 raw = *(const uint4*)(cc + i0);
-      const uint32_t pr[4] = {raw.x, raw.y, raw.z, raw.w};
+  for (int i0 = 0; i0 < HALF; i0 += CPR) {
+    const uint4 raw = *(const uint4*)(cc + i0);
+    const uint32_t pr[4] = {raw.x, raw.y, raw.z, raw.w};
+    uint32_t wb[CPR / 4];
 #pragma unroll
-      for (int u = 0; u < CPR; ++u) {
-        const int i = i0 + u;
-        const int b = bcast_i(vb[i / WAVE], i % WAVE);
-        const uint32_t code = (pr[u / (4 / CB)] >> (8 * CB * (u % (4 / CB)))) & ((1u << (8 * CB)) - 1u);
-        acc |= (uint64_t)(code & ((1u << b) - 1u)) << nb;
-        nb += b;
-        if (nb >= 32) {
-          if (first_pending) {
-            first = (uint32_t)acc;
-            first_pending = false;
-          } else {
-            words[wi * DV + col] = (uint32_t)acc;
-          }
-          ++wi;
-          acc >>= 32;
-          nb -= 32;
+    for (int k = 0; k < CPR / 4; ++k) wb[k] = __builtin_amdgcn_readfirstlane(bw[i0 / 4 + k]);
+#pragma unroll
+    for (int u = 0; u < CPR; ++u) {
+      const int b = (int)((wb[u / 4] >> (8 * (u % 4))) & 0xffu);
+      const uint32_t field = __builtin_amdgcn_ubfe(pr[u / (4 / CB)], 8 * CB * (u % (4 / CB)), b);
+      cur |= field << nb;
+      nb += b;
+      if (nb >= 32) {
+        nb -= 32;
+        if (first_pending) {
+          first = cur;
+          first_pending = false;
+        } else {
+          uint32_t* wrow = words + wi * DV;   // uniform base, per-lane offset
+          wrow[col] = cur;
         }
+        ++wi;
+        cur = field >> (b - nb);   // the nb bits that did not fit (0 if none)
       }
     }
   }
   // the lower half's last partial word goes to LDS when the upper half shares it
   const bool shared = (split & 31) != 0;
-  if (active && half == 0 && nb > 0) {
-    if (shared) tail[col] = (uint32_t)acc;
-    else words[wi * DV + col] = (uint32_t)acc;
+  if (half == 0 && nb > 0) {
+    if (shared) tail[col] = cur;
+    else words[wi * DV + col] = cur;
   }
   __syncthreads();
-  if (active && half == 1) {
+  if (half == 1) {
     if (shared) {
-      // first word of the upper half (complete, or still in acc if short)
-      const uint32_t mine = first_pending ? (uint32_t)acc : first;
+      // first word of the upper half (complete, or still open if short)
+      const uint32_t mine = first_pending ? cur : first;
       words[(split >> 5) * DV + col] = mine | tail[col];
-      if (!first_pending && nb > 0) words[wi * DV + col] = (uint32_t)acc;
+      if (!first_pending && nb > 0) words[wi * DV + col] = cur;
     } else if (nb > 0) {
-      words[wi * DV + col] = (uint32_t)acc;
+      words[wi * DV + col] = cur;
     }
   }
 }
@@ -689,7 +688,8 @@ k_requant(KParams p) {
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
   __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD<DK>];
-  __shared__ uint8_t nb[DK], perm[DK];
+  __shared__ __align__(16) uint8_t nb[DK];
+  __shared__ uint8_t perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
   __shared__ OrderSmem<DK> os;
@@ -748,7 +748,8 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)p.records + L.slot * (long long)bh;
   __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD<DK>];
-  __shared__ uint8_t nb[DK], perm[DK];
+  __shared__ __align__(16) uint8_t nb[DK];
+  __shared__ uint8_t perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
   __shared__ float phi[MAX_B + 1][N_FIT];
   __shared__ OrderSmem<DK> os;

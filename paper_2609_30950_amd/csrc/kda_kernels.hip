@@ -36,6 +36,9 @@ __device__ __forceinline__ const uint8_t* slot_ptr(const void* recs, long long s
 
 template <int DK>
 struct MetaSmem {
+  // per-row decode descriptor, read by whole waves as one broadcast:
+  // {first word index * d_v, bit shift | width << 8, mul, add} (see unpack_cols)
+  uint4 desc[DK];
   uint8_t w[DK];      // widths of the stored record
   int P[DK + 1];      // prefix sums of widths (row bit offsets)
   float sc[DK];       // stored scales (FP16 -> float)
@@ -47,7 +50,7 @@ struct MetaSmem {
 // Load widths/scales/stat codes of a record and form the row offsets.
 // Widths above b_max (never written by this library) are clamped so that a
 // damaged record cannot address code words outside its slot.
-template <int DK>
+template <int DK, int DV>
 __device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
   const int tid = threadIdx.x;
   if (tid < DK / 2) {
@@ -76,7 +79,16 @@ __device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, i
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int i = tid * PER + q;
-      if (i < DK) m.P[i] = run;
+      if (i < DK) {
+        m.P[i] = run;
+        // x^ = (code + add) mul: (Delta, 0) for b >= 2, (2 mu, 1/2) for one bit
+        const int b = loc[q];
+        const float sc = m.sc[i];
+        const float mul = b == 1 ? 2.0f * sc : sc;
+        const float add = b == 1 ? 0.5f : 0.0f;
+        m.desc[i] = make_uint4((uint32_t)((run >> 5) * DV), (uint32_t)((run & 31) | (b << 8)),
+                               __builtin_bit_cast(uint32_t, mul), __builtin_bit_cast(uint32_t, add));
+      }
       run += loc[q];
     }
     if (tid == WAVE - 1) m.P[DK] = incl;
@@ -87,10 +99,8 @@ __device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, i
 // Per-row scalars of one token for the recurrence.
 template <int DK>
 struct RowSmem {
-  float a[DK];   // fl32(exp(-s))
-  float k[DK];
-  float q[DK];
-  float g[DK];   // fl32(beta * k)
+  float2 ak[DK];   // {fl32(exp(-s)), k}: first pass of the recurrence
+  float2 gq[DK];   // {fl32(beta * k), q}: second pass
 };
 
 template <bool BF16>
@@ -108,11 +118,9 @@ __device__ __forceinline__ void load_rows(RowSmem<DK>& rs, const KParams& p, int
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;       // (b, tok, h)
     const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
     const float beta = p.beta[th];
-    rs.a[t] = (float)exp(-(double)sv);
     const float kv = in_f32<BF16>(p.k, th * DK + t);
-    rs.k[t] = kv;
-    rs.q[t] = in_f32<BF16>(p.q, th * DK + t);
-    rs.g[t] = beta * kv;
+    rs.ak[t] = make_float2((float)exp(-(double)sv), kv);
+    rs.gq[t] = make_float2(beta * kv, in_f32<BF16>(p.q, th * DK + t));
   }
 }
 
@@ -130,36 +138,41 @@ __device__ __forceinline__ void stage_words(const uint8_t* rec, const Layout& L,
 
 // Decode staged code words into column-layout registers X[r][c] (row
 // 32w + r, column lane + 64c): x^ = fl32(code * Delta), or +-mu for one-bit
-// rows.  Row offsets and widths are wave-uniform.
+// rows.  Each row's descriptor is one LDS broadcast read; its word index,
+// shift and width are wave-uniform (scalar registers).  One expression covers
+// every width: the field is sign-extended, then x^ = (code + add) mul with
+// (mul, add) = (Delta, 0) for b >= 2, which is fl32(code Delta), and
+// (2 mu, 1/2) for one-bit rows (code 0 or -1), which gives mu or -mu exactly,
+// signed zeros included.
 template <int DK, int DV>
 __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSmem<DK>& m,
                             float (&X)[ROW_BLOCK][DV / WAVE]) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
-  // lane r holds row 32w + r's width, offset and scale; rows are broadcast.
-  // One expression covers every width: the field is sign-extended, then
-  // x^ = (code + add) mul with (mul, add) = (Delta, 0) for b >= 2, which is
-  // fl32(code Delta), and (2 mu, 1/2) for one-bit rows (code 0 or -1), which
-  // gives mu or -mu exactly, signed zeros included.
-  const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
-  const int vb = m.w[myrow], vP = m.P[myrow];
-  const float vsc = m.sc[myrow];
-  const float vmul = vb == 1 ? 2.0f * vsc : vsc;
-  const float vadd = vb == 1 ? 0.5f : 0.0f;
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    const int b = bcast_i(vb, r);
-    const int P = bcast_i(vP, r);
-    const float mul = bcast_f(vmul, r), add = bcast_f(vadd, r);
-    const int kw = P >> 5, sh = P & 31;
+    const uint4 d = m.desc[w * ROW_BLOCK + r];
+    const int base = __builtin_amdgcn_readfirstlane((int)d.x);
+    const int shb = __builtin_amdgcn_readfirstlane((int)d.y);
+    const int sh = shb & 31, b = shb >> 8;
+    const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
+    const uint32_t* wr = words + base;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int col = lane + WAVE * c;
-      const uint32_t lo = words[kw * DV + col];
-      const uint32_t hi = words[(kw + 1) * DV + col];   // staged; masked off unless straddling
+      const uint32_t lo = wr[col];
+      const uint32_t hi = wr[DV + col];   // staged; masked off unless straddling
       const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
       const int code = __builtin_amdgcn_sbfe((int)f, 0, b);
       X[r][c] = ((float)code + add) * mul;
+    }
+    // finish row r before the reads of later rows are issued: the compiler
+    // would otherwise keep every row's descriptor and words live at once
+    if (r % 2 == 1) {
+#pragma unroll
+      for (int q = r - 1; q <= r; ++q)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) asm volatile("" : "+v"(X[q][c])::"memory");
     }
   }
 }
@@ -193,8 +206,8 @@ __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], co
                             RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out) {
   constexpr int CPL = DV / WAVE;
   const int w = threadIdx.x / WAVE, lane = lane_id();
-  const int myrow = w * ROW_BLOCK + (lane & (ROW_BLOCK - 1));
-  const float va = rs.a[myrow], vk = rs.k[myrow], vg = rs.g[myrow], vq = rs.q[myrow];
+  const float2* ak = rs.ak + w * ROW_BLOCK;   // row scalars: LDS broadcast reads
+  const float2* gq = rs.gq + w * ROW_BLOCK;
   float vin[CPL];   // this lane's columns of v, loaded before the row sweep
 #pragma unroll
   for (int c = 0; c < CPL; ++c) vin[c] = in_f32<BF16>(v, v_off + lane + WAVE * c);
@@ -203,12 +216,14 @@ __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], co
   for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    const float a = bcast_f(va, r), kk = bcast_f(vk, r);
+    const float2 x = ak[r];
+    const float a = x.x, kk = x.y;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       X[r][c] = a * X[r][c];
       acc[c] = __builtin_fmaf(kk, X[r][c], acc[c]);
     }
+    if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) sm.up[w][lane + WAVE * c] = acc[c];
@@ -223,12 +238,14 @@ __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], co
   }
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) {
-    const float g = bcast_f(vg, r), qq = bcast_f(vq, r);
+    const float2 x = gq[r];
+    const float g = x.x, qq = x.y;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       X[r][c] = __builtin_fmaf(g, wv[c], X[r][c]);
       acc[c] = __builtin_fmaf(qq, X[r][c], acc[c]);
     }
+    if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) sm.op[w][lane + WAVE * c] = acc[c];
@@ -619,7 +636,7 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   // record are requested together with the metadata (one memory round trip)
   load_rows<DK, BF16>(rs, p, bh, p.tok0);
   stage_words<DV, false>(rec, L, L.wc * 32, words);   // the barrier in load_meta covers it
-  load_meta<DK>(rec, L, p.bmax, meta);
+  load_meta<DK, DV>(rec, L, p.bmax, meta);
   float X[ROW_BLOCK][DV / WAVE];
   unpack_cols<DK, DV>(words, meta, X);
   // EMA states of row t (threads t < DK): from the record, or fresh
@@ -786,7 +803,7 @@ __global__ void __launch_bounds__(2 * DK) k_unpack(KParams p, float* S, uint8_t*
   }
   const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
   __shared__ MetaSmem<DK> meta;
-  load_meta<DK>(rec, L, p.bmax, meta);
+  load_meta<DK, DV>(rec, L, p.bmax, meta);
   extern __shared__ uint4 dyn_lds[];
   stage_words<DV>(rec, L, meta.P[DK], (uint32_t*)dyn_lds);
   if (S) {

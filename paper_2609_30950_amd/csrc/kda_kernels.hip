@@ -109,19 +109,27 @@ __device__ __forceinline__ float in_f32(const void* base, size_t idx) {
   return ((const float*)base)[idx];
 }
 
-// Per-row scalars of token `tok` of head bh into LDS (threads t < DK).
+// Inputs of row t for the rate statistics: decay rate, key, beta.
+struct RowIn {
+  float s, k, beta;
+};
+
+// Per-row scalars of token `tok` of head bh into LDS (threads t < DK); returns
+// the row's own inputs for the rate statistics.
 template <int DK, bool BF16>
-__device__ __forceinline__ void load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
+__device__ __forceinline__ RowIn load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
   const int t = threadIdx.x;
+  RowIn in = {0.f, 0.f, 0.f};
   if (t < DK) {
     const int b = bh / p.H, h = bh % p.H;
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;       // (b, tok, h)
-    const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
-    const float beta = p.beta[th];
-    const float kv = in_f32<BF16>(p.k, th * DK + t);
-    rs.ak[t] = make_float2((float)exp(-(double)sv), kv);
-    rs.gq[t] = make_float2(beta * kv, in_f32<BF16>(p.q, th * DK + t));
+    in.s = p.per_head ? p.s[th] : p.s[th * DK + t];
+    in.beta = p.beta[th];
+    in.k = in_f32<BF16>(p.k, th * DK + t);
+    rs.ak[t] = make_float2((float)exp(-(double)in.s), in.k);
+    rs.gq[t] = make_float2(in.beta * in.k, in_f32<BF16>(p.q, th * DK + t));
   }
+  return in;
 }
 
 // Copy the meaningful code words of a record (ceil(sum b / 32) words per
@@ -168,9 +176,9 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
     }
     // finish row r before the reads of later rows are issued: the compiler
     // would otherwise keep every row's descriptor and words live at once
-    if (r % 2 == 1) {
+    if (r % 4 == 3) {
 #pragma unroll
-      for (int q = r - 1; q <= r; ++q)
+      for (int q = r - 3; q <= r; ++q)
 #pragma unroll
         for (int c = 0; c < CPL; ++c) asm volatile("" : "+v"(X[q][c])::"memory");
     }
@@ -579,27 +587,46 @@ __device__ __forceinline__ void store_meta(uint8_t* rec, const Layout& L, unsign
 // Row statistics of one write-back for one head (threads t < DK own row t).
 template <int DK>
 struct StatSmem {
-  float R[DK];
+  float R[DK];     // first member: 16-byte aligned with the struct
   double gam[DK];
   double rms[DK];
   double c[DK];
 };
 
+// Rate statistics of row t after the interval (threads t < DK): s^, r, the
+// weight Gamma^ (or the given window weight) and the stored rate codes.
 template <int DK>
-__device__ __forceinline__ void row_weights(const KParams& p, int bh, const MetaSmem<DK>& meta,
-                            StatSmem<DK>& st, double m_run, double e_run, int t) {
-  // m_run/e_run: EMA states of row t after the last token (thread t < DK)
+__device__ __forceinline__ void row_rates(const KParams& p, int bh, StatSmem<DK>& st, double m_run,
+                                          double e_run, int t) {
   if (t < DK) {
     const double s_hat = -0.5 * log(m_run);
     const double r = 0.5 * e_run;
     st.gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
-  __syncthreads();
+}
+
+// Weights c = Gamma R~^2 from the row ranges st.R (group RMS in float64,
+// rows summed in order).  The caller has synchronised after writing st.R.
+template <int DK>
+__device__ __forceinline__ void row_weights(const KParams& p, int bh, StatSmem<DK>& st, int t) {
   if (t < DK && t % p.G == 0) {
     double acc = 0.0;
-    for (int j = t; j < t + p.G; ++j) {
-      const double R = (double)st.R[j];
+    int j = 0;
+    if ((p.G & 3) == 0) {
+      // 16-byte reads issued ahead of the sequential sum (t is a multiple of 4)
+      const float4* R4 = (const float4*)(st.R + t);
+#pragma unroll 4
+      for (; j < p.G; j += 4) {
+        const float4 v = R4[j >> 2];
+        acc = acc + (double)v.x * (double)v.x;
+        acc = acc + (double)v.y * (double)v.y;
+        acc = acc + (double)v.z * (double)v.z;
+        acc = acc + (double)v.w * (double)v.w;
+      }
+    }
+    for (; j < p.G; ++j) {
+      const double R = (double)st.R[t + j];
       acc = acc + R * R;
     }
     st.rms[t / p.G] = sqrt(acc / (double)p.G);
@@ -629,34 +656,26 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   __shared__ MetaSmem<DK> meta;
   __shared__ RowSmem<DK> rs;
   __shared__ RecSmem<DK, DV> rsm;
-  __shared__ StatSmem<DK> st;
+  __shared__ __align__(16) StatSmem<DK> st;
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
   // the first token's row scalars and the whole code-word capacity of the
   // record are requested together with the metadata (one memory round trip)
-  load_rows<DK, BF16>(rs, p, bh, p.tok0);
+  RowIn in = load_rows<DK, BF16>(rs, p, bh, p.tok0);
   stage_words<DV, false>(rec, L, L.wc * 32, words);   // the barrier in load_meta covers it
   load_meta<DK, DV>(rec, L, p.bmax, meta);
-  float X[ROW_BLOCK][DV / WAVE];
-  unpack_cols<DK, DV>(words, meta, X);
-  // EMA states of row t (threads t < DK): from the record, or fresh
+  // EMA states of row t (threads t < DK): from the record, or fresh; token
+  // samples are folded in as soon as the token's inputs are loaded (float64
+  // work of the row threads that overlaps the other waves' decoding)
   bool fresh = meta.ntok == 0;
   double m_run = 0.0, e_run = 0.0;
   if (t < DK && !fresh) {
     m_run = exp(-2.0 * logq_decode(meta.z[t]));
     e_run = 2.0 * (double)f16_to_f32(meta.r16[t]);
   }
-  for (int j = 0; j < p.ntk; ++j) {
-    const int tok = p.tok0 + j;
-    if (j > 0) load_rows<DK, BF16>(rs, p, bh, tok);
-    __syncthreads();
-    const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV);
+  auto ema = [&](const RowIn& x) {
     if (t < DK) {
-      const float sv = p.per_head ? p.s[th] : p.s[th * DK + t];
-      const float kv = in_f32<BF16>(p.k, th * DK + t);
-      const float beta = p.beta[th];
-      const double zs = decay_sample(sv), ys = erase_sample(kv, beta);
+      const double zs = decay_sample(x.s), ys = erase_sample(x.k, x.beta);
       if (fresh) {
         m_run = zs;
         e_run = ys;
@@ -666,7 +685,18 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
       }
     }
     fresh = false;
+  };
+  ema(in);
+  float X[ROW_BLOCK][DV / WAVE];
+  unpack_cols<DK, DV>(words, meta, X);
+  for (int j = 0; j < p.ntk; ++j) {
+    const int tok = p.tok0 + j;
+    if (j > 0) ema(load_rows<DK, BF16>(rs, p, bh, tok));
+    __syncthreads();
+    const size_t th = ((size_t)b * p.T + tok) * p.H + h;
+    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV);
   }
+  row_rates<DK>(p, bh, st, m_run, e_run, t);
   {
     // float32 state after the last token, row-major, for the requantisation
     const int w = t / WAVE, lane = lane_id();
@@ -678,7 +708,7 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   }
   row_max<DK, DV>(X, st.R);
   __syncthreads();
-  row_weights<DK>(p, bh, meta, st, m_run, e_run, t);
+  row_weights<DK>(p, bh, st, t);
   if constexpr (HEAD) {
     // per-head budget: allocate here (c of this head is in LDS)
     __shared__ AllocSmem asm_;
@@ -828,22 +858,11 @@ __global__ void __launch_bounds__(DK) k_weights_from_ranges(KParams p, const dou
                                                             const float* R) {
   const int bh = blockIdx.x;
   const int t = threadIdx.x;
-  __shared__ StatSmem<DK> st;
+  __shared__ __align__(16) StatSmem<DK> st;
   st.R[t] = R[(size_t)bh * DK + t];
   st.gam[t] = gamma[(size_t)bh * DK + t];
   __syncthreads();
-  if (t % p.G == 0) {
-    double acc = 0.0;
-    for (int j = t; j < t + p.G; ++j) {
-      const double v = (double)st.R[j];
-      acc = acc + v * v;
-    }
-    st.rms[t / p.G] = sqrt(acc / (double)p.G);
-  }
-  __syncthreads();
-  const double rms = st.rms[t / p.G];
-  const double Rt = rms > 0.0 ? (double)st.R[t] / rms : 0.0;
-  p.ws_c[(size_t)bh * DK + t] = st.gam[t] * (Rt * Rt);
+  row_weights<DK>(p, bh, st, t);
 }
 
 // Windowed Gramian weights: one thread per (b, h, row), sequential in time.

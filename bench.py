@@ -97,17 +97,126 @@ def cpu_baseline(name, budget_s=12.0, warm_tokens=32):
                        f"{w.dk}x{w.dv} states), float32-contract oracle, one thread")
 
 
+def run_state32_reference(w, args, K, torch):
+    """The same decode step in 32-bit mode (float32 state records, no
+    quantiser): the memory-side reference of the step."""
+    cfg = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, state32=1)
+    L = args.layers
+    base = W.base_rates(w)
+    n_tok = args.warmup + args.steps
+    toks = [{n: torch.from_numpy(a).cuda() for n, a in W.token(w, 1000 + t, base=base).items()}
+            for t in range(n_tok)]
+    layers = torch.zeros(L, K.record_bytes(cfg) * w.B * w.H, dtype=torch.uint8, device="cuda")
+    o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+
+    def run(i):
+        x = toks[i]
+        K.kda_step(cfg, layers[i % L], x["q"], x["k"], x["v"], x["s"], x["beta"], o, None)
+
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for i in range(args.warmup, n_tok):
+        run(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    nbh = w.B * w.H
+    step_bytes = nbh * (2 * w.dk * w.dv * 4 + 4 * (3 * w.dk + w.dv) + 4 + 4 * w.dv)
+    del layers
+    return dict(ms_per_step=ms, value=nbh / (ms * 1e-3), unit="state-tokens/s",
+                hbm_GBps=step_bytes / (ms * 1e-3) / 1e9,
+                hbm_frac=step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, bytes_per_step=step_bytes)
+
+
+def run_prefill(args, K, torch):
+    """Prefill of the bf16 workload (B=4 H=32 d=128 T=8192, write-back every
+    64 tokens) from the empty state: one kda_prefill call per pass."""
+    w = W.WORKLOADS["prefill"]
+    cfg = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                   b_min=w.b_min, b_max=w.b_max)
+    t0 = time.time()
+    xs = W.tokens(w, 0, w.T)
+    print(f"# prefill inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    dev = {n: torch.from_numpy(np.ascontiguousarray(xs[n])).cuda() for n in ("s", "beta")}
+    for n in ("q", "k", "v"):
+        dev[n] = torch.from_numpy(np.ascontiguousarray(xs[n])).to(torch.bfloat16).cuda()
+    del xs
+    recs = K.new_records(cfg)
+    ws = K.new_workspace(cfg)
+    o = torch.zeros(w.B * w.T * w.H * w.dv, dtype=torch.float32, device="cuda")
+
+    def run():
+        recs.zero_()
+        K.kda_prefill(cfg, w.T, w.C, recs, dev["q"], dev["k"], dev["v"], dev["s"], dev["beta"], o, ws)
+
+    run()
+    torch.cuda.synchronize()
+    K.kda_profile_enable(K.api.PROFILE_EVENTS)
+    K.kda_profile_read()
+    run()
+    torch.cuda.synchronize()
+    prof = K.kda_profile_read()
+    K.kda_profile_enable(0)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    reps = max(1, args.steps // 20)
+    ev0.record()
+    for _ in range(reps):
+        run()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / reps
+    nbh = w.B * w.H
+    head_tok = 3 * 2 * w.dk + 4 * w.dk + 4 + 4 * w.dv          # q, k, v bf16; s; beta; o
+    meta = 16 + w.dk // 2 + 6 * w.dk
+    wb = -(-w.T // w.C)
+    rec_bytes = 2 * wb * nbh * (meta + w.mean_bits * w.dk * w.dv / 8)
+    total = nbh * w.T * head_tok + rec_bytes
+    kern = {k: dict(ms_avg=v[0] / v[1], launches=v[1]) for k, v in prof.items()}
+    # recurrence lane-ops: a S, k.S', S + g w, q.S per element and token
+    rec_ops = 4.0 * nbh * w.T * w.dk * w.dv
+    t_stats = prof["stats"][0] * 1e-3 if "stats" in prof else None
+    out = {
+        "metric": "state-tokens/s (B·H·T), KDA prefill w/ 4-bit mixed state (write-back every 64)",
+        "value": nbh * w.T / (ms * 1e-3),
+        "unit": "state-tokens/s",
+        "n_gpus": 1, "steps": reps, "warmup": 1, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"prefill B={w.B} H={w.H} d_k=d_v={w.dk} T={w.T} C={w.C}, bf16 "
+                               f"q/k/v, mean {w.mean_bits} bits, widths [{w.b_min},{w.b_max}], "
+                               f"groups of {w.G} rows, layer budget, from the empty state"},
+        "hbm_GBps_step": total / (ms * 1e-3) / 1e9,
+        "hbm_frac_step": total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "bytes_per_step": total,
+        "kernels": kern,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if t_stats:
+        ach = rec_ops / t_stats / 1e12
+        out["roofline"] = dict(bound="alu", achieved=ach, peak=VALU_PEAK_TOPS, unit="TOP/s",
+                               frac=ach / VALU_PEAK_TOPS, traffic=committed_traffic("stats", "prefill"),
+                               kernel="stats", lane_ops_per_pass=rec_ops)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode", choices=["decode"])
+    ap.add_argument("--workload", default="decode", choices=["decode", "prefill"])
     ap.add_argument("--layers", type=int, default=20)
     ap.add_argument("--warm-tokens", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-count-pass", action="store_true",
                     help="skip the untimed counting replay (e.g. under a profiler)")
+    ap.add_argument("--no-ref32", action="store_true",
+                    help="skip the 32-bit-mode reference step")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -120,6 +229,9 @@ def main():
     import paper_2609_30950_amd as K
 
     torch.cuda.set_device(0)
+    if args.workload == "prefill":
+        run_prefill(args, K, torch)
+        return
     cfg = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
                    b_min=w.b_min, b_max=w.b_max)
     ws = K.new_workspace(cfg)
@@ -238,6 +350,9 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
         "roofline": roof,
     }
+    if not args.no_ref32:
+        del layers
+        out["state32_reference"] = run_state32_reference(w, args, K, torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload)
     print(json.dumps(out), flush=True)

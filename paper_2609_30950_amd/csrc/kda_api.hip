@@ -15,7 +15,7 @@ namespace {
 using kda::KParams;
 
 struct WsLayout {
-  size_t c_off, zr_off, bits_off, s32_off, total;
+  size_t c_off, zr_off, bits_off, s32_off, rpart_off, gam_off, total;
 };
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
@@ -27,7 +27,10 @@ WsLayout ws_layout(const kda_config* cfg) {
   w.zr_off = up256(w.c_off + rows * sizeof(double));
   w.bits_off = up256(w.zr_off + rows * sizeof(uint32_t));
   w.s32_off = up256(w.bits_off + rows);
-  w.total = up256(w.s32_off + rows * (size_t)cfg->d_v * sizeof(float));
+  // prefill: per-slice row maxima (d_v / 64 slices) and the rows' weights Gamma
+  w.rpart_off = up256(w.s32_off + rows * (size_t)cfg->d_v * sizeof(float));
+  w.gam_off = up256(w.rpart_off + rows * (size_t)(cfg->d_v / 64) * sizeof(float));
+  w.total = up256(w.gam_off + rows * sizeof(double));
   return w;
 }
 
@@ -90,6 +93,8 @@ void set_ws(KParams& p, const kda_config* cfg, void* ws) {
   p.ws_zr = (uint32_t*)(base + w.zr_off);
   p.ws_bits = base + w.bits_off;
   p.ws_s32 = (float*)(base + w.s32_off);
+  p.ws_rpart = (float*)(base + w.rpart_off);
+  p.ws_gam = (double*)(base + w.gam_off);
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KDA_OK : KDA_ERR_HIP; }

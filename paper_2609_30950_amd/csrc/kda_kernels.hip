@@ -891,6 +891,249 @@ __global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head
   gamma[id] = acc / (double)W;
 }
 
+// ------------------------------------------ prefill: column slices ---
+//
+// A prefill chunk (tokens [tok0, tok0 + ntk)) runs d_v / 64 blocks per head,
+// one per 64-column slice: the recurrence couples the rows of a column but
+// never two columns, so the slices are independent until the write-back.
+// Each block keeps its d_k x 64 slice in registers (wave w: rows 32w..32w+31,
+// lane: column) and stages the row scalars of PF_TS tokens at a time in LDS,
+// the float64 exponentials of all (token, row) pairs computed by all threads.
+// It synchronises once per token (partial sums of u double-buffered by token
+// parity) and combines the outputs of the staged tokens together.  Slice 0
+// also carries the EMA statistics.  Row maxima leave per slice;
+// k_alloc_slices combines them into the weights and allocates.
+
+constexpr int SLICE = 64;
+
+template <int DK>
+constexpr int pf_tokens() { return DK > 128 ? 8 : 16; }
+
+template <int DK>
+struct PfSmem {
+  static constexpr int TS = pf_tokens<DK>();
+  static constexpr int NW = DK / ROW_BLOCK;
+  float4 rq[TS][DK];        // {fl32(exp(-s)), k, fl32(beta k), q} of (token, row)
+  double z[TS][DK];         // exp(-2 s): EMA decay samples (slice 0)
+  float beta[TS];
+  float v[TS][SLICE];
+  float up[2][NW][SLICE];   // partial sums of u, by token parity
+  float op[TS][NW][SLICE];  // partial sums of o
+};
+
+// Row scalars reach the lanes by DPP row broadcasts folded into the
+// arithmetic: lane l of wave w holds the scalars of rows 32w + l % 16 (block
+// 0) and 32w + 16 + l % 16 (block 1), replicated in the four 16-lane rows,
+// and row_newbcast:r hands lane r's value of each 16-lane row to all of its
+// lanes as the first operand.  Sixteen rows per asm block; the leading s_nop
+// covers a vector write of a broadcast source just before the block.
+#define KDA_P1(r)                                                                   \
+  "v_mul_f32_dpp %" #r ", %17, %" #r " row_newbcast:" #r                           \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
+  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+#define KDA_P2(r)                                                                   \
+  "v_fmac_f32_dpp %" #r ", %17, %19 row_newbcast:" #r                              \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
+  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+#define KDA_X16(X, o)                                                                \
+  "+v"(X[o + 0][0]), "+v"(X[o + 1][0]), "+v"(X[o + 2][0]), "+v"(X[o + 3][0]),       \
+      "+v"(X[o + 4][0]), "+v"(X[o + 5][0]), "+v"(X[o + 6][0]), "+v"(X[o + 7][0]),   \
+      "+v"(X[o + 8][0]), "+v"(X[o + 9][0]), "+v"(X[o + 10][0]), "+v"(X[o + 11][0]), \
+      "+v"(X[o + 12][0]), "+v"(X[o + 13][0]), "+v"(X[o + 14][0]), "+v"(X[o + 15][0])
+
+// First pass over 16 rows: X_r = a_r X_r; acc = fma(k_r, X_r, acc) in row order.
+template <int O>
+__device__ __forceinline__ void pass1_16(float (&X)[ROW_BLOCK][1], float& acc, float A, float K) {
+  asm("s_nop 1\n" KDA_P1(0) KDA_P1(1) KDA_P1(2) KDA_P1(3) KDA_P1(4) KDA_P1(5) KDA_P1(6) KDA_P1(7)
+      KDA_P1(8) KDA_P1(9) KDA_P1(10) KDA_P1(11) KDA_P1(12) KDA_P1(13) KDA_P1(14) KDA_P1(15)
+      : KDA_X16(X, O), "+v"(acc)
+      : "v"(A), "v"(K));
+}
+
+// Second pass over 16 rows: X_r = fma(g_r, w, X_r); acc = fma(q_r, X_r, acc).
+template <int O>
+__device__ __forceinline__ void pass2_16(float (&X)[ROW_BLOCK][1], float& acc, float G, float Q,
+                                         float wv) {
+  asm("s_nop 1\n" KDA_P2(0) KDA_P2(1) KDA_P2(2) KDA_P2(3) KDA_P2(4) KDA_P2(5) KDA_P2(6) KDA_P2(7)
+      KDA_P2(8) KDA_P2(9) KDA_P2(10) KDA_P2(11) KDA_P2(12) KDA_P2(13) KDA_P2(14) KDA_P2(15)
+      : KDA_X16(X, O), "+v"(acc)
+      : "v"(G), "v"(Q), "v"(wv));
+}
+
+// One token on a slice (lane = column): the column-layout recurrence with
+// the row scalars of staged token j.  One barrier (before the u combine).
+template <int DK>
+__device__ __forceinline__ void recur_slice(float (&X)[ROW_BLOCK][1], PfSmem<DK>& ps, int j) {
+  const int w = threadIdx.x / WAVE, lane = lane_id();
+  const float4 s0 = ps.rq[j][w * ROW_BLOCK + (lane & 15)];
+  const float4 s1 = ps.rq[j][w * ROW_BLOCK + 16 + (lane & 15)];
+  float acc = 0.f;
+  pass1_16<0>(X, acc, s0.x, s0.y);
+  pass1_16<16>(X, acc, s1.x, s1.y);
+  ps.up[j & 1][w][lane] = acc;
+  __syncthreads();
+  const float u = combine_col<DK, SLICE>(ps.up[j & 1], lane);
+  const float wv = ps.v[j][lane] - u;
+  acc = 0.f;
+  pass2_16<0>(X, acc, s0.z, s0.w, wv);
+  pass2_16<16>(X, acc, s1.z, s1.w, wv);
+  ps.op[j][w][lane] = acc;
+}
+
+template <int DK, bool BF16>
+__global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
+  constexpr int TS = pf_tokens<DK>();
+  const int nsl = p.dv / SLICE;
+  const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
+  const int t = threadIdx.x;
+  const int b = bh / p.H, h = bh % p.H;
+  const Layout L = p.L;
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ PfSmem<DK> ps;
+  __shared__ float Rrow[DK];
+  extern __shared__ uint4 dyn_lds[];
+  uint32_t* words = (uint32_t*)dyn_lds;
+  {
+    // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
+    const uint4* src = (const uint4*)(rec + L.codes_off);
+    constexpr int Q = SLICE / 4;
+    const int n4 = L.wc * Q;
+    for (int e = t; e < n4; e += blockDim.x)
+      ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
+  }
+  load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
+  float X[ROW_BLOCK][1];
+  unpack_cols<DK, SLICE>(words, meta, X);
+  const bool ema_here = sl == 0 && t < DK;
+  const bool fresh0 = meta.ntok == 0;
+  double m_run = 0.0, e_run = 0.0;
+  if (ema_here && !fresh0) {
+    m_run = exp(-2.0 * logq_decode(meta.z[t]));
+    e_run = 2.0 * (double)f16_to_f32(meta.r16[t]);
+  }
+  for (int j0 = 0; j0 < p.ntk; j0 += TS) {
+    const int nt = min(TS, p.ntk - j0);
+    __syncthreads();   // the previous tokens' readers are done with the tables
+    {
+      // thread t stages row t % DK of tokens 2q + t / DK (all loads first)
+      constexpr int NQ = TS / 2;
+      const int i = t % DK, jt = t / DK;
+      float sv[NQ], kv[NQ], qv[NQ], bt[NQ];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int j = 2 * q + jt;
+        const size_t th = ((size_t)b * p.T + p.tok0 + j0 + min(j, nt - 1)) * p.H + h;
+        sv[q] = p.per_head ? p.s[th] : p.s[th * DK + i];
+        kv[q] = in_f32<BF16>(p.k, th * DK + i);
+        qv[q] = in_f32<BF16>(p.q, th * DK + i);
+        bt[q] = p.beta[th];
+      }
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int j = 2 * q + jt;
+        if (j < nt) {
+          ps.rq[j][i] = make_float4((float)exp(-(double)sv[q]), kv[q], bt[q] * kv[q], qv[q]);
+          if (sl == 0) ps.z[j][i] = decay_sample(sv[q]);
+          if (i == 0) ps.beta[j] = bt[q];
+        }
+      }
+    }
+    for (int e = t; e < nt * SLICE; e += blockDim.x) {
+      const int j = e / SLICE, c = e % SLICE;
+      const size_t th = ((size_t)b * p.T + p.tok0 + j0 + j) * p.H + h;
+      ps.v[j][c] = in_f32<BF16>(p.v, th * p.dv + sl * SLICE + c);
+    }
+    __syncthreads();
+    if (ema_here) {
+      // token-sequential EMA of row t (the first token initialises a fresh record)
+      for (int j = 0; j < nt; ++j) {
+        const double zs = ps.z[j][t], ys = erase_sample(ps.rq[j][t].y, ps.beta[j]);
+        if (fresh0 && j0 + j == 0) {
+          m_run = zs;
+          e_run = ys;
+        } else {
+          m_run = p.one_minus_alpha * m_run + p.alpha * zs;
+          e_run = p.one_minus_alpha * e_run + p.alpha * ys;
+        }
+      }
+    }
+    for (int j = 0; j < nt; ++j) recur_slice<DK>(X, ps, j);
+    __syncthreads();
+    for (int e = t; e < nt * SLICE; e += blockDim.x) {
+      const int j = e / SLICE, c = e % SLICE;
+      const size_t th = ((size_t)b * p.T + p.tok0 + j0 + j) * p.H + h;
+      p.o[th * p.dv + sl * SLICE + c] = combine_col<DK, SLICE>(ps.op[j], c);
+    }
+  }
+  {
+    // float32 state after the chunk (this slice's columns), row-major
+    const int w = t / WAVE, lane = lane_id();
+    float* dstS = p.ws_s32 + (size_t)bh * DK * p.dv + sl * SLICE;
+#pragma unroll
+    for (int r = 0; r < ROW_BLOCK; ++r) dstS[(size_t)(w * ROW_BLOCK + r) * p.dv + lane] = X[r][0];
+  }
+  row_max<DK, SLICE>(X, Rrow);
+  __syncthreads();
+  if (t < DK) p.ws_rpart[((size_t)bh * DK + t) * nsl + sl] = Rrow[t];
+  if (ema_here) {
+    const double s_hat = -0.5 * log(m_run);
+    const double r = 0.5 * e_run;
+    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
+  }
+}
+
+// Weights of the rows of one scope unit from the per-slice row maxima and
+// Gamma (group RMS in float64, rows summed in order), then the allocation.
+__global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl) {
+  __shared__ AllocSmem sm;
+  __shared__ __align__(16) float R[ALLOC_MAX_N];
+  __shared__ double rms[ALLOC_MAX_N];
+  __shared__ double c[ALLOC_MAX_N];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const size_t row0 = (size_t)blockIdx.x * N;
+  for (int n = tid; n < N; n += nt) {
+    const float* rp = p.ws_rpart + (row0 + n) * nsl;
+    float m = rp[0];
+    for (int q = 1; q < nsl; ++q) m = fmaxf(m, rp[q]);
+    R[n] = m;
+  }
+  __syncthreads();
+  const int G = p.G;
+  for (int g = tid; g < N / G; g += nt) {
+    double acc = 0.0;
+    const int r0 = g * G;
+    int j = 0;
+    if ((G & 3) == 0) {
+      const float4* R4 = (const float4*)(R + r0);
+#pragma unroll 4
+      for (; j < G; j += 4) {
+        const float4 v = R4[j >> 2];
+        acc = acc + (double)v.x * (double)v.x;
+        acc = acc + (double)v.y * (double)v.y;
+        acc = acc + (double)v.z * (double)v.z;
+        acc = acc + (double)v.w * (double)v.w;
+      }
+    }
+    for (; j < G; ++j) {
+      const double v = (double)R[r0 + j];
+      acc = acc + v * v;
+    }
+    rms[g] = sqrt(acc / (double)G);
+  }
+  __syncthreads();
+  for (int n = tid; n < N; n += nt) {
+    const double rm = rms[n / G];
+    const double Rt = rm > 0.0 ? (double)R[n] / rm : 0.0;
+    c[n] = p.ws_gam[row0 + n] * (Rt * Rt);
+  }
+  __syncthreads();
+  block_allocate([&](int n) { return c[n]; }, N, p.need, p.bmin, p.bmax, p.ws_bits + row0, sm);
+}
+
 // ------------------------------------------------------- launchers ---
 
 // One write-back interval: tokens [p.tok0, p.tok0 + p.ntk), then quantise.
@@ -942,6 +1185,35 @@ static hipError_t launch_interval(const KParams& p, hipStream_t st) {
 
 hipError_t launch_step(const KParams& p, hipStream_t st) { return launch_interval(p, st); }
 
+// One prefill write-back interval on column slices: stats per slice, weights
+// and allocation per scope unit, then the requantisation.
+template <int DK>
+static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
+  const int nsl = p.dv / SLICE;
+  hipError_t e;
+  {
+    ProfScope ps("stats", st);
+    const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
+    if (p.in_bf16)
+      k_chunk_slices<DK, true><<<p.B * p.H * nsl, 2 * DK, dyn, st>>>(p);
+    else
+      k_chunk_slices<DK, false><<<p.B * p.H * nsl, 2 * DK, dyn, st>>>(p);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  {
+    ProfScope ps("alloc", st);
+    const int units = p.scope == 0 ? p.B : p.B * p.H;
+    const int N = p.scope == 0 ? p.H * DK : DK;
+    k_alloc_slices<<<units, 1024, 0, st>>>(p, N, nsl);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  ProfScope ps("requant", st);
+  k_requant<DK, DK><<<p.B * p.H, 2 * DK, 0, st>>>(p);
+  return hipGetLastError();
+}
+
 hipError_t launch_prefill(KParams p, int C, hipStream_t st) {
   if (p.state32) {
     p.tok0 = 0;
@@ -951,7 +1223,13 @@ hipError_t launch_prefill(KParams p, int C, hipStream_t st) {
   for (int t0 = 0; t0 < p.T; t0 += C) {
     p.tok0 = t0;
     p.ntk = (p.T - t0) < C ? (p.T - t0) : C;
-    hipError_t e = launch_interval(p, st);
+    hipError_t e;
+    if (p.dk == 64)
+      e = launch_interval_slices<64>(p, st);
+    else if (p.dk == 256)
+      e = launch_interval_slices<256>(p, st);
+    else
+      e = launch_interval_slices<128>(p, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

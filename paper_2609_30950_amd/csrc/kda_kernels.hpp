@@ -30,6 +30,8 @@ struct KParams {
   uint32_t* ws_zr;
   uint8_t* ws_bits;
   float* ws_s32;            // float32 state after the token, [B][H][dk][dv]
+  float* ws_rpart;          // prefill: row maxima per 64-column slice, [B][H][dk][dv/64]
+  double* ws_gam;           // prefill: row weights Gamma, [B][H][dk]
   unsigned long long* diag_fit;  // profiling: candidate evaluations (or null)
 };
 

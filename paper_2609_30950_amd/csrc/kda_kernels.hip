@@ -185,6 +185,49 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
   }
 }
 
+// Row scalars reach the lanes by DPP row broadcasts folded into the
+// arithmetic: lane l of wave w holds the scalars of rows 32w + l % 16 (block
+// 0) and 32w + 16 + l % 16 (block 1), replicated in the four 16-lane rows,
+// and row_newbcast:r hands lane r's value of each 16-lane row to all of its
+// lanes as the first operand.  Sixteen rows per asm block; the leading s_nop
+// covers a vector write of a broadcast source just before the block.
+#define KDA_P1(r)                                                                   \
+  "v_mul_f32_dpp %" #r ", %17, %" #r " row_newbcast:" #r                           \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
+  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+#define KDA_P2(r)                                                                   \
+  "v_fmac_f32_dpp %" #r ", %17, %19 row_newbcast:" #r                              \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
+  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+#define KDA_X16(X, o, c)                                                             \
+  "+v"(X[o + 0][c]), "+v"(X[o + 1][c]), "+v"(X[o + 2][c]), "+v"(X[o + 3][c]),       \
+      "+v"(X[o + 4][c]), "+v"(X[o + 5][c]), "+v"(X[o + 6][c]), "+v"(X[o + 7][c]),   \
+      "+v"(X[o + 8][c]), "+v"(X[o + 9][c]), "+v"(X[o + 10][c]), "+v"(X[o + 11][c]), \
+      "+v"(X[o + 12][c]), "+v"(X[o + 13][c]), "+v"(X[o + 14][c]), "+v"(X[o + 15][c])
+
+// First pass over rows O..O+15 of column C: X_r = a_r X_r; acc = fma(k_r, X_r, acc)
+// in row order.
+template <int O, int C, int CPL>
+__device__ __forceinline__ void pass1_16(float (&X)[ROW_BLOCK][CPL], float& acc, float A, float K) {
+  asm("s_nop 1\n" KDA_P1(0) KDA_P1(1) KDA_P1(2) KDA_P1(3) KDA_P1(4) KDA_P1(5) KDA_P1(6) KDA_P1(7)
+      KDA_P1(8) KDA_P1(9) KDA_P1(10) KDA_P1(11) KDA_P1(12) KDA_P1(13) KDA_P1(14) KDA_P1(15)
+      : KDA_X16(X, O, C), "+v"(acc)
+      : "v"(A), "v"(K));
+}
+
+// Second pass over rows O..O+15 of column C: X_r = fma(g_r, w, X_r);
+// acc = fma(q_r, X_r, acc).
+template <int O, int C, int CPL>
+__device__ __forceinline__ void pass2_16(float (&X)[ROW_BLOCK][CPL], float& acc, float G, float Q,
+                                         float wv) {
+  asm("s_nop 1\n" KDA_P2(0) KDA_P2(1) KDA_P2(2) KDA_P2(3) KDA_P2(4) KDA_P2(5) KDA_P2(6) KDA_P2(7)
+      KDA_P2(8) KDA_P2(9) KDA_P2(10) KDA_P2(11) KDA_P2(12) KDA_P2(13) KDA_P2(14) KDA_P2(15)
+      : KDA_X16(X, O, C), "+v"(acc)
+      : "v"(G), "v"(Q), "v"(wv));
+}
+
 template <int DK, int DV>
 struct RecSmem {
   float up[DK / ROW_BLOCK][DV];
@@ -213,25 +256,28 @@ template <int DK, int DV, bool BF16>
 __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
                             RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out) {
   constexpr int CPL = DV / WAVE;
+  static_assert(CPL <= 4, "columns per lane");
   const int w = threadIdx.x / WAVE, lane = lane_id();
-  const float2* ak = rs.ak + w * ROW_BLOCK;   // row scalars: LDS broadcast reads
-  const float2* gq = rs.gq + w * ROW_BLOCK;
+  // row scalars of rows 32w + lane % 16 and 32w + 16 + lane % 16 (DPP sources)
+  const float2 ak0 = rs.ak[w * ROW_BLOCK + (lane & 15)], ak1 = rs.ak[w * ROW_BLOCK + 16 + (lane & 15)];
+  const float2 gq0 = rs.gq[w * ROW_BLOCK + (lane & 15)], gq1 = rs.gq[w * ROW_BLOCK + 16 + (lane & 15)];
   float vin[CPL];   // this lane's columns of v, loaded before the row sweep
 #pragma unroll
   for (int c = 0; c < CPL; ++c) vin[c] = in_f32<BF16>(v, v_off + lane + WAVE * c);
   float acc[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
-#pragma unroll
-  for (int r = 0; r < ROW_BLOCK; ++r) {
-    const float2 x = ak[r];
-    const float a = x.x, kk = x.y;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      X[r][c] = a * X[r][c];
-      acc[c] = __builtin_fmaf(kk, X[r][c], acc[c]);
-    }
-    if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+  pass1_16<0, 0, CPL>(X, acc[0], ak0.x, ak0.y);
+  pass1_16<16, 0, CPL>(X, acc[0], ak1.x, ak1.y);
+  if constexpr (CPL > 1) {
+    pass1_16<0, 1, CPL>(X, acc[1], ak0.x, ak0.y);
+    pass1_16<16, 1, CPL>(X, acc[1], ak1.x, ak1.y);
+  }
+  if constexpr (CPL > 2) {
+    pass1_16<0, 2, CPL>(X, acc[2], ak0.x, ak0.y);
+    pass1_16<16, 2, CPL>(X, acc[2], ak1.x, ak1.y);
+    pass1_16<0, 3, CPL>(X, acc[3], ak0.x, ak0.y);
+    pass1_16<16, 3, CPL>(X, acc[3], ak1.x, ak1.y);
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) sm.up[w][lane + WAVE * c] = acc[c];
@@ -244,16 +290,17 @@ __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], co
     wv[c] = vin[c] - u;
     acc[c] = 0.f;
   }
-#pragma unroll
-  for (int r = 0; r < ROW_BLOCK; ++r) {
-    const float2 x = gq[r];
-    const float g = x.x, qq = x.y;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      X[r][c] = __builtin_fmaf(g, wv[c], X[r][c]);
-      acc[c] = __builtin_fmaf(qq, X[r][c], acc[c]);
-    }
-    if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+  pass2_16<0, 0, CPL>(X, acc[0], gq0.x, gq0.y, wv[0]);
+  pass2_16<16, 0, CPL>(X, acc[0], gq1.x, gq1.y, wv[0]);
+  if constexpr (CPL > 1) {
+    pass2_16<0, 1, CPL>(X, acc[1], gq0.x, gq0.y, wv[1]);
+    pass2_16<16, 1, CPL>(X, acc[1], gq1.x, gq1.y, wv[1]);
+  }
+  if constexpr (CPL > 2) {
+    pass2_16<0, 2, CPL>(X, acc[2], gq0.x, gq0.y, wv[2]);
+    pass2_16<16, 2, CPL>(X, acc[2], gq1.x, gq1.y, wv[2]);
+    pass2_16<0, 3, CPL>(X, acc[3], gq0.x, gq0.y, wv[3]);
+    pass2_16<16, 3, CPL>(X, acc[3], gq1.x, gq1.y, wv[3]);
   }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) sm.op[w][lane + WAVE * c] = acc[c];
@@ -921,47 +968,6 @@ struct PfSmem {
   float op[TS][NW][SLICE];  // partial sums of o
 };
 
-// Row scalars reach the lanes by DPP row broadcasts folded into the
-// arithmetic: lane l of wave w holds the scalars of rows 32w + l % 16 (block
-// 0) and 32w + 16 + l % 16 (block 1), replicated in the four 16-lane rows,
-// and row_newbcast:r hands lane r's value of each 16-lane row to all of its
-// lanes as the first operand.  Sixteen rows per asm block; the leading s_nop
-// covers a vector write of a broadcast source just before the block.
-#define KDA_P1(r)                                                                   \
-  "v_mul_f32_dpp %" #r ", %17, %" #r " row_newbcast:" #r                           \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
-  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
-#define KDA_P2(r)                                                                   \
-  "v_fmac_f32_dpp %" #r ", %17, %19 row_newbcast:" #r                              \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
-  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
-#define KDA_X16(X, o)                                                                \
-  "+v"(X[o + 0][0]), "+v"(X[o + 1][0]), "+v"(X[o + 2][0]), "+v"(X[o + 3][0]),       \
-      "+v"(X[o + 4][0]), "+v"(X[o + 5][0]), "+v"(X[o + 6][0]), "+v"(X[o + 7][0]),   \
-      "+v"(X[o + 8][0]), "+v"(X[o + 9][0]), "+v"(X[o + 10][0]), "+v"(X[o + 11][0]), \
-      "+v"(X[o + 12][0]), "+v"(X[o + 13][0]), "+v"(X[o + 14][0]), "+v"(X[o + 15][0])
-
-// First pass over 16 rows: X_r = a_r X_r; acc = fma(k_r, X_r, acc) in row order.
-template <int O>
-__device__ __forceinline__ void pass1_16(float (&X)[ROW_BLOCK][1], float& acc, float A, float K) {
-  asm("s_nop 1\n" KDA_P1(0) KDA_P1(1) KDA_P1(2) KDA_P1(3) KDA_P1(4) KDA_P1(5) KDA_P1(6) KDA_P1(7)
-      KDA_P1(8) KDA_P1(9) KDA_P1(10) KDA_P1(11) KDA_P1(12) KDA_P1(13) KDA_P1(14) KDA_P1(15)
-      : KDA_X16(X, O), "+v"(acc)
-      : "v"(A), "v"(K));
-}
-
-// Second pass over 16 rows: X_r = fma(g_r, w, X_r); acc = fma(q_r, X_r, acc).
-template <int O>
-__device__ __forceinline__ void pass2_16(float (&X)[ROW_BLOCK][1], float& acc, float G, float Q,
-                                         float wv) {
-  asm("s_nop 1\n" KDA_P2(0) KDA_P2(1) KDA_P2(2) KDA_P2(3) KDA_P2(4) KDA_P2(5) KDA_P2(6) KDA_P2(7)
-      KDA_P2(8) KDA_P2(9) KDA_P2(10) KDA_P2(11) KDA_P2(12) KDA_P2(13) KDA_P2(14) KDA_P2(15)
-      : KDA_X16(X, O), "+v"(acc)
-      : "v"(G), "v"(Q), "v"(wv));
-}
-
 // One token on a slice (lane = column): the column-layout recurrence with
 // the row scalars of staged token j.  One barrier (before the u combine).
 template <int DK>
@@ -970,15 +976,15 @@ __device__ __forceinline__ void recur_slice(float (&X)[ROW_BLOCK][1], PfSmem<DK>
   const float4 s0 = ps.rq[j][w * ROW_BLOCK + (lane & 15)];
   const float4 s1 = ps.rq[j][w * ROW_BLOCK + 16 + (lane & 15)];
   float acc = 0.f;
-  pass1_16<0>(X, acc, s0.x, s0.y);
-  pass1_16<16>(X, acc, s1.x, s1.y);
+  pass1_16<0, 0, 1>(X, acc, s0.x, s0.y);
+  pass1_16<16, 0, 1>(X, acc, s1.x, s1.y);
   ps.up[j & 1][w][lane] = acc;
   __syncthreads();
   const float u = combine_col<DK, SLICE>(ps.up[j & 1], lane);
   const float wv = ps.v[j][lane] - u;
   acc = 0.f;
-  pass2_16<0>(X, acc, s0.z, s0.w, wv);
-  pass2_16<16>(X, acc, s1.z, s1.w, wv);
+  pass2_16<0, 0, 1>(X, acc, s0.z, s0.w, wv);
+  pass2_16<16, 0, 1>(X, acc, s1.z, s1.w, wv);
   ps.op[j][w][lane] = acc;
 }
 

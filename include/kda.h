@@ -147,6 +147,25 @@ int kda_step(const kda_config* cfg, void* records, const float* q,
              const float* k, const float* v, const float* s, const float* beta,
              const double* gamma, float* o, void* ws, void* stream);
 
+/* kda_step in two phases, for callers that overlap a layer's write-back with
+ * later work (the outputs precede the quantisation, Sec. 2, so the next
+ * layer needs only the first phase).
+ * kda_step_outputs: the token's recurrence, outputs o, rate statistics,
+ *   weights and widths; the float32 state after the token is left in ws.
+ *   Records are only read.  Arguments as kda_step.
+ * kda_step_writeback: quantise the state left in ws with those widths and
+ *   rewrite the records in place.  Must follow kda_step_outputs of the same
+ *   records and ws (stream order or an event), before ws or the records are
+ *   used by another call.  Not available in 32-bit mode (kda_step_outputs
+ *   then does the whole step and kda_step_writeback returns KDA_OK).
+ * kda_step(...) is kda_step_outputs(...) then kda_step_writeback(...) on one
+ * stream. */
+int kda_step_outputs(const kda_config* cfg, void* records, const float* q,
+                     const float* k, const float* v, const float* s,
+                     const float* beta, const double* gamma, float* o, void* ws,
+                     void* stream);
+int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* stream);
+
 /* Prefill of T tokens with a write-back after every C-th token and after the
  * last one (Sec. 2: once per prefill chunk).
  * In:  q, k [B][T][H][d_k] bf16 (raw 16-bit patterns); v [B][T][H][d_v] bf16;

@@ -128,6 +128,24 @@ def kda_step(cfg, records, q, k, v, s, beta, o, ws, gamma=None):
         _stream()))
 
 
+def kda_step_outputs(cfg, records, q, k, v, s, beta, o, ws, gamma=None):
+    n_s = cfg.B * cfg.H * (1 if cfg.decay_per_head else cfg.d_k)
+    _check(load().kda_step_outputs(
+        ctypes.byref(cfg.c()), _ptr(records, torch.uint8, cfg.B * cfg.H * record_bytes(cfg), "records"),
+        _ptr(q, torch.float32, _rows(cfg), "q"), _ptr(k, torch.float32, _rows(cfg), "k"),
+        _ptr(v, torch.float32, cfg.B * cfg.H * cfg.d_v, "v"), _ptr(s, torch.float32, n_s, "s"),
+        _ptr(beta, torch.float32, cfg.B * cfg.H, "beta"),
+        _ptr(gamma, torch.float64, _rows(cfg), "gamma"),
+        _ptr(o, torch.float32, cfg.B * cfg.H * cfg.d_v, "o"), _ptr(ws, torch.uint8, None, "ws"),
+        _stream()))
+
+
+def kda_step_writeback(cfg, records, ws):
+    _check(load().kda_step_writeback(
+        ctypes.byref(cfg.c()), _ptr(records, torch.uint8, cfg.B * cfg.H * record_bytes(cfg), "records"),
+        _ptr(ws, torch.uint8, None, "ws"), _stream()))
+
+
 _BF16 = (torch.bfloat16, torch.int16)   # bf16 values or their raw bit patterns
 
 

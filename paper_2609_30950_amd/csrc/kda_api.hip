@@ -178,13 +178,15 @@ int kda_unpack_state(const kda_config* cfg, const void* records, float* S, uint8
   return hip_status(kda::launch_unpack(p, S, bits, s_hat, r, (hipStream_t)stream));
 }
 
-int kda_step(const kda_config* cfg, void* records, const float* q, const float* k, const float* v,
-             const float* s, const float* beta, const double* gamma, float* o, void* ws,
-             void* stream) {
+// Checked parameters of a decode step (phase: 1 outputs, 2 write-back, 3 both).
+static int step_params(const kda_config* cfg, void* records, const float* q, const float* k,
+                       const float* v, const float* s, const float* beta, const double* gamma,
+                       float* o, void* ws, int phase, KParams* out) {
   int need = 0;
   int st = check_cfg(cfg, &need);
   if (st != KDA_OK) return st;
-  if (!records || !q || !k || !v || !s || !beta || !o) return KDA_ERR_ARG;
+  if (!records) return KDA_ERR_ARG;
+  if ((phase & 1) && (!q || !k || !v || !s || !beta || !o)) return KDA_ERR_ARG;
   if (!cfg->state32 && !ws) return KDA_ERR_WORKSPACE;
   if (!aligned16(records) || (ws && !aligned16(ws))) return KDA_ERR_ARG;
   KParams p = make_params(cfg, need);
@@ -201,7 +203,34 @@ int kda_step(const kda_config* cfg, void* records, const float* q, const float* 
   p.ntk = 1;
   p.in_bf16 = 0;
   if (!cfg->state32) set_ws(p, cfg, ws);
+  *out = p;
+  return KDA_OK;
+}
+
+int kda_step(const kda_config* cfg, void* records, const float* q, const float* k, const float* v,
+             const float* s, const float* beta, const double* gamma, float* o, void* ws,
+             void* stream) {
+  KParams p;
+  const int st = step_params(cfg, records, q, k, v, s, beta, gamma, o, ws, 3, &p);
+  if (st != KDA_OK) return st;
   return hip_status(kda::launch_step(p, (hipStream_t)stream));
+}
+
+int kda_step_outputs(const kda_config* cfg, void* records, const float* q, const float* k,
+                     const float* v, const float* s, const float* beta, const double* gamma,
+                     float* o, void* ws, void* stream) {
+  KParams p;
+  const int st = step_params(cfg, records, q, k, v, s, beta, gamma, o, ws, 1, &p);
+  if (st != KDA_OK) return st;
+  return hip_status(kda::launch_step_outputs(p, (hipStream_t)stream));
+}
+
+int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* stream) {
+  KParams p;
+  const int st = step_params(cfg, records, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                             nullptr, ws, 2, &p);
+  if (st != KDA_OK) return st;
+  return hip_status(kda::launch_step_writeback(p, (hipStream_t)stream));
 }
 
 int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, const uint16_t* q,

@@ -1143,10 +1143,13 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
 // ------------------------------------------------------- launchers ---
 
 // One write-back interval: tokens [p.tok0, p.tok0 + p.ntk), then quantise.
+// Phases of one write-back interval (PHASES: 1 = stats and allocation,
+// 2 = requantisation, 3 = both).
 template <int DK, int DV>
-static hipError_t launch_interval_t(const KParams& p, hipStream_t st) {
+static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases = 3) {
   const int nbh = p.B * p.H;
   if (p.state32) {
+    if (!(phases & 1)) return hipSuccess;
     ProfScope ps("step32", st);
     if (p.in_bf16)
       k_step32<DK, DV, true><<<nbh, 2 * DK, 0, st>>>(p);
@@ -1154,8 +1157,8 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st) {
       k_step32<DK, DV, false><<<nbh, 2 * DK, 0, st>>>(p);
     return hipGetLastError();
   }
-  hipError_t e;
-  {
+  hipError_t e = hipSuccess;
+  if (phases & 1) {
     ProfScope ps("stats", st);
     const size_t dyn = (size_t)(p.L.wc + 1) * DV * 4;
     if (p.scope == 1) {
@@ -1172,24 +1175,29 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st) {
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
-  if (p.scope == 0) {
+  if ((phases & 1) && p.scope == 0) {
     ProfScope ps("alloc", st);
     k_alloc<<<p.B, 1024, 0, st>>>(p.ws_c, p.H * DK, p.need, p.bmin, p.bmax, p.ws_bits);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (!(phases & 2)) return hipSuccess;
   ProfScope ps("requant", st);
   k_requant<DK, DV><<<nbh, 2 * DK, 0, st>>>(p);
   return hipGetLastError();
 }
 
-static hipError_t launch_interval(const KParams& p, hipStream_t st) {
-  if (p.dk == 64) return launch_interval_t<64, 64>(p, st);
-  if (p.dk == 256) return launch_interval_t<256, 256>(p, st);
-  return launch_interval_t<128, 128>(p, st);
+static hipError_t launch_interval(const KParams& p, hipStream_t st, int phases = 3) {
+  if (p.dk == 64) return launch_interval_t<64, 64>(p, st, phases);
+  if (p.dk == 256) return launch_interval_t<256, 256>(p, st, phases);
+  return launch_interval_t<128, 128>(p, st, phases);
 }
 
 hipError_t launch_step(const KParams& p, hipStream_t st) { return launch_interval(p, st); }
+hipError_t launch_step_outputs(const KParams& p, hipStream_t st) { return launch_interval(p, st, 1); }
+hipError_t launch_step_writeback(const KParams& p, hipStream_t st) {
+  return launch_interval(p, st, 2);
+}
 
 // One prefill write-back interval on column slices: stats per slice, weights
 // and allocation per scope unit, then the requantisation.

@@ -36,6 +36,8 @@ struct KParams {
 };
 
 hipError_t launch_step(const KParams& p, hipStream_t st);
+hipError_t launch_step_outputs(const KParams& p, hipStream_t st);
+hipError_t launch_step_writeback(const KParams& p, hipStream_t st);
 hipError_t launch_prefill(KParams p, int C, hipStream_t st);
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st);

@@ -14,7 +14,7 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes
+from tests._gpu import bytes_to_state, dev, host, meaningful_equal, say, state_to_bytes
 
 pytestmark = pytest.mark.gpu
 
@@ -157,3 +157,31 @@ def test_step_rejects_bad_config():
     with pytest.raises(K.KdaError):
         K.kda_step(kc, K.new_records(_cfgs(w)[0]), *[torch.zeros(1, device="cuda")] * 5,
                    torch.zeros(1, device="cuda"), K.new_workspace(_cfgs(w)[0]))
+
+
+def test_split_phases_equal_step():
+    """kda_step_outputs then kda_step_writeback (on another stream, after an
+    event) leave the same records and outputs as kda_step."""
+    w = W.sized(W.WORKLOADS["decode"], B=2)
+    kc, oc = _cfgs(w)
+    xs = W.tokens(w, 0, 12)
+    st, _ = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
+    start = state_to_bytes(st, w.dk, w.dv, w.b_max)
+    base = W.base_rates(w)
+    recs_a, recs_b = dev(start), dev(start)
+    ws_a, ws_b = K.new_workspace(kc), K.new_workspace(kc)
+    o_a = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    o_b = torch.zeros_like(o_a)
+    side = torch.cuda.Stream()
+    for t in range(12, 15):
+        x = {n: dev(a) for n, a in W.token(w, t, base=base).items()}
+        K.kda_step(kc, recs_a, x["q"], x["k"], x["v"], x["s"], x["beta"], o_a, ws_a)
+        K.kda_step_outputs(kc, recs_b, x["q"], x["k"], x["v"], x["s"], x["beta"], o_b, ws_b)
+        ev = torch.cuda.Event()
+        ev.record()
+        side.wait_event(ev)
+        with torch.cuda.stream(side):
+            K.kda_step_writeback(kc, recs_b, ws_b)
+        torch.cuda.current_stream().wait_stream(side)
+        assert torch.equal(o_a, o_b)
+    assert not meaningful_equal(host(recs_a), host(recs_b), w.B, w.H, w.dk, w.dv, w.b_max)

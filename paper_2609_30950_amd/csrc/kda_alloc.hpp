@@ -25,7 +25,6 @@ namespace kda {
 
 constexpr int ALLOC_MAX_N = 4096;     // rows per scope unit
 constexpr int ALLOC_MAX_T = 1024;     // threads per block
-constexpr int ALLOC_RPT = 4;          // rows per thread (N <= 4096 with 1024 threads)
 constexpr int E_ZERO = -100000;       // exponent sentinel of c = 0
 constexpr int EBINS = 2304;           // exponent histogram range (frexp: [-1073, 1024])
 constexpr int EOFF = 1100;
@@ -64,31 +63,38 @@ __device__ __forceinline__ int block_excl_scan(int v, int* scratch, int* total) 
   return off + incl - v;
 }
 
-// c_at(n): weight of row n (any address space); out: N widths.
-template <typename Load>
+// 52 fraction bits of the frexp mantissa of c > 0 (c = (1 + F 2^-52) 2^(E-1)).
+__device__ __forceinline__ unsigned long long frac_bits(double c) {
+  int e;
+  const double m = frexp(c, &e);
+  return (unsigned long long)ldexp(m, 53) - (1ull << 52);
+}
+
+// c_at(n): weight of row n (any address space); out: N widths.  RPT: rows per
+// thread, at least ceil(N / blockDim.x).
+template <int RPT, typename Load>
 __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax, uint8_t* out,
                                AllocSmem& sm) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id();
   const int L = bmax - bmin;
-  // rows n = tid + k * nt, k < ALLOC_RPT
-  int E[ALLOC_RPT];
-  unsigned long long F[ALLOC_RPT];   // 52-bit fraction of the frexp mantissa
+  // rows n = tid + k * nt, k < RPT; the fraction bits of a row are
+  // recomputed from c_at(n) when the row is a boundary candidate
+  static_assert(RPT <= 32, "candidate mask");
+  int E[RPT];
   for (int e = tid; e < EBINS; e += nt) sm.hist_e[e] = 0;
   for (int n = tid; n < N; n += nt) sm.extra[n] = 0;
   if (tid == 0) sm.cand_n = 0;
   int npos = 0;
 #pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k) {
+  for (int k = 0; k < RPT; ++k) {
     const int n = tid + k * nt;
     E[k] = E_ZERO;
-    F[k] = 0;
     if (n < N) {
       const double cv = c_at(n);
       if (cv > 0.0) {
         int ei;
-        const double m = frexp(cv, &ei);
+        frexp(cv, &ei);
         E[k] = ei;
-        F[k] = (unsigned long long)ldexp(m, 53) - (1ull << 52);
         ++npos;
       }
     }
@@ -96,11 +102,11 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   __syncthreads();
   // histogram of exponents (few distinct values: LDS atomics conflict little)
 #pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k)
+  for (int k = 0; k < RPT; ++k)
     if (E[k] != E_ZERO) atomicAdd(&sm.hist_e[E[k] + EOFF], 1);
   int emin = 0x7fffffff, emax = -0x7fffffff;
 #pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k)
+  for (int k = 0; k < RPT; ++k)
     if (E[k] != E_ZERO) { emin = min(emin, E[k]); emax = max(emax, E[k]); }
   block_sum_min_max(npos, emin, emax, sm.red);
   __syncthreads();
@@ -115,7 +121,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     const long long rem0 = need - ptot;
     int carry = 0;
 #pragma unroll
-    for (int k = 0; k < ALLOC_RPT; ++k) {
+    for (int k = 0; k < RPT; ++k) {
       const int n = tid + k * nt;
       const int isz = (n < N && E[k] == E_ZERO) ? 1 : 0;
       int tot;
@@ -170,31 +176,30 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   const int beta = sm.sel_beta;
   int rem = sm.sel_rem;
 
-  // stage 2: radix narrowing of the candidates of bucket beta
-  bool cand[ALLOC_RPT];
+  // stage 2: radix narrowing of the candidates of bucket beta (bit k of cand:
+  // row tid + k nt is a candidate)
+  unsigned cand = 0u;
 #pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k) {
-    cand[k] = false;
+  for (int k = 0; k < RPT; ++k) {
     if (E[k] != E_ZERO && ((E[k] - beta) & 1) == 0) {
       const int l = (E[k] - beta) >> 1;
-      cand[k] = l >= bmin + 1 && l <= bmax;
+      if (l >= bmin + 1 && l <= bmax) cand |= 1u << k;
     }
   }
   bool many = true;
   for (int pass = 0; pass < 7; ++pass) {
     const int shift = pass < 6 ? 44 - 8 * pass : 0;
     const unsigned long long dmask = pass < 6 ? 255ull : 15ull;
-    int live = 0;
-#pragma unroll
-    for (int k = 0; k < ALLOC_RPT; ++k) live += cand[k];
+    int live = __builtin_popcount(cand);
     live = block_reduce(live, sm.red, [](int a, int b) { return a + b; });
     if (live <= WAVE) { many = false; break; }
     // candidates above the boundary digit are granted; keep the boundary bin
     for (int e = tid; e < 256; e += nt) sm.hist_d[e] = 0;
     __syncthreads();
-#pragma unroll
-    for (int k = 0; k < ALLOC_RPT; ++k)
-      if (cand[k]) atomicAdd(&sm.hist_d[(F[k] >> shift) & dmask], 1);
+    for (unsigned m = cand; m != 0u; m &= m - 1u) {
+      const int k = __builtin_ctz(m);
+      atomicAdd(&sm.hist_d[(frac_bits(c_at(tid + k * nt)) >> shift) & dmask], 1);
+    }
     __syncthreads();
     if (tid < WAVE) {
       // lane j covers bins 4j+3..4j of the descending order dmask..0
@@ -225,15 +230,14 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     }
     __syncthreads();
     const unsigned long long dg = (unsigned long long)sm.sel_digit;
-#pragma unroll
-    for (int k = 0; k < ALLOC_RPT; ++k) {
-      if (!cand[k]) continue;
-      const unsigned long long d = (F[k] >> shift) & dmask;
+    for (unsigned m = cand; m != 0u; m &= m - 1u) {
+      const int k = __builtin_ctz(m);
+      const unsigned long long d = (frac_bits(c_at(tid + k * nt)) >> shift) & dmask;
       if (d > dg) {
         sm.extra[tid + k * nt] = 1;   // above the boundary digit: granted
-        cand[k] = false;
+        cand &= ~(1u << k);
       } else if (d < dg) {
-        cand[k] = false;
+        cand &= ~(1u << k);
       }
     }
     rem = sm.sel_rem;
@@ -243,23 +247,22 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     // more than a wave of candidates with identical keys: lowest rows first
     int carry = 0;
 #pragma unroll
-    for (int k = 0; k < ALLOC_RPT; ++k) {
+    for (int k = 0; k < RPT; ++k) {
       int tot;
-      const int z = carry + block_excl_scan(cand[k] ? 1 : 0, sm.red, &tot);
-      if (cand[k] && z < rem) sm.extra[tid + k * nt] = 1;
-      cand[k] = false;
+      const int ck = (cand >> k) & 1u;
+      const int z = carry + block_excl_scan(ck, sm.red, &tot);
+      if (ck && z < rem) sm.extra[tid + k * nt] = 1;
       carry += tot;
       __syncthreads();
     }
+    cand = 0u;
   }
   // stage 3: at most one wave of candidates left; rank them in wave 0
-#pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k) {
-    if (cand[k]) {
-      const int pos = atomicAdd(&sm.cand_n, 1);
-      sm.cand_key[pos] = F[k];
-      sm.cand_row[pos] = tid + k * nt;
-    }
+  for (unsigned m = cand; m != 0u; m &= m - 1u) {
+    const int k = __builtin_ctz(m);
+    const int pos = atomicAdd(&sm.cand_n, 1);
+    sm.cand_key[pos] = frac_bits(c_at(tid + k * nt));
+    sm.cand_row[pos] = tid + k * nt;
   }
   __syncthreads();
   if (tid < WAVE) {
@@ -278,7 +281,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   }
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < ALLOC_RPT; ++k) {
+  for (int k = 0; k < RPT; ++k) {
     const int n = tid + k * nt;
     if (n < N) out[n] = (uint8_t)(bmin + slots_ge(E[k], beta + 1, bmin, L) + sm.extra[n]);
   }

@@ -15,7 +15,7 @@ namespace {
 using kda::KParams;
 
 struct WsLayout {
-  size_t c_off, zr_off, bits_off, s32_off, rpart_off, gam_off, total;
+  size_t c_off, zr_off, bits_off, s32_off, rpart_off, gam_off, hv_off, total;
 };
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
@@ -30,7 +30,9 @@ WsLayout ws_layout(const kda_config* cfg) {
   // prefill: per-slice row maxima (d_v / 64 slices) and the rows' weights Gamma
   w.rpart_off = up256(w.s32_off + rows * (size_t)cfg->d_v * sizeof(float));
   w.gam_off = up256(w.rpart_off + rows * (size_t)(cfg->d_v / 64) * sizeof(float));
-  w.total = up256(w.gam_off + rows * sizeof(double));
+  // decode: the token's vectors w (d_v), a and g (d_k) per head
+  w.hv_off = up256(w.gam_off + rows * sizeof(double));
+  w.total = up256(w.hv_off + (size_t)cfg->B * cfg->H * (cfg->d_v + 2 * cfg->d_k) * sizeof(float));
   return w;
 }
 
@@ -95,6 +97,7 @@ void set_ws(KParams& p, const kda_config* cfg, void* ws) {
   p.ws_s32 = (float*)(base + w.s32_off);
   p.ws_rpart = (float*)(base + w.rpart_off);
   p.ws_gam = (double*)(base + w.gam_off);
+  p.ws_hv = (float*)(base + w.hv_off);
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KDA_OK : KDA_ERR_HIP; }

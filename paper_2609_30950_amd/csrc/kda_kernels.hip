@@ -254,7 +254,8 @@ __device__ __forceinline__ float combine_col(const float (&P)[DK / ROW_BLOCK][DV
 // o = S^T q.  Writes o to o_out (if non-null).  All threads must call.
 template <int DK, int DV, bool BF16>
 __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
-                            RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out) {
+                            RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out,
+                            float* w_out = nullptr) {
   constexpr int CPL = DV / WAVE;
   static_assert(CPL <= 4, "columns per lane");
   const int w = threadIdx.x / WAVE, lane = lane_id();
@@ -289,6 +290,7 @@ __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], co
     const float u = combine_col<DK, DV>(sm.up, col);
     wv[c] = vin[c] - u;
     acc[c] = 0.f;
+    if (w_out != nullptr && w == 0) w_out[col] = wv[c];
   }
   pass2_16<0, 0, CPL>(X, acc[0], gq0.x, gq0.y, wv[0]);
   pass2_16<16, 0, CPL>(X, acc[0], gq1.x, gq1.y, wv[0]);
@@ -386,7 +388,9 @@ using CodeT = typename std::conditional<(DK > 128), int8_t, int16_t>::type;
 // Column stride (elements) of the column-major code buffer: padded by 16 bytes
 // so that the 16-byte reads of consecutive columns hit distinct LDS banks.
 template <int DK>
-constexpr int CT_LD = DK + 16 / (int)sizeof(CodeT<DK>);
+constexpr int CT_LD_OF = DK + 16 / (int)sizeof(CodeT<DK>);
+template <int DK, typename CT>
+constexpr int ct_ld() { return DK + 16 / (int)sizeof(CT); }
 
 // Sum of the per-segment partials of one row held by SEGS adjacent lanes, in
 // the halving order (p[s] + p[s + SEGS/2] first), via DPP quad permutes.
@@ -455,10 +459,11 @@ __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, 
 // grows as m falls.  Once that bound exceeds the best error no smaller f can
 // reach the minimum, so the scan stops; the result equals the exhaustive
 // first strict minimum over all 16 candidates.
-template <int DK, int DV>
-__device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, const uint8_t* perm,
-                         const float (*phi)[N_FIT], CodeT<DK>* Ct, uint16_t* scale_out,
+template <int DK, int DV, bool SYNC_AFTER_LOAD = false, typename LoadRow, typename CT>
+__device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, const uint8_t* perm,
+                         const float (*phi)[N_FIT], CT* Ct, uint16_t* scale_out,
                          unsigned long long* diag) {
+  constexpr int LD = ct_ld<DK, CT>();
   constexpr int SEGS = DV / SEG;
   constexpr int ITEMS = DK * SEGS;
   const int tid = threadIdx.x, nt = blockDim.x;
@@ -469,22 +474,16 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
   const int i = valid ? perm[item / SEGS] : 0;
   const int sg = item % SEGS;
   float x[SEG];
-  const float4* src = (const float4*)(S + (size_t)i * DV + sg * SEG);
-#pragma unroll
-  for (int q = 0; q < SEG / 4; ++q) {
-    const float4 v = src[q];
-    x[4 * q] = v.x;
-    x[4 * q + 1] = v.y;
-    x[4 * q + 2] = v.z;
-    x[4 * q + 3] = v.w;
-  }
+  load_row(i, sg, x);
+  // the code tile may share LDS with what the loader reads (one item per thread)
+  if constexpr (SYNC_AFTER_LOAD) __syncthreads();
   float mx = 0.f;
 #pragma unroll
   for (int j = 0; j < SEG; ++j) mx = fmaxf(mx, fabsf(x[j]));
   if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0xB1>(mx));
   if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
   const int b = bits[i];
-  CodeT<DK>* dst = Ct + (size_t)(sg * SEG) * CT_LD<DK> + i;
+  CT* dst = Ct + (size_t)(sg * SEG) * LD + i;
   int evals = 0;
   if (b == 1) {
     float acc = 0.f;
@@ -495,7 +494,7 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
     const uint16_t mu = f32_to_f16_sat(acc * (1.0f / (float)DV));
     if (valid) {
 #pragma unroll
-      for (int j = 0; j < SEG; ++j) dst[(size_t)j * CT_LD<DK>] = (CodeT<DK>)(x[j] < 0.f ? 1 : 0);
+      for (int j = 0; j < SEG; ++j) dst[(size_t)j * LD] = (CT)(x[j] < 0.f ? 1 : 0);
       if (sg == 0) scale_out[i] = mu;
     }
   } else {
@@ -527,7 +526,7 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
         const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-        dst[(size_t)j * CT_LD<DK>] = (CodeT<DK>)c;
+        dst[(size_t)j * LD] = (CT)c;
       }
       if (sg == 0) scale_out[i] = dh;
     }
@@ -547,8 +546,8 @@ __device__ __forceinline__ void fit_rows(const float* S, const uint8_t* bits, co
 // widths, the bit position and every word boundary are wave-uniform (scalar
 // registers and branches): each code costs one field extract and one
 // shift-or into the current word.
-template <int DK, int DV>
-__device__ __forceinline__ void pack_cols(const CodeT<DK>* Ct, const uint8_t* bits, const int* P,
+template <int DK, int DV, typename CT>
+__device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, const int* P,
                                           uint32_t* words, uint32_t* tail) {
   constexpr int HALF = DK / 2;
   static_assert(DV == DK && DV % WAVE == 0, "one (column, half) per thread, halves wave-aligned");
@@ -565,9 +564,9 @@ __device__ __forceinline__ void pack_cols(const CodeT<DK>* Ct, const uint8_t* bi
   int wi = start >> 5;
   uint32_t first = 0;       // upper half: its first word, merged after the barrier
   bool first_pending = half == 1 && (split & 31) != 0;
-  constexpr int CB = (int)sizeof(CodeT<DK>);   // bytes per code
+  constexpr int CB = (int)sizeof(CT);   // bytes per code
   constexpr int CPR = 16 / CB;                  // codes per 16-byte read
-  const CodeT<DK>* cc = Ct + (size_t)col * CT_LD<DK> + r0;
+  const CT* cc = Ct + (size_t)col * ct_ld<DK, CT>() + r0;
 #pragma unroll
   for (int i0 = 0; i0 < HALF; i0 += CPR) {
     const uint4 raw = *(const uint4*)(cc + i0);
@@ -689,26 +688,44 @@ __device__ __forceinline__ void row_weights(const KParams& p, int bh, StatSmem<D
   __syncthreads();
 }
 
+// Decode steps of heads with d_k <= 128 hand the requantisation the token's
+// vectors (a, g, w) instead of the float32 state; it rebuilds the state from
+// the record (d_k = 256 would need a larger LDS staging than its code tile).
+constexpr bool compact_decode(int dk) { return dk <= 128; }
+
+// LDS of the statistics pass of one head; the record's code words follow it
+// in the same allocation (and, for the per-head budget, the allocator's
+// scratch once the words are decoded).
+template <int DK, int DV>
+struct StatsLds {
+  MetaSmem<DK> meta;
+  RowSmem<DK> rs;
+  RecSmem<DK, DV> rsm;
+  __align__(16) StatSmem<DK> st;
+};
+
+// Bytes of the code-word staging area that follows StatsLds.
+__host__ __device__ inline size_t stats_words_bytes(int wc, int dv) {
+  return (size_t)(wc + 1) * dv * 4;
+}
+
 // Tokens [tok0, tok0 + ntk) of one head with the state resident in registers,
 // starting from the record: outputs o for every token, the float32 state after
 // the last token (to the workspace), row ranges and EMA rates, weights c and,
-// for the per-head scope, the widths.  Decode is the one-token case.
-template <int DK, int DV, bool HEAD, bool BF16>
-__global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
-  const int bh = blockIdx.x;
+// for the per-head scope, the widths (with alloc_sm as the allocator's LDS).
+// Decode is the one-token case.  All threads of the block (2 d_k) call it.
+template <int DK, int DV, bool HEAD, bool BF16, bool COMPACT>
+__device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK, DV>& sm,
+                                           uint32_t* words, AllocSmem* alloc_sm) {
   const int t = threadIdx.x;
   const int b = bh / p.H, h = bh % p.H;
   const Layout L = p.L;
   const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
-  __shared__ MetaSmem<DK> meta;
-  __shared__ RowSmem<DK> rs;
-  __shared__ RecSmem<DK, DV> rsm;
-  __shared__ __align__(16) StatSmem<DK> st;
-  extern __shared__ uint4 dyn_lds[];
-  uint32_t* words = (uint32_t*)dyn_lds;
+  MetaSmem<DK>& meta = sm.meta;
+  StatSmem<DK>& st = sm.st;
   // the first token's row scalars and the whole code-word capacity of the
   // record are requested together with the metadata (one memory round trip)
-  RowIn in = load_rows<DK, BF16>(rs, p, bh, p.tok0);
+  RowIn in = load_rows<DK, BF16>(sm.rs, p, bh, p.tok0);
   stage_words<DV, false>(rec, L, L.wc * 32, words);   // the barrier in load_meta covers it
   load_meta<DK, DV>(rec, L, p.bmax, meta);
   // EMA states of row t (threads t < DK): from the record, or fresh; token
@@ -736,15 +753,24 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   ema(in);
   float X[ROW_BLOCK][DV / WAVE];
   unpack_cols<DK, DV>(words, meta, X);
+  // COMPACT (one token): the requantisation rebuilds the state from the
+  // record and the token's vectors a, g, w; else it reads the float32 state
+  constexpr bool compact = COMPACT;
+  float* hv = p.ws_hv + (size_t)bh * (DV + 2 * DK);
   for (int j = 0; j < p.ntk; ++j) {
     const int tok = p.tok0 + j;
-    if (j > 0) ema(load_rows<DK, BF16>(rs, p, bh, tok));
+    if (j > 0) ema(load_rows<DK, BF16>(sm.rs, p, bh, tok));
     __syncthreads();
+    if (compact && t < DK) {
+      hv[DV + t] = sm.rs.ak[t].x;        // a = fl32(exp(-s))
+      hv[DV + DK + t] = sm.rs.gq[t].x;   // g = fl32(beta k)
+    }
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV);
+    recur_token<DK, DV, BF16>(X, sm.rs, sm.rsm, p.v, th * DV, p.o + th * DV,
+                              compact ? hv : nullptr);
   }
   row_rates<DK>(p, bh, st, m_run, e_run, t);
-  {
+  if (!compact) {
     // float32 state after the last token, row-major, for the requantisation
     const int w = t / WAVE, lane = lane_id();
     float* dstS = p.ws_s32 + (size_t)bh * DK * DV;
@@ -758,10 +784,17 @@ __global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
   row_weights<DK>(p, bh, st, t);
   if constexpr (HEAD) {
     // per-head budget: allocate here (c of this head is in LDS)
-    __shared__ AllocSmem asm_;
-    block_allocate([&](int n) { return st.c[n]; }, DK, p.need, p.bmin, p.bmax,
-                   p.ws_bits + (size_t)bh * DK, asm_);
+    block_allocate<1>([&](int n) { return st.c[n]; }, DK, p.need, p.bmin, p.bmax,
+                      p.ws_bits + (size_t)bh * DK, *alloc_sm);
   }
+}
+
+template <int DK, int DV, bool HEAD, bool BF16>
+__global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
+  extern __shared__ uint4 dyn_lds[];
+  __shared__ StatsLds<DK, DV> sm;
+  uint32_t* words = (uint32_t*)dyn_lds;
+  stats_head<DK, DV, HEAD, BF16, compact_decode(DK)>(p, blockIdx.x, sm, words, (AllocSmem*)dyn_lds);
 }
 
 // Layer budget: one block per scope unit of N rows (contiguous in ws_c).
@@ -769,40 +802,133 @@ __global__ void __launch_bounds__(1024) k_alloc(const double* c, int N, int need
                                                 int bmax, uint8_t* bits) {
   __shared__ AllocSmem sm;
   const double* cu = c + (size_t)blockIdx.x * N;
-  block_allocate([&](int n) { return cu[n]; }, N, need, bmin, bmax,
-                 bits + (size_t)blockIdx.x * N, sm);
+  block_allocate<ALLOC_MAX_N / 1024>([&](int n) { return cu[n]; }, N, need, bmin, bmax,
+                                     bits + (size_t)blockIdx.x * N, sm);
 }
 
-// Quantise the float32 state the stats pass left in the workspace with the
-// allocated widths and pack it into the record in place.
+// Row loader of a row-major float32 state S[DK][DV]: segment sg of row i.
+template <int DV>
+__device__ __forceinline__ void load_dense(const float* S, int i, int sg, float (&x)[SEG]) {
+  const float4* src = (const float4*)(S + (size_t)i * DV + sg * SEG);
+#pragma unroll
+  for (int q = 0; q < SEG / 4; ++q) {
+    const float4 v = src[q];
+    x[4 * q] = v.x;
+    x[4 * q + 1] = v.y;
+    x[4 * q + 2] = v.z;
+    x[4 * q + 3] = v.w;
+  }
+}
+
+// What the requantisation of a decode step needs besides its own tables when
+// it rebuilds the state from the record: the record's decode metadata and the
+// token's column vector w.
+template <int DK, int DV, bool COMPACT>
+struct RebuildLds {
+  MetaSmem<DK> meta;
+  float wv[DV];
+};
 template <int DK, int DV>
-__global__ void __launch_bounds__(2 * DK) __attribute__((amdgpu_waves_per_eu(4)))
-k_requant(KParams p) {
-  const int bh = blockIdx.x;
+struct RebuildLds<DK, DV, false> {};
+
+// LDS of the requantisation of one head.  With COMPACT the record's code
+// words are staged column-major in the space of the code tile Ct (they are
+// decoded before the first code is written).
+template <int DK, int DV, bool COMPACT, typename CT>
+struct RequantLds {
+  RebuildLds<DK, DV, COMPACT> rb;
+  __align__(16) CT Ct[DV * ct_ld<DK, CT>()];
+  __align__(16) uint8_t nb[DK];
+  uint8_t perm[DK];
+  uint16_t sc16[DK], zz[DK], rr[DK];
+  float phi[MAX_B + 1][N_FIT];
+  OrderSmem<DK> os;
+  uint32_t tail[DV];
+};
+
+// Quantise the state after the write-back interval with the allocated widths
+// and pack it into the record in place.  COMPACT (a decode step): the state is
+// rebuilt row by row from the record and the token's vectors the stats pass
+// left in the workspace, S_ij = fma(g_i, w_j, fl32(a_i x^_ij)) with x^ the
+// record's dequantised value -- the same operations as the stats pass, so the
+// same float32 state.  Otherwise the stats pass left the float32 state itself.
+// All threads of the block (2 d_k) call it.
+template <int DK, int DV, bool COMPACT, typename CT>
+__device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLds<DK, DV, COMPACT, CT>& sm) {
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
-  __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD<DK>];
-  __shared__ __align__(16) uint8_t nb[DK];
-  __shared__ uint8_t perm[DK];
-  __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
-  __shared__ float phi[MAX_B + 1][N_FIT];
-  __shared__ OrderSmem<DK> os;
-  __shared__ uint32_t tail[DV];
   const int t = threadIdx.x;
   const unsigned ntok = *(const unsigned*)rec;
   if (t < DK) {
-    nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
+    sm.nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
     const uint32_t zr = p.ws_zr[(size_t)bh * DK + t];
-    zz[t] = (uint16_t)(zr & 0xffffu);
-    rr[t] = (uint16_t)(zr >> 16);
+    sm.zz[t] = (uint16_t)(zr & 0xffffu);
+    sm.rr[t] = (uint16_t)(zr >> 16);
   }
-  for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
+  for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x)
+    sm.phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
+  if constexpr (COMPACT) {
+    // the staging needs DV (wc + 1) words, wc = ceil(d_k b_max / 32): 16-bit
+    // tiles hold any b_max <= 16, byte tiles b_max <= 8 (the launcher's choice)
+    static_assert((size_t)DV * (DK * (sizeof(CT) == 1 ? 8 : MAX_B) / 32 + 1) * 4 <= sizeof(sm.Ct),
+                  "staging fits the code tile");
+    const float* hv = p.ws_hv + (size_t)bh * (DV + 2 * DK);
+    load_meta<DK, DV>(rec, L, p.bmax, sm.rb.meta);   // synchronises
+    // the record's code words, column-major: word k of column j at
+    // stg[j * str + k], so a field that straddles two words is one pair
+    uint32_t* stg = (uint32_t*)sm.Ct;
+    const int str = L.wc + 1;
+    const int nw = (sm.rb.meta.P[DK] + 31) >> 5;
+    const uint4* src = (const uint4*)(rec + L.codes_off);
+    for (int e = t; e < nw * (DV / 4); e += blockDim.x) {
+      const int k = e / (DV / 4), c4 = e % (DV / 4);
+      const uint4 v = src[(size_t)k * (DV / 4) + c4];
+      stg[(4 * c4) * str + k] = v.x;
+      stg[(4 * c4 + 1) * str + k] = v.y;
+      stg[(4 * c4 + 2) * str + k] = v.z;
+      stg[(4 * c4 + 3) * str + k] = v.w;
+    }
+    for (int e = t; e < DV; e += blockDim.x) sm.rb.wv[e] = hv[e];
+    __syncthreads();
+    width_order<DK>(sm.nb, sm.perm, sm.os);
+    auto rebuild = [&](int i, int sg, float (&x)[SEG]) {
+      const int P = sm.rb.meta.P[i];
+      const int sh = P & 31, bo = sm.rb.meta.w[i];
+      const uint4 d = sm.rb.meta.desc[i];
+      const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
+      const float ai = hv[DV + i], gi = hv[DV + DK + i];
+      const uint32_t* cw = stg + (size_t)(sg * SEG) * str + (P >> 5);
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        const uint32_t lo = cw[j * str], hi = cw[j * str + 1];
+        const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
+        const int code = __builtin_amdgcn_sbfe((int)f, 0, bo);   // signed field
+        const float xh = ((float)code + add) * mul;
+        x[j] = __builtin_fmaf(gi, sm.rb.wv[sg * SEG + j], ai * xh);
+      }
+    };
+    fit_rows<DK, DV, true>(rebuild, sm.nb, sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
+  } else {
+    __syncthreads();
+    width_order<DK>(sm.nb, sm.perm, sm.os);
+    const float* S = p.ws_s32 + (size_t)bh * DK * DV;
+    fit_rows<DK, DV>([&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(S, i, sg, x); }, sm.nb,
+                     sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
+  }
   __syncthreads();
-  width_order<DK>(nb, perm, os);
-  fit_rows<DK, DV>(p.ws_s32 + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16, p.diag_fit);
-  __syncthreads();
-  pack_cols<DK, DV>(Ct, nb, os.P, (uint32_t*)(rec + L.codes_off), tail);
-  store_meta<DK>(rec, L, ntok + (unsigned)p.ntk, nb, sc16, zz, rr);
+  pack_cols<DK, DV>(sm.Ct, sm.nb, sm.os.P, (uint32_t*)(rec + L.codes_off), sm.tail);
+  store_meta<DK>(rec, L, ntok + (unsigned)p.ntk, sm.nb, sm.sc16, sm.zz, sm.rr);
+}
+
+// Code tile element: bytes when widths fit (b_max <= 8), else 16 bits.
+template <bool C8>
+using CodeTile = typename std::conditional<C8, int8_t, int16_t>::type;
+
+template <int DK, int DV, bool COMPACT, bool C8>
+__global__ void __launch_bounds__(2 * DK) __attribute__((amdgpu_waves_per_eu(4)))
+k_requant(KParams p) {
+  __shared__ RequantLds<DK, DV, COMPACT, CodeTile<C8>> sm;
+  requant_head<DK, DV, COMPACT, CodeTile<C8>>(p, blockIdx.x, sm);
 }
 
 // Unquantised ("32-bit") state: load, one token, store.
@@ -841,7 +967,7 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   const int bh = blockIdx.x;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)p.records + L.slot * (long long)bh;
-  __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD<DK>];
+  __shared__ __align__(16) CodeT<DK> Ct[DV * CT_LD_OF<DK>];
   __shared__ __align__(16) uint8_t nb[DK];
   __shared__ uint8_t perm[DK];
   __shared__ uint16_t sc16[DK], zz[DK], rr[DK];
@@ -857,7 +983,9 @@ __global__ void __launch_bounds__(2 * DK) k_pack(KParams p, const float* S, cons
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x) phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
   __syncthreads();
   width_order<DK>(nb, perm, os);
-  fit_rows<DK, DV>(S + (size_t)bh * DK * DV, nb, perm, phi, Ct, sc16, p.diag_fit);
+  const float* Sh = S + (size_t)bh * DK * DV;
+  fit_rows<DK, DV>([&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(Sh, i, sg, x); }, nb, perm,
+                   phi, Ct, sc16, p.diag_fit);
   __syncthreads();
   pack_cols<DK, DV>(Ct, nb, os.P, (uint32_t*)(rec + L.codes_off), tail);
   store_meta<DK>(rec, L, ntok, nb, sc16, zz, rr);
@@ -1137,7 +1265,8 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
     c[n] = p.ws_gam[row0 + n] * (Rt * Rt);
   }
   __syncthreads();
-  block_allocate([&](int n) { return c[n]; }, N, p.need, p.bmin, p.bmax, p.ws_bits + row0, sm);
+  block_allocate<ALLOC_MAX_N / 1024>([&](int n) { return c[n]; }, N, p.need, p.bmin, p.bmax,
+                                     p.ws_bits + row0, sm);
 }
 
 // ------------------------------------------------------- launchers ---
@@ -1183,7 +1312,10 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases
   }
   if (!(phases & 2)) return hipSuccess;
   ProfScope ps("requant", st);
-  k_requant<DK, DV><<<nbh, 2 * DK, 0, st>>>(p);
+  if (DK > 128 || p.bmax <= 8)
+    k_requant<DK, DV, compact_decode(DK), true><<<nbh, 2 * DK, 0, st>>>(p);
+  else
+    k_requant<DK, DV, compact_decode(DK), (DK > 128)><<<nbh, 2 * DK, 0, st>>>(p);
   return hipGetLastError();
 }
 
@@ -1224,7 +1356,10 @@ static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
   }
   if (e != hipSuccess) return e;
   ProfScope ps("requant", st);
-  k_requant<DK, DK><<<p.B * p.H, 2 * DK, 0, st>>>(p);
+  if (DK > 128 || p.bmax <= 8)
+    k_requant<DK, DK, false, true><<<p.B * p.H, 2 * DK, 0, st>>>(p);
+  else
+    k_requant<DK, DK, false, (DK > 128)><<<p.B * p.H, 2 * DK, 0, st>>>(p);
   return hipGetLastError();
 }
 

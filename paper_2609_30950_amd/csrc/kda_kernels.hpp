@@ -32,6 +32,7 @@ struct KParams {
   float* ws_s32;            // float32 state after the token, [B][H][dk][dv]
   float* ws_rpart;          // prefill: row maxima per 64-column slice, [B][H][dk][dv/64]
   double* ws_gam;           // prefill: row weights Gamma, [B][H][dk]
+  float* ws_hv;             // decode: token vectors per head {w[dv], a[dk], g[dk]}
   unsigned long long* diag_fit;  // profiling: candidate evaluations (or null)
 };
 

@@ -31,10 +31,11 @@ constexpr int EOFF = 1100;
 
 struct AllocSmem {
   int hist_e[EBINS];
-  int hist_d[256];
+  int hist_d[2][256];   // digit histograms of consecutive radix passes
   int red[48];
   int cand_n;
-  int sel_beta, sel_digit, sel_rem, sel_mode;
+  int npos, emin, emax;
+  int sel_beta, sel_digit, sel_rem, sel_live;
   unsigned long long cand_key[WAVE];
   int cand_row[WAVE];
   unsigned char extra[ALLOC_MAX_N];
@@ -82,9 +83,15 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   static_assert(RPT <= 32, "candidate mask");
   int E[RPT];
   for (int e = tid; e < EBINS; e += nt) sm.hist_e[e] = 0;
+  for (int e = tid; e < 2 * 256; e += nt) sm.hist_d[e >> 8][e & 255] = 0;
   for (int n = tid; n < N; n += nt) sm.extra[n] = 0;
-  if (tid == 0) sm.cand_n = 0;
-  int npos = 0;
+  if (tid == 0) {
+    sm.cand_n = 0;
+    sm.npos = 0;
+    sm.emin = 0x7fffffff;
+    sm.emax = -0x7fffffff;
+  }
+  int npos = 0, emin = 0x7fffffff, emax = -0x7fffffff;
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
     const int n = tid + k * nt;
@@ -96,20 +103,29 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
         frexp(cv, &ei);
         E[k] = ei;
         ++npos;
+        emin = min(emin, ei);
+        emax = max(emax, ei);
       }
     }
   }
   __syncthreads();
-  // histogram of exponents (few distinct values: LDS atomics conflict little)
+  // histogram of exponents (few distinct values: LDS atomics conflict little);
+  // count and exponent range reduced per wave, one LDS atomic each
 #pragma unroll
   for (int k = 0; k < RPT; ++k)
     if (E[k] != E_ZERO) atomicAdd(&sm.hist_e[E[k] + EOFF], 1);
-  int emin = 0x7fffffff, emax = -0x7fffffff;
-#pragma unroll
-  for (int k = 0; k < RPT; ++k)
-    if (E[k] != E_ZERO) { emin = min(emin, E[k]); emax = max(emax, E[k]); }
-  block_sum_min_max(npos, emin, emax, sm.red);
+  npos = wave_reduce_i(npos, [](int a, int b) { return a + b; });
+  emin = wave_reduce_i(emin, [](int a, int b) { return a < b ? a : b; });
+  emax = wave_reduce_i(emax, [](int a, int b) { return a > b ? a : b; });
+  if (lane == 0) {
+    atomicAdd(&sm.npos, npos);
+    atomicMin(&sm.emin, emin);
+    atomicMax(&sm.emax, emax);
+  }
   __syncthreads();
+  npos = sm.npos;
+  emin = sm.emin;
+  emax = sm.emax;
   const long long ptot = (long long)npos * L;
 
   if (need <= 0) {
@@ -166,6 +182,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
         if (lane == f) {
           sm.sel_beta = bb;
           sm.sel_rem = (int)(need - (run + incl - cnt));
+          sm.sel_live = cnt;   // rows with a slot in bucket bb: the candidates
         }
         break;
       }
@@ -175,6 +192,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   __syncthreads();
   const int beta = sm.sel_beta;
   int rem = sm.sel_rem;
+  int live = sm.sel_live;
 
   // stage 2: radix narrowing of the candidates of bucket beta (bit k of cand:
   // row tid + k nt is a candidate)
@@ -186,32 +204,30 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
       if (l >= bmin + 1 && l <= bmax) cand |= 1u << k;
     }
   }
+  // each pass: histogram of the candidates' next digit, the digit bin that
+  // holds the boundary (wave 0; the other waves clear the next pass's
+  // histogram meanwhile), then candidates above it are granted and below it
+  // dropped; the bin's count is the next pass's number of candidates
   bool many = true;
   for (int pass = 0; pass < 7; ++pass) {
+    if (live <= WAVE) { many = false; break; }
     const int shift = pass < 6 ? 44 - 8 * pass : 0;
     const unsigned long long dmask = pass < 6 ? 255ull : 15ull;
-    int live = __builtin_popcount(cand);
-    live = block_reduce(live, sm.red, [](int a, int b) { return a + b; });
-    if (live <= WAVE) { many = false; break; }
-    // candidates above the boundary digit are granted; keep the boundary bin
-    for (int e = tid; e < 256; e += nt) sm.hist_d[e] = 0;
-    __syncthreads();
+    int* hd = sm.hist_d[pass & 1];
     for (unsigned m = cand; m != 0u; m &= m - 1u) {
       const int k = __builtin_ctz(m);
-      atomicAdd(&sm.hist_d[(frac_bits(c_at(tid + k * nt)) >> shift) & dmask], 1);
+      atomicAdd(&hd[(frac_bits(c_at(tid + k * nt)) >> shift) & dmask], 1);
     }
     __syncthreads();
     if (tid < WAVE) {
       // lane j covers bins 4j+3..4j of the descending order dmask..0
-      const int nb = (int)dmask + 1;
       int h[4], tot = 0;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int d = (int)dmask - (4 * lane + u);
-        h[u] = d >= 0 ? sm.hist_d[d] : 0;
+        h[u] = d >= 0 ? hd[d] : 0;
         tot += h[u];
       }
-      (void)nb;
       const int incl = wave_incl_scan(tot);
       const unsigned long long hit = __ballot(incl >= rem);
       const int f = __ffsll((long long)hit) - 1;
@@ -222,11 +238,16 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
           if (run + h[u] >= rem) {
             sm.sel_digit = (int)dmask - (4 * lane + u);
             sm.sel_rem = rem - run;
+            sm.sel_live = h[u];
             break;
           }
           run += h[u];
         }
       }
+      if (nt == WAVE)
+        for (int e = lane; e < 256; e += WAVE) sm.hist_d[(pass + 1) & 1][e] = 0;
+    } else {
+      for (int e = tid - WAVE; e < 256; e += nt - WAVE) sm.hist_d[(pass + 1) & 1][e] = 0;
     }
     __syncthreads();
     const unsigned long long dg = (unsigned long long)sm.sel_digit;
@@ -241,7 +262,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
       }
     }
     rem = sm.sel_rem;
-    __syncthreads();
+    live = sm.sel_live;
   }
   if (many) {
     // more than a wave of candidates with identical keys: lowest rows first

@@ -1289,7 +1289,10 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases
   hipError_t e = hipSuccess;
   if (phases & 1) {
     ProfScope ps("stats", st);
-    const size_t dyn = (size_t)(p.L.wc + 1) * DV * 4;
+    // code-word staging; with the per-head budget the allocator's scratch
+    // reuses it after the words are decoded
+    size_t dyn = stats_words_bytes(p.L.wc, DV);
+    if (p.scope == 1 && dyn < sizeof(AllocSmem)) dyn = sizeof(AllocSmem);
     if (p.scope == 1) {
       if (p.in_bf16)
         k_chunk<DK, DV, true, true><<<nbh, 2 * DK, dyn, st>>>(p);

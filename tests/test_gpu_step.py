@@ -132,6 +132,34 @@ def test_oracle_forced_steps_decode_shape(scope):
     assert bad / tot <= 1e-5
 
 
+@pytest.mark.parametrize("scope", [0, 1])
+@pytest.mark.parametrize("d", [64, 128])
+def test_forced_steps_narrow_widths(d, scope):
+    # widths in [1, 3] at a 2-bit mean: the record's code words take less LDS
+    # than the allocator's scratch, which the per-head budget places there
+    w = W.sized(W.WORKLOADS["decode"], B=2, H=4, dk=d, dv=d, G=min(64, d), mean_bits=2.0,
+                b_min=1, b_max=3)
+    kc, oc = _cfgs(w, scope=scope)
+    xs = W.tokens(w, 0, 16)
+    st, _ = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
+    ws = K.new_workspace(kc)
+    o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    base = W.base_rates(w)
+    bad = tot = 0
+    for t in range(16, 19):
+        x = W.token(w, t, base=base)
+        recs = dev(state_to_bytes(st, w.dk, w.dv, w.b_max))
+        K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o, ws)
+        st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
+        stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
+        dc, n = _compare(stg, st, f"narrow d={d} scope={scope} t={t}")
+        bad += dc
+        tot += n
+        og = host(o).reshape(o_or.shape)
+        assert np.max(np.abs(og - o_or)) <= 1e-6 * np.max(np.abs(o_or))
+    assert bad / tot <= 1e-5
+
+
 def test_window_gamma_input_and_span1():
     w = W.WORKLOADS["tiny"]
     kc, oc = _cfgs(w, span=1)

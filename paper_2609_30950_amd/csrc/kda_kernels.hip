@@ -1272,54 +1272,38 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
 // ------------------------------------------------------- launchers ---
 
 // One write-back interval: tokens [p.tok0, p.tok0 + p.ntk), then quantise.
-// Phases of one write-back interval (PHASES: 1 = stats and allocation,
-// 2 = requantisation, 3 = both).
+// phases: 1 = stats and allocation, 2 = requantisation, 3 = both.
 template <int DK, int DV>
 static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases = 3) {
   const int nbh = p.B * p.H;
   if (p.state32) {
     if (!(phases & 1)) return hipSuccess;
-    ProfScope ps("step32", st);
-    if (p.in_bf16)
-      k_step32<DK, DV, true><<<nbh, 2 * DK, 0, st>>>(p);
-    else
-      k_step32<DK, DV, false><<<nbh, 2 * DK, 0, st>>>(p);
-    return hipGetLastError();
+    if (p.in_bf16) return launch("step32", k_step32<DK, DV, true>, nbh, 2 * DK, 0, st, p);
+    return launch("step32", k_step32<DK, DV, false>, nbh, 2 * DK, 0, st, p);
   }
   hipError_t e = hipSuccess;
   if (phases & 1) {
-    ProfScope ps("stats", st);
     // code-word staging; with the per-head budget the allocator's scratch
     // reuses it after the words are decoded
     size_t dyn = stats_words_bytes(p.L.wc, DV);
     if (p.scope == 1 && dyn < sizeof(AllocSmem)) dyn = sizeof(AllocSmem);
-    if (p.scope == 1) {
-      if (p.in_bf16)
-        k_chunk<DK, DV, true, true><<<nbh, 2 * DK, dyn, st>>>(p);
-      else
-        k_chunk<DK, DV, true, false><<<nbh, 2 * DK, dyn, st>>>(p);
-    } else {
-      if (p.in_bf16)
-        k_chunk<DK, DV, false, true><<<nbh, 2 * DK, dyn, st>>>(p);
-      else
-        k_chunk<DK, DV, false, false><<<nbh, 2 * DK, dyn, st>>>(p);
-    }
-    e = hipGetLastError();
-  }
-  if (e != hipSuccess) return e;
-  if ((phases & 1) && p.scope == 0) {
-    ProfScope ps("alloc", st);
-    k_alloc<<<p.B, 1024, 0, st>>>(p.ws_c, p.H * DK, p.need, p.bmin, p.bmax, p.ws_bits);
-    e = hipGetLastError();
+    if (p.scope == 1)
+      e = p.in_bf16 ? launch("stats", k_chunk<DK, DV, true, true>, nbh, 2 * DK, dyn, st, p)
+                    : launch("stats", k_chunk<DK, DV, true, false>, nbh, 2 * DK, dyn, st, p);
+    else
+      e = p.in_bf16 ? launch("stats", k_chunk<DK, DV, false, true>, nbh, 2 * DK, dyn, st, p)
+                    : launch("stats", k_chunk<DK, DV, false, false>, nbh, 2 * DK, dyn, st, p);
     if (e != hipSuccess) return e;
+    if (p.scope == 0) {
+      e = launch("alloc", k_alloc, p.B, 1024, 0, st, p.ws_c, p.H * DK, p.need, p.bmin, p.bmax,
+                 p.ws_bits);
+      if (e != hipSuccess) return e;
+    }
   }
   if (!(phases & 2)) return hipSuccess;
-  ProfScope ps("requant", st);
   if (DK > 128 || p.bmax <= 8)
-    k_requant<DK, DV, compact_decode(DK), true><<<nbh, 2 * DK, 0, st>>>(p);
-  else
-    k_requant<DK, DV, compact_decode(DK), (DK > 128)><<<nbh, 2 * DK, 0, st>>>(p);
-  return hipGetLastError();
+    return launch("requant", k_requant<DK, DV, compact_decode(DK), true>, nbh, 2 * DK, 0, st, p);
+  return launch("requant", k_requant<DK, DV, compact_decode(DK), (DK > 128)>, nbh, 2 * DK, 0, st, p);
 }
 
 static hipError_t launch_interval(const KParams& p, hipStream_t st, int phases = 3) {
@@ -1339,31 +1323,18 @@ hipError_t launch_step_writeback(const KParams& p, hipStream_t st) {
 template <int DK>
 static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
   const int nsl = p.dv / SLICE;
-  hipError_t e;
-  {
-    ProfScope ps("stats", st);
-    const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
-    if (p.in_bf16)
-      k_chunk_slices<DK, true><<<p.B * p.H * nsl, 2 * DK, dyn, st>>>(p);
-    else
-      k_chunk_slices<DK, false><<<p.B * p.H * nsl, 2 * DK, dyn, st>>>(p);
-    e = hipGetLastError();
-  }
+  const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
+  hipError_t e = p.in_bf16
+      ? launch("stats", k_chunk_slices<DK, true>, p.B * p.H * nsl, 2 * DK, dyn, st, p)
+      : launch("stats", k_chunk_slices<DK, false>, p.B * p.H * nsl, 2 * DK, dyn, st, p);
   if (e != hipSuccess) return e;
-  {
-    ProfScope ps("alloc", st);
-    const int units = p.scope == 0 ? p.B : p.B * p.H;
-    const int N = p.scope == 0 ? p.H * DK : DK;
-    k_alloc_slices<<<units, 1024, 0, st>>>(p, N, nsl);
-    e = hipGetLastError();
-  }
+  const int units = p.scope == 0 ? p.B : p.B * p.H;
+  const int N = p.scope == 0 ? p.H * DK : DK;
+  e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl);
   if (e != hipSuccess) return e;
-  ProfScope ps("requant", st);
   if (DK > 128 || p.bmax <= 8)
-    k_requant<DK, DK, false, true><<<p.B * p.H, 2 * DK, 0, st>>>(p);
-  else
-    k_requant<DK, DK, false, (DK > 128)><<<p.B * p.H, 2 * DK, 0, st>>>(p);
-  return hipGetLastError();
+    return launch("requant", k_requant<DK, DK, false, true>, p.B * p.H, 2 * DK, 0, st, p);
+  return launch("requant", k_requant<DK, DK, false, (DK > 128)>, p.B * p.H, 2 * DK, 0, st, p);
 }
 
 hipError_t launch_prefill(KParams p, int C, hipStream_t st) {
@@ -1387,60 +1358,47 @@ hipError_t launch_prefill(KParams p, int C, hipStream_t st) {
   return hipSuccess;
 }
 
-template <int DK, int DV>
-static hipError_t launch_pack_t(const KParams& p, const float* S, const uint8_t* bits,
-                                const double* s_hat, const double* r, unsigned ntok,
-                                hipStream_t st) {
-  ProfScope ps("pack", st);
-  k_pack<DK, DV><<<p.B * p.H, 2 * DK, 0, st>>>(p, S, bits, s_hat, r, ntok);
-  return hipGetLastError();
-}
-
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st) {
-  if (p.dk == 64) return launch_pack_t<64, 64>(p, S, bits, s_hat, r, ntok, st);
-  if (p.dk == 256) return launch_pack_t<256, 256>(p, S, bits, s_hat, r, ntok, st);
-  return launch_pack_t<128, 128>(p, S, bits, s_hat, r, ntok, st);
+  const int nbh = p.B * p.H;
+  if (p.dk == 64) return launch("pack", k_pack<64, 64>, nbh, 128, 0, st, p, S, bits, s_hat, r, ntok);
+  if (p.dk == 256)
+    return launch("pack", k_pack<256, 256>, nbh, 512, 0, st, p, S, bits, s_hat, r, ntok);
+  return launch("pack", k_pack<128, 128>, nbh, 256, 0, st, p, S, bits, s_hat, r, ntok);
 }
 
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,
                          hipStream_t st) {
-  ProfScope ps("unpack", st);
+  const int nbh = p.B * p.H;
   const size_t dyn = p.state32 ? 0 : (size_t)(p.L.wc + 1) * p.dv * 4;
-  if (p.dk == 64)
-    k_unpack<64, 64><<<p.B * p.H, 128, dyn, st>>>(p, S, bits, s_hat, r);
-  else if (p.dk == 256)
-    k_unpack<256, 256><<<p.B * p.H, 512, dyn, st>>>(p, S, bits, s_hat, r);
-  else
-    k_unpack<128, 128><<<p.B * p.H, 256, dyn, st>>>(p, S, bits, s_hat, r);
-  return hipGetLastError();
+  if (p.dk == 64) return launch("unpack", k_unpack<64, 64>, nbh, 128, dyn, st, p, S, bits, s_hat, r);
+  if (p.dk == 256)
+    return launch("unpack", k_unpack<256, 256>, nbh, 512, dyn, st, p, S, bits, s_hat, r);
+  return launch("unpack", k_unpack<128, 128>, nbh, 256, dyn, st, p, S, bits, s_hat, r);
 }
 
 hipError_t launch_alloc_bits(const KParams& p, const double* gamma, const float* R, uint8_t* bits,
                              hipStream_t st) {
+  const int nbh = p.B * p.H;
+  hipError_t e;
   if (p.dk == 64)
-    k_weights_from_ranges<64><<<p.B * p.H, 64, 0, st>>>(p, gamma, R);
+    e = launch("weights", k_weights_from_ranges<64>, nbh, 64, 0, st, p, gamma, R);
   else if (p.dk == 256)
-    k_weights_from_ranges<256><<<p.B * p.H, 256, 0, st>>>(p, gamma, R);
+    e = launch("weights", k_weights_from_ranges<256>, nbh, 256, 0, st, p, gamma, R);
   else
-    k_weights_from_ranges<128><<<p.B * p.H, 128, 0, st>>>(p, gamma, R);
-  hipError_t e = hipGetLastError();
+    e = launch("weights", k_weights_from_ranges<128>, nbh, 128, 0, st, p, gamma, R);
   if (e != hipSuccess) return e;
   const int units = p.scope == 0 ? p.B : p.B * p.H;
   const int N = p.scope == 0 ? p.H * p.dk : p.dk;
-  ProfScope ps("alloc", st);
-  k_alloc<<<units, 1024, 0, st>>>(p.ws_c, N, p.need, p.bmin, p.bmax, bits);
-  return hipGetLastError();
+  return launch("alloc", k_alloc, units, 1024, 0, st, p.ws_c, N, p.need, p.bmin, p.bmax, bits);
 }
 
 hipError_t launch_window_gamma(const KParams& p, int W, int C, const float* q, const float* s,
                                const float* beta, const float* k, double* gamma, hipStream_t st) {
   const long long total = (long long)p.B * p.H * p.dk;
   const int bs = 256;
-  ProfScope ps("weights", st);
-  k_window_gamma<<<(unsigned)((total + bs - 1) / bs), bs, 0, st>>>(p.B, W, p.H, p.dk, C,
-                                                                   p.per_head, q, s, beta, k, gamma);
-  return hipGetLastError();
+  return launch("weights", k_window_gamma, (unsigned)((total + bs - 1) / bs), bs, 0, st, p.B, W,
+                p.H, p.dk, C, p.per_head, q, s, beta, k, gamma);
 }
 
 }  // namespace kda

@@ -19,8 +19,6 @@ bool g_on = false;          // per-kernel events
 bool g_count = false;       // quantiser work counter
 std::vector<Mark> g_marks;      // recorded since the last read
 std::vector<hipEvent_t> g_pool; // spare events
-const char* g_pending = nullptr;
-hipEvent_t g_pending_start = nullptr;
 unsigned long long* g_counter = nullptr;   // device memory, 8 bytes
 
 hipEvent_t take() {
@@ -36,23 +34,15 @@ hipEvent_t take() {
 
 }  // namespace
 
-void prof_begin(const char* kind, hipStream_t st) {
-  if (!g_on) return;
-  g_pending = kind;
-  g_pending_start = take();
-  if (g_pending_start) (void)hipEventRecord(g_pending_start, st);
+ProfEvents prof_events(const char* kind) {
+  if (!g_on) return {nullptr, nullptr};
+  hipEvent_t a = take(), b = take();
+  if (!a || !b) return {nullptr, nullptr};
+  g_marks.push_back({kind, a, b});
+  return {a, b};
 }
 
 unsigned long long* prof_counter() { return g_count ? g_counter : nullptr; }
-
-void prof_end(hipStream_t st) {
-  if (!g_on || !g_pending_start) return;
-  hipEvent_t stop = take();
-  if (!stop) return;
-  (void)hipEventRecord(stop, st);
-  g_marks.push_back({g_pending, g_pending_start, stop});
-  g_pending_start = nullptr;
-}
 
 }  // namespace kda
 

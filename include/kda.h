@@ -112,6 +112,19 @@ int kda_weights(const kda_config* cfg, int32_t W, int32_t C, const float* q,
                 const float* s, const float* beta, const float* k,
                 double* gamma, void* stream);
 
+/* Exact Gramian row weights (Prop. 1, eq. gram) over a window, with the full
+ * transition F_t = (I - beta_t k_t k_t^T) diag(exp(-s_t)) instead of the
+ * diagonal erase approximation: backward over the window,
+ *   M <- F_t^T (q_t q_t^T + M) F_t   for t = W-1 down to 1,
+ *   gamma_i = (1/W) sum_t chi_{t-1} M_ii,
+ * chi as in kda_weights (the exact-Gramian allocation the paper compares its
+ * estimate against, Sec. 3, State bit allocation).  Float64, O(d_k^2) per
+ * token and head.  Arguments and layouts as kda_weights; d_k <= 128
+ * (KDA_ERR_UNSUPPORTED otherwise: the matrix is held in registers). */
+int kda_weights_exact(const kda_config* cfg, int32_t W, int32_t C, const float* q,
+                      const float* s, const float* beta, const float* k,
+                      double* gamma, void* stream);
+
 /* Bit allocation (Sec. 3, eq. weight and eq. alloc, rounded, clipped and
  * adjusted to the budget): R~ = R / RMS_group(R), c = gamma * R~^2, widths
  * minimising sum c_i 2^(-2 b_i) with sum b_i = floor(mean_bits*N + 0.5) over

@@ -28,6 +28,7 @@ SIGNATURES = {
     "kda_workspace_bytes": (ctypes.c_size_t, [_CFG]),
     "kda_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "kda_weights": (ctypes.c_int, [_CFG, _I32, _I32, _P, _P, _P, _P, _P, _P]),
+    "kda_weights_exact": (ctypes.c_int, [_CFG, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "kda_alloc_bits": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P]),
     "kda_pack_state": (ctypes.c_int, [_CFG, _P, _P, _P, _P, ctypes.c_uint32, _P, _P]),
     "kda_unpack_state": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P, _P]),

@@ -93,6 +93,16 @@ def kda_weights(cfg, W, C, q, s, beta, k, gamma):
         _ptr(gamma, torch.float64, _rows(cfg), "gamma"), _stream()))
 
 
+def kda_weights_exact(cfg, W, C, q, s, beta, k, gamma):
+    n_s = cfg.B * W * cfg.H * (1 if cfg.decay_per_head else cfg.d_k)
+    _check(load().kda_weights_exact(
+        ctypes.byref(cfg.c()), W, C,
+        _ptr(q, torch.float32, cfg.B * W * cfg.H * cfg.d_k, "q"), _ptr(s, torch.float32, n_s, "s"),
+        _ptr(beta, torch.float32, cfg.B * W * cfg.H, "beta"),
+        _ptr(k, torch.float32, cfg.B * W * cfg.H * cfg.d_k, "k"),
+        _ptr(gamma, torch.float64, _rows(cfg), "gamma"), _stream()))
+
+
 def kda_alloc_bits(cfg, gamma, R, bits, ws):
     _check(load().kda_alloc_bits(
         ctypes.byref(cfg.c()), _ptr(gamma, torch.float64, _rows(cfg), "gamma"),

@@ -143,6 +143,18 @@ int kda_weights(const kda_config* cfg, int32_t W, int32_t C, const float* q, con
   return hip_status(kda::launch_window_gamma(p, W, C, q, s, beta, k, gamma, (hipStream_t)stream));
 }
 
+int kda_weights_exact(const kda_config* cfg, int32_t W, int32_t C, const float* q, const float* s,
+                      const float* beta, const float* k, double* gamma, void* stream) {
+  int need = 0;
+  int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (W < 1 || C < 1) return KDA_ERR_ARG;
+  if (!q || !s || !beta || !k || !gamma) return KDA_ERR_ARG;
+  if (cfg->d_k > 128) return KDA_ERR_UNSUPPORTED;   // the float64 matrix per head
+  KParams p = make_params(cfg, need);
+  return hip_status(kda::launch_exact_gamma(p, W, C, q, s, beta, k, gamma, (hipStream_t)stream));
+}
+
 int kda_alloc_bits(const kda_config* cfg, const double* gamma, const float* R, uint8_t* bits,
                    void* ws, void* stream) {
   int need = 0;

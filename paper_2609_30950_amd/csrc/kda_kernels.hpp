@@ -46,6 +46,8 @@ hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_ha
                          hipStream_t st);
 hipError_t launch_alloc_bits(const KParams& p, const double* gamma, const float* R, uint8_t* bits,
                              hipStream_t st);
+hipError_t launch_exact_gamma(const KParams& p, int W, int C, const float* q, const float* s,
+                              const float* beta, const float* k, double* gamma, hipStream_t st);
 hipError_t launch_window_gamma(const KParams& p, int W, int C, const float* q, const float* s,
                                const float* beta, const float* k, double* gamma, hipStream_t st);
 

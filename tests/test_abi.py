@@ -69,4 +69,10 @@ def test_null_pointers_rejected_before_launch():
     assert lib.kda_pack_state(ctypes.byref(cfg.c()), None, None, None, None, 0, None, None) == 1
     assert lib.kda_unpack_state(ctypes.byref(cfg.c()), None, None, None, None, None, None) == 1
     assert lib.kda_weights(ctypes.byref(cfg.c()), 0, 1, None, None, None, None, None, None) == 1
+    assert lib.kda_weights_exact(ctypes.byref(cfg.c()), 4, 1, None, None, None, None, None,
+                                 None) == 1
+    wide = K.Config(B=1, H=2, d_k=256, d_v=256, group_rows=256)
+    one = ctypes.c_void_p(1)
+    assert lib.kda_weights_exact(ctypes.byref(wide.c()), 4, 1, one, one, one, one, one,
+                                 one) == 3   # rejected before any launch
     assert lib.kda_status_str(3).decode() == "unsupported configuration"

@@ -75,6 +75,34 @@ def test_window_weights_match_oracle(C):
     np.testing.assert_allclose(host(g).reshape(2, 3, 64), want, rtol=1e-12)
 
 
+def _exact_oracle(x, b, h, C, per_head):
+    """Oracle exact-Gramian weights of head (b, h): matrices F_t from the
+    token's k, s, beta (eq. rule, KDA erase) and the backward recursion."""
+    q = x["q"][b, :, h].astype(np.float64)
+    ks = x["k"][b, :, h]
+    Wn = q.shape[0]
+    Fs = np.stack([stats.transition(ks[t], x["s"][b, t, h, 0] if per_head else x["s"][b, t, h],
+                                    float(x["beta"][b, t, h])) for t in range(Wn)])
+    return stats.exact_window_gamma(q, Fs, C)
+
+
+@pytest.mark.parametrize("d,C,per_head", [(64, 1, False), (64, 4, True), (128, 1, False),
+                                          (128, 3, False)])
+def test_exact_weights_match_oracle(d, C, per_head):
+    w = W.sized(W.WORKLOADS["gdn2" if per_head else "tiny"], B=2, H=2, dk=d, dv=d)
+    Wn = 40
+    x = W.tokens(w, 0, Wn)
+    cfg = K.Config(B=2, H=2, d_k=d, d_v=d, group_rows=d, decay_per_head=int(per_head))
+    g = torch.zeros(2 * 2 * d, dtype=torch.float64, device="cuda")
+    s_arg = x["s"][..., 0] if per_head else x["s"]
+    K.kda_weights_exact(cfg, Wn, C, dev(x["q"]), dev(s_arg), dev(x["beta"]), dev(x["k"]), g)
+    got = host(g).reshape(2, 2, d)
+    want = np.stack([[_exact_oracle(x, b, h, C, per_head) for h in range(2)] for b in range(2)])
+    err = float(np.max(np.abs(got - want) / np.abs(want)))
+    say(f"exact weights d={d} C={C} per_head={per_head}: max rel err {err:.2e}")
+    np.testing.assert_allclose(got, want, rtol=1e-9)
+
+
 def _weights_case(kind, rng, B, H, d):
     gamma = np.exp(rng.normal(0, 3, (B, H, d)))
     R = np.abs(rng.standard_normal((B, H, d))).astype(np.float32)

@@ -4,7 +4,9 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 
 * ``normalized_ranges``: R~_i = R_i / RMS of R over the output-normalisation
   group of row i (Sec. 2, Range normalization; Sec. 3 after eq. weight).
-  Groups are G consecutive rows of one head.  Sum of squares is sequential in
+  Groups are G consecutive rows: within one head (KDA, Gated DeltaNet), or
+  spanning consecutive heads (Mamba-2 normalises over 12 heads); the caller
+  passes the rows of all heads of a group along the last axis.  Sum of squares is sequential in
   row order in float64 (each R_j^2 is exact); RMS = sqrt(sum / G); a group with
   RMS 0 gives R~ = 0.
 * ``weights``: c_i = Gamma_i * (R~_i * R~_i)  (eq. weight).

@@ -8,6 +8,9 @@ DeltaNet choice stated after eq. rule):
 
     S_t = (I - k a^T) D S_{t-1} + k (w * v)^T,      o_t = S_t^T q.
 
+With erase=False the erase vector is a = 0 (Mamba-2 has no erasure, stated
+after eq. rule): S_t = D S_{t-1} + k (w * v)^T.
+
 ``truth_step`` evaluates that definition literally in float64 with explicit
 d_k x d_k matrices.  ``truth_step_rowform`` is the algebraically equal
 row form (I - b k k^T) D S = D S - b k (k^T D S), also float64.
@@ -19,6 +22,8 @@ row form (I - b k k^T) D S = D S - b k (k^T D S), also float64.
     g_i  = fl32(beta * k_i),   w_j = fl32(v_j - u_j)
     S_ij = fma32(g_i, w_j, S'_ij)
     o_j  = blockdot(q, S[:, j])
+
+(without erasure: w_j = v_j, and u is not formed.)
 
 blockdot: rows are cut into blocks of 32 consecutive rows; inside a block the
 products are accumulated sequentially from the first row with float32 fused
@@ -47,7 +52,7 @@ def truth_step(S, q, k, v, s, beta, erase=True):
     return S_new, S_new.T @ np.asarray(q, F64)
 
 
-def truth_step_rowform(S, q, k, v, s, beta):
+def truth_step_rowform(S, q, k, v, s, beta, erase=True):
     """Row form of the same update, float64, batched over leading axes.
 
     S: [..., dk, dv]; q, k, s: [..., dk] (s may be [..., 1]); v: [..., dv];
@@ -58,7 +63,7 @@ def truth_step_rowform(S, q, k, v, s, beta):
     beta = np.asarray(beta, F64)[..., None]
     a = np.exp(-np.asarray(s, F64))
     Sd = a[..., :, None] * S
-    u = np.einsum("...i,...ij->...j", k, Sd)
+    u = np.einsum("...i,...ij->...j", k, Sd) if erase else 0.0
     S_new = Sd + (beta * k)[..., :, None] * (np.asarray(v, F64) - u)[..., None, :]
     o = np.einsum("...i,...ij->...j", np.asarray(q, F64), S_new)
     return S_new, o
@@ -84,7 +89,7 @@ def decay_factors(s):
     return np.exp(-np.asarray(s, F32).astype(F64)).astype(F32)
 
 
-def mirror_step(S, q, k, v, s, beta):
+def mirror_step(S, q, k, v, s, beta, erase=True):
     """float32 contract form, batched: S [..., dk, dv] float32.
 
     s is [..., dk] (per-row decay) or [..., 1] (one rate per head).
@@ -93,9 +98,11 @@ def mirror_step(S, q, k, v, s, beta):
     S = np.asarray(S, F32)
     a = decay_factors(s)
     Sd = (a[..., :, None] * S).astype(F32)
-    u = blockdot(k, Sd)
     g = (np.asarray(beta, F32)[..., None] * np.asarray(k, F32)).astype(F32)
-    w = (np.asarray(v, F32) - u).astype(F32)
+    if erase:
+        w = (np.asarray(v, F32) - blockdot(k, Sd)).astype(F32)
+    else:
+        w = np.asarray(v, F32)
     S_new = fma32(g[..., :, None], w[..., None, :], Sd)
     o = blockdot(q, S_new)
     return S_new, o

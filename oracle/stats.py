@@ -9,14 +9,16 @@ through one may differ in the last float64 bit.
 
 * ``ema_init`` / ``ema_update``: the exponential moving averages of Sec. 3
   (State bit allocation): m_i tracks exp(2 g) = exp(-2 s) and e_i tracks
-  beta (2 - beta) k_i^2, with alpha = 2 / (span + 1); the first token of a
+  beta (2 - beta) k_i^2 (0 without erasure: the erase term comes from the
+  erase vector a = beta k), with alpha = 2 / (span + 1); the first token of a
   fresh state initialises both; updates are token-sequential, so any write-back
   interval C sees the same estimates.  s_hat = -log(m)/2, r = e/2.
 * ``gamma_hat``: eq. weight, 1 / expm1(2 (s_hat + r)), with s_hat + r clamped
   below at 1e-12 (the paper requires s > 0).
 * ``window_gamma``: eq. gram restricted to a window of W tokens with the
   diagonal erase approximation of Sec. 2 (Approximate erasure rate): per row,
-  lambda_t = exp(-2 s_t - beta_t (2 - beta_t) k_t^2),
+  lambda_t = exp(-2 s_t - beta_t (2 - beta_t) k_t^2)  (no erase term
+  without erasure),
   A_t = lambda_t (chi_{t-1} + A_{t-1}), Gamma = (1/W) sum_{t>=1} q_t^2 A_t,
   chi_tau = 1 when a write-back follows token tau.
 * ``exact_window_gamma`` / ``stationary_gamma``: the full matrix Gramian of
@@ -50,22 +52,24 @@ def decay_sample(s):
     return np.exp(F64(-2.0) * np.asarray(s, F32).astype(F64))
 
 
-def erase_sample(k, beta):
-    """y = (beta (2 - beta)) (k k), float64, each product rounded once."""
+def erase_sample(k, beta, erase=True):
+    """y = (beta (2 - beta)) (k k), float64, each product rounded once
+    (0 without erasure)."""
     b = np.asarray(beta, F32).astype(F64)
     kk = np.asarray(k, F32).astype(F64)
-    return (b * (F64(2.0) - b)) * (kk * kk)
+    y = (b * (F64(2.0) - b)) * (kk * kk)
+    return y if erase else np.zeros_like(y)
 
 
-def ema_init(s, k, beta):
-    return decay_sample(s), erase_sample(k, beta)
+def ema_init(s, k, beta, erase=True):
+    return decay_sample(s), erase_sample(k, beta, erase)
 
 
-def ema_update(m, e, s, k, beta, span):
+def ema_update(m, e, s, k, beta, span, erase=True):
     al = ema_alpha(span)
     om = F64(1.0) - al
     m = om * m + al * decay_sample(s)
-    e = om * e + al * erase_sample(k, beta)
+    e = om * e + al * erase_sample(k, beta, erase)
     return m, e
 
 
@@ -111,14 +115,14 @@ def writeback_positions(W, C, offset=0):
     return (t % C == 0).astype(F64)
 
 
-def window_gamma(q, s, k, beta, C):
+def window_gamma(q, s, k, beta, C, erase=True):
     """Windowed query-weighted decay sums, float64.
 
     q, s, k: [W, ..., dk]; beta: [W, ...].  Returns [..., dk].
     """
     q = np.asarray(q, F32).astype(F64)
     W = q.shape[0]
-    y = erase_sample(k, np.asarray(beta, F32)[..., None])
+    y = erase_sample(k, np.asarray(beta, F32)[..., None], erase)
     lam = np.exp(F64(-2.0) * np.asarray(s, F32).astype(F64) - y)
     chi = writeback_positions(W, C)
     A = np.zeros(q.shape[1:], F64)

@@ -42,6 +42,7 @@ class Cfg:
     b_min: int = 2
     b_max: int = 8
     span: int = 64
+    erase: bool = True              # False: no erasure (Mamba-2)
 
 
 def zero_state(B, H, cfg):
@@ -88,7 +89,12 @@ def write_back(S, m, e, ntok, cfg, gamma=None):
     s_hat, r = stats.ema_rates(m, e)
     g = stats.gamma_hat(s_hat, r) if gamma is None else np.asarray(gamma, F64)
     R = np.max(np.abs(S), axis=-1).astype(F32)
-    c = alloc.weights(g, alloc.normalized_ranges(R, cfg.G))
+    if cfg.G <= dk:
+        Rt = alloc.normalized_ranges(R, cfg.G)
+    else:
+        # groups of G rows across consecutive heads of a sequence
+        Rt = alloc.normalized_ranges(R.reshape(B, H * dk), cfg.G).reshape(B, H, dk)
+    c = alloc.weights(g, Rt)
     widths = allocate_widths(c, cfg)
     codes, scale, mstar = quant.quantize_rows(S.reshape(-1, dv), widths.reshape(-1))
     state = dict(ntok=np.asarray(ntok, np.int64), widths=widths,
@@ -102,11 +108,11 @@ def mirror_decode_step(state, q, k, v, s, beta, cfg, gamma=None):
     """One token for B x H heads.  q, k: [B,H,dk]; v: [B,H,dv]; s: [B,H,dk]
     or [B,H,1]; beta: [B,H].  Returns (new state, o [B,H,dv], diag)."""
     X = dequantize(state)
-    S, o = recurrence.mirror_step(X, q, k, v, s, beta)
+    S, o = recurrence.mirror_step(X, q, k, v, s, beta, cfg.erase)
     sr = _rows(s, cfg.dk)
     m0, e0 = ema_start(state)
-    mi, ei = stats.ema_init(sr, k, np.asarray(beta)[..., None])
-    mu, eu = stats.ema_update(m0, e0, sr, k, np.asarray(beta)[..., None], cfg.span)
+    mi, ei = stats.ema_init(sr, k, np.asarray(beta)[..., None], cfg.erase)
+    mu, eu = stats.ema_update(m0, e0, sr, k, np.asarray(beta)[..., None], cfg.span, cfg.erase)
     fresh = (state["ntok"] == 0)[..., None]
     m = np.where(fresh, mi, mu)
     e = np.where(fresh, ei, eu)
@@ -128,12 +134,12 @@ def mirror_prefill(state, q, k, v, s, beta, C, cfg, gamma=None):
     diags = []
     since = 0
     for t in range(T):
-        X, o = recurrence.mirror_step(X, q[:, t], k[:, t], v[:, t], s[:, t], beta[:, t])
+        X, o = recurrence.mirror_step(X, q[:, t], k[:, t], v[:, t], s[:, t], beta[:, t], cfg.erase)
         o_all[:, t] = o
         sr = _rows(s[:, t], cfg.dk)
         bt = np.asarray(beta[:, t])[..., None]
-        mi, ei = stats.ema_init(sr, k[:, t], bt)
-        mu, eu = stats.ema_update(m, e, sr, k[:, t], bt, cfg.span)
+        mi, ei = stats.ema_init(sr, k[:, t], bt, cfg.erase)
+        mu, eu = stats.ema_update(m, e, sr, k[:, t], bt, cfg.span, cfg.erase)
         m = np.where(fresh[..., None], mi, mu)
         e = np.where(fresh[..., None], ei, eu)
         fresh = np.zeros_like(fresh)
@@ -148,9 +154,9 @@ def mirror_prefill(state, q, k, v, s, beta, C, cfg, gamma=None):
     return state, o_all, diags
 
 
-def truth_outputs(X, q, k, v, s, beta):
+def truth_outputs(X, q, k, v, s, beta, erase=True):
     """float64 outputs of one token from the float32 state X (no quantisation)."""
-    return recurrence.truth_step_rowform(X, q, k, v, s, beta)[1]
+    return recurrence.truth_step_rowform(X, q, k, v, s, beta, erase)[1]
 
 
 def warm_state(q, k, v, s, beta, cfg):
@@ -166,12 +172,13 @@ def warm_state(q, k, v, s, beta, cfg):
     S = np.zeros((B, H, cfg.dk, cfg.dv), F64)
     m = e = None
     for t in range(T):
-        S, _ = recurrence.truth_step_rowform(S, q[:, t], k[:, t], v[:, t], s[:, t], beta[:, t])
+        S, _ = recurrence.truth_step_rowform(S, q[:, t], k[:, t], v[:, t], s[:, t], beta[:, t],
+                                             cfg.erase)
         sr = _rows(s[:, t], cfg.dk)
         bt = np.asarray(beta[:, t])[..., None]
         if m is None:
-            m, e = stats.ema_init(sr, k[:, t], bt)
+            m, e = stats.ema_init(sr, k[:, t], bt, cfg.erase)
         else:
-            m, e = stats.ema_update(m, e, sr, k[:, t], bt, cfg.span)
+            m, e = stats.ema_update(m, e, sr, k[:, t], bt, cfg.span, cfg.erase)
     st, _ = write_back(S.astype(F32), m, e, np.full((B, H), T, np.int64), cfg)
     return st, S

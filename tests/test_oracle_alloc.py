@@ -75,3 +75,15 @@ def test_allocation_orders_by_weight():
     b = alloc.allocate(c, 4.0, 2, 8)
     o = np.argsort(c)
     assert np.all(np.diff(b[o]) >= 0)
+
+
+def test_p12_groups_spanning_heads():
+    # Mamba-2 normalises over groups of several heads: the RMS of R~ is 1 over
+    # each group of consecutive rows, whichever heads they belong to
+    rng = np.random.default_rng(14)
+    B, H, dk = 2, 6, 16
+    R = np.abs(rng.standard_normal((B, H * dk))).astype(np.float32)
+    Rt = alloc.normalized_ranges(R, 3 * dk)
+    for g in range(2):
+        rms = np.sqrt(np.mean(Rt[:, 3 * dk * g:3 * dk * (g + 1)] ** 2, axis=1))
+        np.testing.assert_allclose(rms, 1.0, rtol=1e-14)

@@ -80,3 +80,40 @@ def test_blockdot_order_is_the_contract():
     M = np.zeros((128, 1), np.float32)
     M[0, 0], M[64, 0], M[32, 0], M[96, 0] = 1e8, -1e8, 1.0, 1.0
     assert rec.blockdot(x, M)[0] == np.float32(2.0)
+
+
+def test_no_erasure_is_the_decayed_sum_of_writes():
+    # without erasure (a = 0, Mamba-2) eq. rule is the linear recurrence
+    # S_T = diag(exp(-sum s)) S_0 + sum_t diag(exp(-sum_{tau>t} s_tau)) beta_t k_t v_t^T
+    rng = np.random.default_rng(21)
+    dk, dv, T = 16, 8, 12
+    S0 = rng.standard_normal((dk, dv))
+    ins = [_inputs(rng, dk, dv) for _ in range(T)]
+    S = S0.copy()
+    for q, k, v, s, beta in ins:
+        Sd, _ = rec.truth_step(S, q, k, v, s, beta, erase=False)
+        Sr, _ = rec.truth_step_rowform(S, q, k, v, s, beta, erase=False)
+        np.testing.assert_allclose(Sr, Sd, rtol=0, atol=1e-12)
+        S = Sd
+    ssum = np.sum([x[3] for x in ins], axis=0)
+    want = np.exp(-ssum)[:, None] * S0
+    for t, (q, k, v, s, beta) in enumerate(ins):
+        later = np.sum([x[3] for x in ins[t + 1:]], axis=0) if t + 1 < T else np.zeros(dk)
+        want += np.exp(-later)[:, None] * beta * np.outer(k, v)
+    np.testing.assert_allclose(S, want, rtol=1e-12, atol=1e-12)
+
+
+def test_no_erasure_mirror_tracks_truth():
+    rng = np.random.default_rng(22)
+    S = rng.standard_normal((2, 64, 64)).astype(np.float32)
+    q = rng.standard_normal((2, 64)); q /= np.linalg.norm(q, axis=-1, keepdims=True)
+    k = rng.standard_normal((2, 64)); k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((2, 64))
+    s = np.exp(rng.uniform(-5, 0, (2, 1)))
+    beta = rng.uniform(0, 1, 2)
+    args = [a.astype(np.float32) for a in (q, k, v, s, beta)]
+    Sm, om = rec.mirror_step(S, *args, erase=False)
+    St, ot = rec.truth_step_rowform(S.astype(np.float64), *[a.astype(np.float64) for a in args],
+                                    erase=False)
+    assert np.max(np.abs(Sm - St)) <= 4 * 2.0 ** -23 * np.max(np.abs(St))
+    assert np.max(np.abs(om - ot)) <= 64 * 2.0 ** -23 * np.max(np.abs(St))

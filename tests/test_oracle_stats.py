@@ -142,3 +142,34 @@ def test_p18_ema_constant_and_span_one():
     sh, r = stats.ema_rates(m0, e0)
     np.testing.assert_allclose(sh, 0.03, rtol=1e-6)
     np.testing.assert_allclose(r, 0.5 * 0.4 * 1.6 * 0.09, rtol=1e-6)
+
+
+@pytest.mark.parametrize("s", [0.05, 0.5])
+def test_no_erasure_window_weights_are_the_closed_form(s):
+    # Prop. 1: constant diagonal decay without erasure gives rho / expm1(2 s);
+    # with a = 0 the keys and beta must drop out of the window weights
+    W = 1024
+    rng = np.random.default_rng(23)
+    k = rng.standard_normal((W, 4)).astype(np.float32)
+    beta = rng.uniform(0, 2, W).astype(np.float32)
+    g = stats.window_gamma(np.ones((W, 4), np.float32), np.full((W, 4), s, np.float32), k, beta,
+                           C=1, erase=False)
+    lam = np.exp(-2 * np.float64(np.float32(s)))
+    np.testing.assert_allclose(g, _closed_finite(lam, W), rtol=1e-12)
+
+
+@pytest.mark.parametrize("C", [1, 3])
+def test_no_erasure_exact_gramian_is_the_diagonal_recursion(C):
+    # F = diag(exp(-s)) has a diagonal Gramian: the matrix recursion and the
+    # per-row recursion are two computations of the same numbers
+    rng = np.random.default_rng(24)
+    W, dk = 40, 5
+    qs = rng.standard_normal((W, dk)).astype(np.float32)
+    ss = np.exp(rng.uniform(np.log(1e-3), 0, (W, dk))).astype(np.float32)
+    ks = rng.standard_normal((W, dk)).astype(np.float32)
+    bs = rng.uniform(0, 1, W).astype(np.float32)
+    Fs = np.stack([stats.transition(ks[t], ss[t].astype(np.float64), bs[t], erase=False)
+                   for t in range(W)])
+    ge = stats.exact_window_gamma(qs.astype(np.float64), Fs, C)
+    gw = stats.window_gamma(qs, ss, ks, bs, C, erase=False)
+    np.testing.assert_allclose(ge, gw, rtol=1e-12)

@@ -94,3 +94,17 @@ def test_decay_weighting_gives_slow_rows_more_bits():
     m, e = stats.ema_init(s, np.zeros((1, 1, 64), np.float32), np.zeros((1, 1, 1), np.float32))
     st, _ = step.write_back(S, m, e, np.ones((1, 1), np.int64), cfg)
     assert st["widths"][0, 0, :32].min() > st["widths"][0, 0, 32:].max()
+
+
+def test_no_erasure_stores_zero_erase_rates_and_spans_heads():
+    # without erasure the erase statistic is 0, so the stored rate r is 0; the
+    # normalisation groups may span heads (G = 2 d_k)
+    w = W.sized(W.WORKLOADS["tiny"], B=1, H=4, dk=32, dv=32)
+    cfg = step.Cfg(dk=32, dv=32, G=64, mean_bits=3.0, b_min=1, b_max=8, erase=False)
+    xs = W.tokens(w, 0, 6)
+    st, S = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], cfg)
+    assert np.all(st["r16"] == 0)
+    R = np.max(np.abs(S.astype(np.float32)), axis=-1).astype(np.float32)
+    Rt = alloc.normalized_ranges(R.reshape(1, 4 * 32), 64)
+    assert np.allclose(np.sqrt(np.mean(Rt.reshape(2, 64) ** 2, axis=1)), 1.0)
+    assert int(st["widths"].sum()) == alloc.budget(3.0, 4 * 32)

@@ -67,7 +67,10 @@ typedef struct {
                              b_max <= 8)                                      */
   int32_t d_v;            /* columns (value channels): equal to d_k           */
   int32_t group_rows;     /* G: rows per output-normalisation group (Sec. 2,
-                             Range normalization); divides d_k                */
+                             Range normalization): divides d_k, or (groups
+                             spanning heads, as Mamba-2's 12-head groups) a
+                             multiple of d_k dividing H*d_k with
+                             KDA_SCOPE_SEQUENCE                               */
   int32_t scope;          /* allocation scope: KDA_SCOPE_SEQUENCE = all H*d_k
                              rows of a sequence share the budget (the paper's
                              layer budget, Sec. 3); KDA_SCOPE_HEAD = per head */
@@ -77,6 +80,9 @@ typedef struct {
   int32_t decay_per_head; /* 0: s is per row [.., H, d_k]; 1: one rate per
                              head [.., H] (Gated DeltaNet style, Sec. 1)      */
   int32_t state32;        /* 1: unquantised float32 state ("32-bit mode")     */
+  int32_t no_erase;       /* 1: no erasure, a_t = 0 in eq. rule (Mamba-2):
+                             S = D S + beta k v^T and no erase term in the
+                             rate statistics and weights; 0: KDA/GDN erase */
 } kda_config;
 
 /* Bytes of one (sequence, head) record slot; 0 if the config is invalid.

@@ -25,11 +25,12 @@ class Config:
     ema_span: int = 64
     decay_per_head: int = 0
     state32: int = 0
+    no_erase: int = 0          # 1: Mamba-2 style recurrence without erasure
 
     def c(self):
         return kda_config(self.B, self.H, self.d_k, self.d_v, self.group_rows, self.scope,
                           float(self.mean_bits), self.b_min, self.b_max, self.ema_span,
-                          self.decay_per_head, self.state32)
+                          self.decay_per_head, self.state32, self.no_erase)
 
 
 def _ptr(t, dtype=None, numel=None, name="tensor"):

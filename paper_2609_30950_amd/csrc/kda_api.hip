@@ -44,12 +44,21 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg->d_k != 64 && cfg->d_k != 128 && cfg->d_k != 256) return KDA_ERR_UNSUPPORTED;
   if (cfg->decay_per_head != 0 && cfg->decay_per_head != 1) return KDA_ERR_ARG;
   if (cfg->state32 != 0 && cfg->state32 != 1) return KDA_ERR_ARG;
+  if (cfg->no_erase != 0 && cfg->no_erase != 1) return KDA_ERR_ARG;
   if (cfg->state32) {
     if (need) *need = 0;
     return KDA_OK;
   }
-  if (cfg->group_rows < 1 || cfg->d_k % cfg->group_rows != 0) return KDA_ERR_ARG;
   if (cfg->scope != KDA_SCOPE_SEQUENCE && cfg->scope != KDA_SCOPE_HEAD) return KDA_ERR_ARG;
+  if (cfg->group_rows < 1) return KDA_ERR_ARG;
+  if (cfg->group_rows <= cfg->d_k) {
+    if (cfg->d_k % cfg->group_rows != 0) return KDA_ERR_ARG;
+  } else {
+    // groups spanning heads: whole heads, inside one sequence's budget
+    if (cfg->group_rows % cfg->d_k != 0 || (cfg->H * cfg->d_k) % cfg->group_rows != 0 ||
+        cfg->scope != KDA_SCOPE_SEQUENCE)
+      return KDA_ERR_ARG;
+  }
   if (cfg->b_min < 1 || cfg->b_max < cfg->b_min || cfg->b_max > 16) return KDA_ERR_ARG;
   if (cfg->d_k == 256 && cfg->b_max > 8) return KDA_ERR_UNSUPPORTED;   // LDS code tile
   if (cfg->ema_span < 1) return KDA_ERR_ARG;
@@ -75,6 +84,7 @@ KParams make_params(const kda_config* cfg, int need) {
   p.bmax = cfg->b_max;
   p.per_head = cfg->decay_per_head;
   p.state32 = cfg->state32;
+  p.no_erase = cfg->no_erase;
   p.need = need;
   p.alpha = 2.0 / (double)(cfg->ema_span + 1);
   p.one_minus_alpha = 1.0 - p.alpha;

@@ -255,7 +255,7 @@ __device__ __forceinline__ float combine_col(const float (&P)[DK / ROW_BLOCK][DV
 template <int DK, int DV, bool BF16>
 __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
                             RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out,
-                            float* w_out = nullptr) {
+                            bool erase, float* w_out = nullptr) {
   constexpr int CPL = DV / WAVE;
   static_assert(CPL <= 4, "columns per lane");
   const int w = threadIdx.x / WAVE, lane = lane_id();
@@ -288,7 +288,7 @@ __device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], co
   for (int c = 0; c < CPL; ++c) {
     const int col = lane + WAVE * c;
     const float u = combine_col<DK, DV>(sm.up, col);
-    wv[c] = vin[c] - u;
+    wv[c] = erase ? vin[c] - u : vin[c];   // no erasure: w = v
     acc[c] = 0.f;
     if (w_out != nullptr && w == 0) w_out[col] = wv[c];
   }
@@ -739,7 +739,7 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
   }
   auto ema = [&](const RowIn& x) {
     if (t < DK) {
-      const double zs = decay_sample(x.s), ys = erase_sample(x.k, x.beta);
+      const double zs = decay_sample(x.s), ys = p.no_erase ? 0.0 : erase_sample(x.k, x.beta);
       if (fresh) {
         m_run = zs;
         e_run = ys;
@@ -766,7 +766,7 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
       hv[DV + DK + t] = sm.rs.gq[t].x;   // g = fl32(beta k)
     }
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV, BF16>(X, sm.rs, sm.rsm, p.v, th * DV, p.o + th * DV,
+    recur_token<DK, DV, BF16>(X, sm.rs, sm.rsm, p.v, th * DV, p.o + th * DV, !p.no_erase,
                               compact ? hv : nullptr);
   }
   row_rates<DK>(p, bh, st, m_run, e_run, t);
@@ -781,6 +781,14 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
   }
   row_max<DK, DV>(X, st.R);
   __syncthreads();
+  if (p.G > DK) {
+    // groups spanning heads: the allocation pass forms R~ over the group
+    if (t < DK) {
+      p.ws_rpart[(size_t)bh * DK + t] = st.R[t];
+      p.ws_gam[(size_t)bh * DK + t] = st.gam[t];
+    }
+    return;
+  }
   row_weights<DK>(p, bh, st, t);
   if constexpr (HEAD) {
     // per-head budget: allocate here (c of this head is in LDS)
@@ -951,7 +959,7 @@ __global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
     load_rows<DK, BF16>(rs, p, bh, tok);
     __syncthreads();
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV);
+    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV, !p.no_erase);
   }
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r)
@@ -1027,21 +1035,8 @@ __global__ void __launch_bounds__(2 * DK) k_unpack(KParams p, float* S, uint8_t*
   }
 }
 
-// Weights c = gamma * R~^2 from given gamma and R (kda_alloc_bits).
-template <int DK>
-__global__ void __launch_bounds__(DK) k_weights_from_ranges(KParams p, const double* gamma,
-                                                            const float* R) {
-  const int bh = blockIdx.x;
-  const int t = threadIdx.x;
-  __shared__ __align__(16) StatSmem<DK> st;
-  st.R[t] = R[(size_t)bh * DK + t];
-  st.gam[t] = gamma[(size_t)bh * DK + t];
-  __syncthreads();
-  row_weights<DK>(p, bh, st, t);
-}
-
 // Windowed Gramian weights: one thread per (b, h, row), sequential in time.
-__global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head,
+__global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head, int no_erase,
                                const float* q, const float* s, const float* beta,
                                const float* k, double* gamma) {
   const long long id = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1054,7 +1049,7 @@ __global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head
   for (int t = 0; t < W; ++t) {
     const size_t tok = ((size_t)b * W + t) * H + h;
     const float sv = per_head ? s[tok] : s[tok * DKr + i];
-    const double y = erase_sample(k[tok * DKr + i], beta[tok]);
+    const double y = no_erase ? 0.0 : erase_sample(k[tok * DKr + i], beta[tok]);
     const double lam = exp(-2.0 * (double)sv - y);
     if (t >= 1) {
       const double chi = (t % C == 0) ? 1.0 : 0.0;  // write-back after token t-1
@@ -1082,6 +1077,7 @@ __global__ void k_window_gamma(int B, int W, int H, int DKr, int C, int per_head
 // operations as the matrix entry (r, r).
 template <int DK>
 __global__ void __launch_bounds__(DK * (DK / 32)) k_exact_gamma(int W, int H, int C, int per_head,
+                                                               int no_erase,
                                                                const float* q, const float* s,
                                                                const float* beta, const float* k,
                                                                double* gamma) {
@@ -1107,7 +1103,7 @@ __global__ void __launch_bounds__(DK * (DK / 32)) k_exact_gamma(int W, int H, in
       kv[t] = (double)k[tok * DK + t];
       dv[t] = exp(-(double)(per_head ? s[tok] : s[tok * DK + t]));
     }
-    const double bt = (double)beta[tok];
+    const double bt = no_erase ? 0.0 : (double)beta[tok];   // no erasure: F = D
     __syncthreads();
     const double qr = qv[r], kr = kv[r], dr = dv[r];
     // X = q q^T + M and this thread's part of u_r = (X k)_r
@@ -1184,7 +1180,8 @@ struct PfSmem {
 // One token on a slice (lane = column): the column-layout recurrence with
 // the row scalars of staged token j.  One barrier (before the u combine).
 template <int DK>
-__device__ __forceinline__ void recur_slice(float (&X)[ROW_BLOCK][1], PfSmem<DK>& ps, int j) {
+__device__ __forceinline__ void recur_slice(float (&X)[ROW_BLOCK][1], PfSmem<DK>& ps, int j,
+                                            bool erase) {
   const int w = threadIdx.x / WAVE, lane = lane_id();
   const float4 s0 = ps.rq[j][w * ROW_BLOCK + (lane & 15)];
   const float4 s1 = ps.rq[j][w * ROW_BLOCK + 16 + (lane & 15)];
@@ -1194,7 +1191,7 @@ __device__ __forceinline__ void recur_slice(float (&X)[ROW_BLOCK][1], PfSmem<DK>
   ps.up[j & 1][w][lane] = acc;
   __syncthreads();
   const float u = combine_col<DK, SLICE>(ps.up[j & 1], lane);
-  const float wv = ps.v[j][lane] - u;
+  const float wv = erase ? ps.v[j][lane] - u : ps.v[j][lane];   // no erasure: w = v
   acc = 0.f;
   pass2_16<0, 0, 1>(X, acc, s0.z, s0.w, wv);
   pass2_16<16, 0, 1>(X, acc, s1.z, s1.w, wv);
@@ -1269,7 +1266,8 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
     if (ema_here) {
       // token-sequential EMA of row t (the first token initialises a fresh record)
       for (int j = 0; j < nt; ++j) {
-        const double zs = ps.z[j][t], ys = erase_sample(ps.rq[j][t].y, ps.beta[j]);
+        const double zs = ps.z[j][t];
+        const double ys = p.no_erase ? 0.0 : erase_sample(ps.rq[j][t].y, ps.beta[j]);
         if (fresh0 && j0 + j == 0) {
           m_run = zs;
           e_run = ys;
@@ -1279,7 +1277,7 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
         }
       }
     }
-    for (int j = 0; j < nt; ++j) recur_slice<DK>(X, ps, j);
+    for (int j = 0; j < nt; ++j) recur_slice<DK>(X, ps, j, !p.no_erase);
     __syncthreads();
     for (int e = t; e < nt * SLICE; e += blockDim.x) {
       const int j = e / SLICE, c = e % SLICE;
@@ -1305,9 +1303,11 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
   }
 }
 
-// Weights of the rows of one scope unit from the per-slice row maxima and
-// Gamma (group RMS in float64, rows summed in order), then the allocation.
-__global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl) {
+// Weights of the rows of one scope unit from row maxima (given per slice:
+// Rp[row][nsl]) and Gamma (group RMS of G consecutive rows in float64, rows
+// summed in order; groups may span heads), then the allocation into bits.
+__global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl, const float* Rp,
+                                                       const double* gam, uint8_t* bits) {
   __shared__ AllocSmem sm;
   __shared__ __align__(16) float R[ALLOC_MAX_N];
   __shared__ double rms[ALLOC_MAX_N];
@@ -1315,7 +1315,7 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
   const int tid = threadIdx.x, nt = blockDim.x;
   const size_t row0 = (size_t)blockIdx.x * N;
   for (int n = tid; n < N; n += nt) {
-    const float* rp = p.ws_rpart + (row0 + n) * nsl;
+    const float* rp = Rp + (row0 + n) * nsl;
     float m = rp[0];
     for (int q = 1; q < nsl; ++q) m = fmaxf(m, rp[q]);
     R[n] = m;
@@ -1347,11 +1347,11 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
   for (int n = tid; n < N; n += nt) {
     const double rm = rms[n / G];
     const double Rt = rm > 0.0 ? (double)R[n] / rm : 0.0;
-    c[n] = p.ws_gam[row0 + n] * (Rt * Rt);
+    c[n] = gam[row0 + n] * (Rt * Rt);
   }
   __syncthreads();
   block_allocate<ALLOC_MAX_N / 1024>([&](int n) { return c[n]; }, N, p.need, p.bmin, p.bmax,
-                                     p.ws_bits + row0, sm);
+                                     bits + row0, sm);
 }
 
 // ------------------------------------------------------- launchers ---
@@ -1380,8 +1380,12 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases
                     : launch("stats", k_chunk<DK, DV, false, false>, nbh, 2 * DK, dyn, st, p);
     if (e != hipSuccess) return e;
     if (p.scope == 0) {
-      e = launch("alloc", k_alloc, p.B, 1024, 0, st, p.ws_c, p.H * DK, p.need, p.bmin, p.bmax,
-                 p.ws_bits);
+      if (p.G > DK)   // groups spanning heads: weights from the row maxima and Gamma
+        e = launch("alloc", k_alloc_slices, p.B, 1024, 0, st, p, p.H * DK, 1,
+                   (const float*)p.ws_rpart, (const double*)p.ws_gam, p.ws_bits);
+      else
+        e = launch("alloc", k_alloc, p.B, 1024, 0, st, p.ws_c, p.H * DK, p.need, p.bmin, p.bmax,
+                   p.ws_bits);
       if (e != hipSuccess) return e;
     }
   }
@@ -1415,7 +1419,8 @@ static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
   if (e != hipSuccess) return e;
   const int units = p.scope == 0 ? p.B : p.B * p.H;
   const int N = p.scope == 0 ? p.H * DK : DK;
-  e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl);
+  e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl, (const float*)p.ws_rpart,
+             (const double*)p.ws_gam, p.ws_bits);
   if (e != hipSuccess) return e;
   if (DK > 128 || p.bmax <= 8)
     return launch("requant", k_requant<DK, DK, false, true>, p.B * p.H, 2 * DK, 0, st, p);
@@ -1464,28 +1469,19 @@ hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_ha
 
 hipError_t launch_alloc_bits(const KParams& p, const double* gamma, const float* R, uint8_t* bits,
                              hipStream_t st) {
-  const int nbh = p.B * p.H;
-  hipError_t e;
-  if (p.dk == 64)
-    e = launch("weights", k_weights_from_ranges<64>, nbh, 64, 0, st, p, gamma, R);
-  else if (p.dk == 256)
-    e = launch("weights", k_weights_from_ranges<256>, nbh, 256, 0, st, p, gamma, R);
-  else
-    e = launch("weights", k_weights_from_ranges<128>, nbh, 128, 0, st, p, gamma, R);
-  if (e != hipSuccess) return e;
   const int units = p.scope == 0 ? p.B : p.B * p.H;
   const int N = p.scope == 0 ? p.H * p.dk : p.dk;
-  return launch("alloc", k_alloc, units, 1024, 0, st, p.ws_c, N, p.need, p.bmin, p.bmax, bits);
+  return launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, 1, R, gamma, bits);
 }
 
 hipError_t launch_exact_gamma(const KParams& p, int W, int C, const float* q, const float* s,
                               const float* beta, const float* k, double* gamma, hipStream_t st) {
   const int nbh = p.B * p.H;
   if (p.dk == 64)
-    return launch("weights", k_exact_gamma<64>, nbh, 128, 0, st, W, p.H, C, p.per_head, q, s, beta,
-                  k, gamma);
-  return launch("weights", k_exact_gamma<128>, nbh, 512, 0, st, W, p.H, C, p.per_head, q, s, beta,
-                k, gamma);
+    return launch("weights", k_exact_gamma<64>, nbh, 128, 0, st, W, p.H, C, p.per_head,
+                  p.no_erase, q, s, beta, k, gamma);
+  return launch("weights", k_exact_gamma<128>, nbh, 512, 0, st, W, p.H, C, p.per_head, p.no_erase,
+                q, s, beta, k, gamma);
 }
 
 hipError_t launch_window_gamma(const KParams& p, int W, int C, const float* q, const float* s,
@@ -1493,7 +1489,7 @@ hipError_t launch_window_gamma(const KParams& p, int W, int C, const float* q, c
   const long long total = (long long)p.B * p.H * p.dk;
   const int bs = 256;
   return launch("weights", k_window_gamma, (unsigned)((total + bs - 1) / bs), bs, 0, st, p.B, W,
-                p.H, p.dk, C, p.per_head, q, s, beta, k, gamma);
+                p.H, p.dk, C, p.per_head, p.no_erase, q, s, beta, k, gamma);
 }
 
 }  // namespace kda

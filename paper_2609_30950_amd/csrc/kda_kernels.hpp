@@ -11,6 +11,7 @@ namespace kda {
 // Everything a kernel needs, passed by value.
 struct KParams {
   int B, H, dk, dv, G, scope, bmin, bmax, per_head, state32;
+  int no_erase;             // 1: no erasure (w = v, no erase statistic)
   int need;                 // granted slots per scope unit: K - N * b_min
   double alpha, one_minus_alpha;
   Layout L;

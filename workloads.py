@@ -19,6 +19,9 @@ Recipes (the paper's models and data are not available; these stand in):
             (b, h, channel): 10% logU[1e-4, 1e-3), else logU[1e-3, 2]
   gdn       B=16 H=16 d=256  T=4096  one s per (b, h, token): logU[1e-4, 1]
   long      B=128 H=32 d=128 T=32768 v ~ Student-t(3); decay as tiny
+  mamba2    B=16 H=24 d=128 T=4096  Mamba-2-style layer: one rate per (b, h,
+            token) logU[1e-4, 1], no erasure, normalisation groups of 12 heads
+            (1536 rows), mean 4 bits, widths [1,8]; draws as tiny otherwise
 """
 from dataclasses import dataclass, field
 
@@ -43,6 +46,7 @@ class Workload:
     bf16: bool = False
     warmup: int = 0
     window: int = 0
+    erase: bool = True           # False: no erasure (Mamba-2)
 
 
 WORKLOADS = {
@@ -57,6 +61,8 @@ WORKLOADS = {
                      G=256, decay="head"),
     "long": Workload("long", 128, 32, 128, 128, 32768, C=1, mean_bits=3.0, b_min=2, b_max=8,
                      G=64, v_dist="t3", window=1024),
+    "mamba2": Workload("mamba2", 16, 24, 128, 128, 4096, C=1, mean_bits=4.0, b_min=1, b_max=8,
+                       G=12 * 128, decay="head", erase=False),
 }
 
 

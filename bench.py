@@ -73,7 +73,8 @@ def cpu_baseline(name, budget_s=12.0, warm_tokens=32):
     budget_s seconds, after a short oracle warm-up of its own."""
     from oracle import step
     w = W.WORKLOADS[name]
-    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                  erase=w.erase)
     base = W.base_rates(w)
     xs = {n: [] for n in ("q", "k", "v", "s", "beta")}
     for t in range(warm_tokens):
@@ -204,12 +205,86 @@ def run_prefill(args, K, torch):
     print(json.dumps(out), flush=True)
 
 
+def kcfg(K, w, **kw):
+    """Library config of workload w."""
+    return K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                    b_min=w.b_min, b_max=w.b_max, decay_per_head=int(w.decay == "head"),
+                    no_erase=int(not w.erase), **kw)
+
+
+# float64 lane-ops of the exact Gramian recursion per matrix element and token:
+# X = q q^T + M, u += X k, two rank-one corrections, the decay product d_i d_j
+# and its multiply
+EXACT_OPS_PER_ELEMENT = 6
+
+
+def run_weights(args, K, torch):
+    """Window weights of the long-context layer (B=128 H=32 d=128, W=1024):
+    the exact Gramian recursion (kda_weights_exact, dominant) and the
+    diagonal-erase estimate (kda_weights), one call each per pass."""
+    w = W.WORKLOADS["long"]
+    Wn = w.window
+    t0 = time.time()
+    xs = W.tokens(W.sized(w, B=2), 0, Wn)
+    print(f"# weights inputs (2 sequences, tiled to {w.B}) in {time.time() - t0:.1f}s",
+          file=sys.stderr, flush=True)
+    rep = w.B // 2
+    dev = {n: torch.from_numpy(np.ascontiguousarray(a)).cuda().repeat(
+        (rep,) + (1,) * (a.ndim - 1)).contiguous() for n, a in xs.items()}
+    del xs
+    cfg = kcfg(K, w)
+    g = torch.zeros(w.B * w.H * w.dk, dtype=torch.float64, device="cuda")
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        K.kda_profile_enable(K.api.PROFILE_EVENTS)
+        K.kda_profile_read()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(reps):
+            fn()
+        ev1.record()
+        torch.cuda.synchronize()
+        prof = K.kda_profile_read()
+        K.kda_profile_enable(0)
+        return ev0.elapsed_time(ev1) / reps, prof["weights"][0] / prof["weights"][1]
+
+    reps = max(2, args.steps // 20)
+    ms_exact, k_exact = timed(lambda: K.kda_weights_exact(
+        cfg, Wn, 1, dev["q"], dev["s"], dev["beta"], dev["k"], g), reps)
+    ms_diag, k_diag = timed(lambda: K.kda_weights(
+        cfg, Wn, 1, dev["q"], dev["s"], dev["beta"], dev["k"], g), reps)
+    nbh = w.B * w.H
+    ops = float(EXACT_OPS_PER_ELEMENT) * nbh * (Wn - 1) * w.dk * w.dk
+    ach = ops / (k_exact * 1e-3) / 1e12
+    in_bytes = nbh * Wn * (4 * w.dk * 3 + 4)          # q, k, s, beta
+    out = {
+        "metric": "head-windows/s, exact Gramian row weights (1024-token window)",
+        "value": nbh / (ms_exact * 1e-3), "unit": "head-windows/s",
+        "n_gpus": 1, "steps": reps, "warmup": 1, "ms_per_step": ms_exact,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"weights B={w.B} H={w.H} d_k={w.dk} W={Wn} C=1, long-context "
+                               f"inputs (2 sequences tiled)"},
+        "diagonal_estimate_ms": ms_diag,
+        "diagonal_estimate_hbm_GBps": in_bytes / (k_diag * 1e-3) / 1e9,
+        "roofline": dict(bound="alu", achieved=ach, peak=VALU_PEAK_TOPS, unit="TOP/s",
+                         frac=ach / VALU_PEAK_TOPS, traffic=None, kernel="weights (exact)",
+                         lane_ops_per_launch=ops),
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode", choices=["decode", "prefill"])
+    ap.add_argument("--workload", default="decode",
+                    choices=["decode", "prefill", "mamba2", "weights"])
     ap.add_argument("--layers", type=int, default=20)
     ap.add_argument("--warm-tokens", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -224,7 +299,6 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    w = W.WORKLOADS[args.workload]
     import torch
     import paper_2609_30950_amd as K
 
@@ -232,8 +306,11 @@ def main():
     if args.workload == "prefill":
         run_prefill(args, K, torch)
         return
-    cfg = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
-                   b_min=w.b_min, b_max=w.b_max)
+    if args.workload == "weights":
+        run_weights(args, K, torch)
+        return
+    w = W.WORKLOADS[args.workload]
+    cfg = kcfg(K, w)
     ws = K.new_workspace(cfg)
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
     base = W.base_rates(w)
@@ -304,7 +381,8 @@ def main():
     # plus the budgeted code bits), inputs q, k, v, s, beta and outputs o
     meta = 16 + w.dk // 2 + 6 * w.dk
     code_bytes = w.mean_bits * elems / 8
-    io = w.B * w.H * (4 * (w.dk * 3 + w.dv) + 4)
+    s_elems = 1 if w.decay == "head" else w.dk
+    io = w.B * w.H * (4 * (w.dk * 2 + s_elems + w.dv) + 4 + 4 * w.dv)   # q k s v beta, o
     step_bytes = 2 * (w.B * w.H * meta + code_bytes) + io
     hbm = step_bytes / (ms * 1e-3) / 1e9
     evals_per_launch = (fit_evals or 0) / max(1, kern.get("requant", {}).get("launches", 1))
@@ -339,9 +417,12 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"decode step B={w.B} H={w.H} d_k=d_v={w.dk}, mean {w.mean_bits} "
-                               f"bits, widths [{w.b_min},{w.b_max}], groups of {w.G} rows, layer "
-                               f"budget, prior state after {args.warm_tokens} warm-up decode tokens",
+        "config": {"workload": f"{w.name} decode step B={w.B} H={w.H} d_k=d_v={w.dk}, mean "
+                               f"{w.mean_bits} bits, widths [{w.b_min},{w.b_max}], groups of "
+                               f"{w.G} rows, layer budget, "
+                               f"{'per-head' if w.decay == 'head' else 'per-channel'} decay, "
+                               f"{'KDA erase' if w.erase else 'no erasure'}, prior state after "
+                               f"{args.warm_tokens} warm-up decode tokens",
                    "layers_rotated": L},
         "hbm_GBps_step": hbm,
         "hbm_frac_step": hbm / HBM_PEAK_GBPS,
@@ -350,7 +431,7 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
         "roofline": roof,
     }
-    if not args.no_ref32:
+    if not args.no_ref32 and w.name == "decode":
         del layers
         out["state32_reference"] = run_state32_reference(w, args, K, torch)
     if not args.no_cpu_baseline:

@@ -35,8 +35,10 @@
  * - Records, workspace and state arrays must be 16-byte aligned (device
  *   allocations are); misaligned pointers give KDA_ERR_ARG.
  * - Workspace: kda_workspace_bytes() bytes, used as scratch by one call at a
- *   time (per-row weights, widths, rate codes and the float32 state between
- *   the passes of a write-back).  Concurrent calls must not share one.
+ *   time (per-row weights, widths, rate codes, and between the passes of a
+ *   write-back either the token's vectors a, g, w (decode, d_k <= 128: the
+ *   requantisation rebuilds the state from the record) or the float32 state
+ *   (prefill, d_k = 256)).  Concurrent calls must not share one.
  */
 #ifndef KDA_H_
 #define KDA_H_
@@ -99,7 +101,8 @@ typedef struct {
  * 32-bit mode: the float32 state, row-major [d_k][d_v]. */
 size_t kda_record_bytes(const kda_config* cfg);
 
-/* Bytes of workspace kda_step / kda_prefill / kda_alloc_bits need. */
+/* Bytes of workspace kda_step / kda_prefill / kda_alloc_bits need.  Any
+ * contents are valid on entry. */
 size_t kda_workspace_bytes(const kda_config* cfg);
 
 /* Static description of a status code. */
@@ -107,7 +110,8 @@ const char* kda_status_str(int status);
 
 /* Windowed observability-Gramian row weights (Prop. 1, eq. gram, with the
  * diagonal erase approximation of Sec. 2, Approximate erasure rate):
- *   lambda_t,i = exp(-2 s_t,i - beta_t (2 - beta_t) k_t,i^2),
+ *   lambda_t,i = exp(-2 s_t,i - beta_t (2 - beta_t) k_t,i^2)   (no erase
+ *                term with no_erase),
  *   A_0 = 0, A_t = lambda_t (chi_{t-1} + A_{t-1}),
  *   gamma_i = (1/W) sum_{t=1}^{W-1} q_t,i^2 A_t,i,
  * chi_tau = 1 when a write-back follows token tau ((tau+1) % C == 0).
@@ -135,8 +139,10 @@ int kda_weights_exact(const kda_config* cfg, int32_t W, int32_t C, const float* 
  * adjusted to the budget): R~ = R / RMS_group(R), c = gamma * R~^2, widths
  * minimising sum c_i 2^(-2 b_i) with sum b_i = floor(mean_bits*N + 0.5) over
  * each scope unit of N rows; ties to the lower row index.
+ * Groups of G rows may span heads (see group_rows).
  * In:  gamma [B][H][d_k] f64 (>= 0); R [B][H][d_k] f32 row absolute maxima.
- * Out: bits [B][H][d_k] u8.  ws: workspace (scratch for the weights). */
+ * Out: bits [B][H][d_k] u8.  ws: a workspace of kda_workspace_bytes (the
+ * weights are formed in LDS; it is checked, not written). */
 int kda_alloc_bits(const kda_config* cfg, const double* gamma, const float* R,
                    uint8_t* bits, void* ws, void* stream);
 
@@ -170,12 +176,13 @@ int kda_step(const kda_config* cfg, void* records, const float* q,
  * later work (the outputs precede the quantisation, Sec. 2, so the next
  * layer needs only the first phase).
  * kda_step_outputs: the token's recurrence, outputs o, rate statistics,
- *   weights and widths; the float32 state after the token is left in ws.
- *   Records are only read.  Arguments as kda_step.
- * kda_step_writeback: quantise the state left in ws with those widths and
- *   rewrite the records in place.  Must follow kda_step_outputs of the same
- *   records and ws (stream order or an event), before ws or the records are
- *   used by another call.  Not available in 32-bit mode (kda_step_outputs
+ *   weights and widths; what the write-back needs of the state after the
+ *   token is left in ws (the token's vectors for d_k <= 128, else the float32
+ *   state).  Records are only read.  Arguments as kda_step.
+ * kda_step_writeback: quantise the state after the token (rebuilt from the
+ *   unchanged records and ws) with those widths and rewrite the records in
+ *   place.  Must follow kda_step_outputs of the same records and ws (stream
+ *   order or an event), before ws or the records are used by another call.  Not available in 32-bit mode (kda_step_outputs
  *   then does the whole step and kda_step_writeback returns KDA_OK).
  * kda_step(...) is kda_step_outputs(...) then kda_step_writeback(...) on one
  * stream. */

@@ -1303,6 +1303,225 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
   }
 }
 
+// ------------------------------------- prefill: row blocks in one wave ---
+//
+// The same chunk on 64-column slices for d_k <= 128, with the d_k / 32 row
+// blocks of a column held by one wave: lane l of wave w has row block
+// rb = l / CPW and slice column w * CPW + l % CPW (CPW = 64 / (d_k / 32)
+// columns per wave), rows 32 rb .. 32 rb + 31 in registers.  The partial sums
+// of a column's row blocks meet inside the wave: permlane32 swaps pair row
+// blocks rb and rb + 2 (or rb + 1 when there are two), permlane16 swaps then
+// pair rb and rb + 1, the contract's halving order with the same operands.
+// So a token needs no barrier; row scalars still reach the lanes by DPP
+// row broadcasts (a 16-lane DPP row lies inside one row block).
+
+// Sum of the partials of the row blocks of a column (see above); every lane
+// of the column receives the total.
+template <int NRB>
+__device__ __forceinline__ float rowblock_sum(float x) {
+  static_assert(NRB == 2 || NRB == 4, "row blocks per wave");
+  const int xi = __builtin_bit_cast(int, x);
+  const auto a = __builtin_amdgcn_permlane32_swap(xi, xi, false, false);
+  x = __builtin_bit_cast(float, (int)a[0]) + __builtin_bit_cast(float, (int)a[1]);
+  if constexpr (NRB == 4) {
+    const int yi = __builtin_bit_cast(int, x);
+    const auto c = __builtin_amdgcn_permlane16_swap(yi, yi, false, false);
+    x = __builtin_bit_cast(float, (int)c[0]) + __builtin_bit_cast(float, (int)c[1]);
+  }
+  return x;
+}
+
+// Maximum over the CPW lanes of a row block (every lane receives it).
+template <int CPW>
+__device__ __forceinline__ float rowblock_max(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));    // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_f<0x4E>(v));    // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_f<0x141>(v));   // row_half_mirror
+  v = fmaxf(v, dpp_f<0x140>(v));   // row_mirror: the 16-lane row's maximum
+  if constexpr (CPW == 32) {
+    const int vi = __builtin_bit_cast(int, v);
+    const auto c = __builtin_amdgcn_permlane16_swap(vi, vi, false, false);
+    v = fmaxf(__builtin_bit_cast(float, (int)c[0]), __builtin_bit_cast(float, (int)c[1]));
+  }
+  return v;
+}
+
+template <int DK>
+struct PcSmem {
+  static constexpr int TS = 16;
+  static constexpr int NRB = DK / ROW_BLOCK;
+  float4 rq[TS][DK];        // {fl32(exp(-s)), k, fl32(beta k), q} of (token, row)
+  double z[TS][DK];         // exp(-2 s): EMA decay samples (slice 0)
+  float beta[TS];
+  float v[TS][SLICE];
+  float o[TS][SLICE];
+  float Rw[NRB][DK];        // row maxima of each wave's columns
+};
+
+template <int DK, bool BF16>
+__global__ void __launch_bounds__(2 * DK) k_chunk_cols(KParams p) {
+  constexpr int NRB = DK / ROW_BLOCK;       // row blocks = waves per block
+  constexpr int CPW = WAVE / NRB;           // columns per wave
+  constexpr int TS = PcSmem<DK>::TS;
+  constexpr int NQ = TS / 2;                // tokens staged per thread and batch
+  constexpr int NV = TS * SLICE / (2 * DK); // values of v staged per thread and batch
+  static_assert(NRB * CPW == SLICE && CPW >= 16, "16-lane DPP rows inside a row block");
+  const int nsl = p.dv / SLICE;
+  const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
+  const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
+  const int rb = lane / CPW, col = w * CPW + lane % CPW;   // slice-local column
+  const int b = bh / p.H, h = bh % p.H;
+  const Layout L = p.L;
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ PcSmem<DK> ps;
+  extern __shared__ uint4 dyn_lds[];
+  uint32_t* words = (uint32_t*)dyn_lds;
+  // token inputs of one batch in registers: thread t holds row t % DK of
+  // tokens 2q + t / DK, and NV values of v; the next batch's loads are in
+  // flight while the current batch runs
+  const int si = t % DK, sj = t / DK;
+  float sv[NQ], kv[NQ], qv[NQ], bt[NQ], vv[NV];
+  auto issue = [&](int j0) {
+    const int nt = min(TS, p.ntk - j0);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int j = 2 * q + sj;
+      const size_t th = ((size_t)b * p.T + p.tok0 + j0 + min(j, nt - 1)) * p.H + h;
+      sv[q] = p.per_head ? p.s[th] : p.s[th * DK + si];
+      kv[q] = in_f32<BF16>(p.k, th * DK + si);
+      qv[q] = in_f32<BF16>(p.q, th * DK + si);
+      bt[q] = p.beta[th];
+    }
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int e = t + u * (2 * DK), j = e / SLICE, c = e % SLICE;
+      const size_t th = ((size_t)b * p.T + p.tok0 + j0 + min(j, nt - 1)) * p.H + h;
+      vv[u] = in_f32<BF16>(p.v, th * p.dv + sl * SLICE + c);
+    }
+  };
+  auto stage = [&](int nt) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int j = 2 * q + sj;
+      if (j < nt) {
+        ps.rq[j][si] = make_float4((float)exp(-(double)sv[q]), kv[q], bt[q] * kv[q], qv[q]);
+        if (sl == 0) ps.z[j][si] = decay_sample(sv[q]);
+        if (si == 0) ps.beta[j] = bt[q];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int e = t + u * (2 * DK);
+      ps.v[e / SLICE][e % SLICE] = vv[u];
+    }
+  };
+  auto write_o = [&](int j0, int nt) {
+    for (int e = t; e < nt * SLICE; e += blockDim.x) {
+      const int j = e / SLICE, c = e % SLICE;
+      const size_t th = ((size_t)b * p.T + p.tok0 + j0 + j) * p.H + h;
+      p.o[th * p.dv + sl * SLICE + c] = ps.o[j][c];
+    }
+  };
+  if (p.ntk > 0) issue(0);
+  {
+    // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
+    const uint4* src = (const uint4*)(rec + L.codes_off);
+    constexpr int Q = SLICE / 4;
+    const int n4 = L.wc * Q;
+    for (int e = t; e < n4; e += blockDim.x)
+      ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
+  }
+  load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
+  float X[ROW_BLOCK][1];
+  // decode rows 32 rb + r of this lane's column: descriptors per lane (the
+  // row blocks of a wave differ), x^ = (code + add) mul as in unpack_cols
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r) {
+    const uint4 d = meta.desc[rb * ROW_BLOCK + r];
+    const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
+    const uint32_t lo = words[d.x + col], hi = words[d.x + SLICE + col];
+    const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
+    X[r][0] = ((float)code + __builtin_bit_cast(float, d.w)) * __builtin_bit_cast(float, d.z);
+  }
+  const bool ema_here = sl == 0 && t < DK;
+  const bool fresh0 = meta.ntok == 0;
+  double m_run = 0.0, e_run = 0.0;
+  if (ema_here && !fresh0) {
+    m_run = exp(-2.0 * logq_decode(meta.z[t]));
+    e_run = 2.0 * (double)f16_to_f32(meta.r16[t]);
+  }
+  const bool erase = !p.no_erase;
+  int prev0 = 0, prevn = 0;
+  for (int j0 = 0; j0 < p.ntk; j0 += TS) {
+    const int nt = min(TS, p.ntk - j0);
+    __syncthreads();   // the previous batch's readers are done with the tables
+    if (prevn > 0) write_o(prev0, prevn);
+    stage(nt);
+    if (j0 + TS < p.ntk) issue(j0 + TS);
+    __syncthreads();
+    if (ema_here) {
+      // token-sequential EMA of row t (the first token initialises a fresh record)
+      for (int j = 0; j < nt; ++j) {
+        const double zs = ps.z[j][t];
+        const double ys = erase ? erase_sample(ps.rq[j][t].y, ps.beta[j]) : 0.0;
+        if (fresh0 && j0 + j == 0) {
+          m_run = zs;
+          e_run = ys;
+        } else {
+          m_run = p.one_minus_alpha * m_run + p.alpha * zs;
+          e_run = p.one_minus_alpha * e_run + p.alpha * ys;
+        }
+      }
+    }
+    for (int j = 0; j < nt; ++j) {
+      // rows 32 rb + lane % 16 and 32 rb + 16 + lane % 16: DPP broadcast sources
+      const float4 s0 = ps.rq[j][rb * ROW_BLOCK + (lane & 15)];
+      const float4 s1 = ps.rq[j][rb * ROW_BLOCK + 16 + (lane & 15)];
+      const float vj = ps.v[j][col];
+      float acc = 0.f;
+      pass1_16<0, 0, 1>(X, acc, s0.x, s0.y);
+      pass1_16<16, 0, 1>(X, acc, s1.x, s1.y);
+      const float u = rowblock_sum<NRB>(acc);
+      const float wv = erase ? vj - u : vj;   // no erasure: w = v
+      acc = 0.f;
+      pass2_16<0, 0, 1>(X, acc, s0.z, s0.w, wv);
+      pass2_16<16, 0, 1>(X, acc, s1.z, s1.w, wv);
+      const float o = rowblock_sum<NRB>(acc);
+      if (rb == 0) ps.o[j][col] = o;
+    }
+    prev0 = j0;
+    prevn = nt;
+  }
+  __syncthreads();
+  write_o(prev0, prevn);
+  {
+    // float32 state after the chunk (this lane's column), row-major
+    float* dstS = p.ws_s32 + (size_t)bh * DK * p.dv + sl * SLICE + col;
+#pragma unroll
+    for (int r = 0; r < ROW_BLOCK; ++r) dstS[(size_t)(rb * ROW_BLOCK + r) * p.dv] = X[r][0];
+  }
+  // row maxima over the slice: the wave's columns, then the waves
+#pragma unroll
+  for (int r = 0; r < ROW_BLOCK; ++r) {
+    const float m = rowblock_max<CPW>(fabsf(X[r][0]));
+    if (lane % CPW == 0) ps.Rw[w][rb * ROW_BLOCK + r] = m;
+  }
+  __syncthreads();
+  if (t < DK) {
+    float m = ps.Rw[0][t];
+#pragma unroll
+    for (int q = 1; q < NRB; ++q) m = fmaxf(m, ps.Rw[q][t]);
+    p.ws_rpart[((size_t)bh * DK + t) * nsl + sl] = m;
+  }
+  if (ema_here) {
+    const double s_hat = -0.5 * log(m_run);
+    const double r = 0.5 * e_run;
+    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
+  }
+}
+
 // Weights of the rows of one scope unit from row maxima (given per slice:
 // Rp[row][nsl]) and Gamma (group RMS of G consecutive rows in float64, rows
 // summed in order; groups may span heads), then the allocation into bits.
@@ -1413,9 +1632,13 @@ template <int DK>
 static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
   const int nsl = p.dv / SLICE;
   const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
-  hipError_t e = p.in_bf16
-      ? launch("stats", k_chunk_slices<DK, true>, p.B * p.H * nsl, 2 * DK, dyn, st, p)
-      : launch("stats", k_chunk_slices<DK, false>, p.B * p.H * nsl, 2 * DK, dyn, st, p);
+  hipError_t e;
+  if constexpr (DK <= 128)
+    e = p.in_bf16 ? launch("stats", k_chunk_cols<DK, true>, p.B * p.H * nsl, 2 * DK, dyn, st, p)
+                  : launch("stats", k_chunk_cols<DK, false>, p.B * p.H * nsl, 2 * DK, dyn, st, p);
+  else
+    e = p.in_bf16 ? launch("stats", k_chunk_slices<DK, true>, p.B * p.H * nsl, 2 * DK, dyn, st, p)
+                  : launch("stats", k_chunk_slices<DK, false>, p.B * p.H * nsl, 2 * DK, dyn, st, p);
   if (e != hipSuccess) return e;
   const int units = p.scope == 0 ? p.B : p.B * p.H;
   const int N = p.scope == 0 ? p.H * DK : DK;

@@ -1640,14 +1640,23 @@ static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
     e = p.in_bf16 ? launch("stats", k_chunk_slices<DK, true>, p.B * p.H * nsl, 2 * DK, dyn, st, p)
                   : launch("stats", k_chunk_slices<DK, false>, p.B * p.H * nsl, 2 * DK, dyn, st, p);
   if (e != hipSuccess) return e;
+  return launch_chunk_writeback(p, nsl, st);
+}
+
+hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st) {
+  const int DK = p.dk;
   const int units = p.scope == 0 ? p.B : p.B * p.H;
   const int N = p.scope == 0 ? p.H * DK : DK;
-  e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl, (const float*)p.ws_rpart,
-             (const double*)p.ws_gam, p.ws_bits);
+  hipError_t e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl,
+                        (const float*)p.ws_rpart, (const double*)p.ws_gam, p.ws_bits);
   if (e != hipSuccess) return e;
-  if (DK > 128 || p.bmax <= 8)
-    return launch("requant", k_requant<DK, DK, false, true>, p.B * p.H, 2 * DK, 0, st, p);
-  return launch("requant", k_requant<DK, DK, false, (DK > 128)>, p.B * p.H, 2 * DK, 0, st, p);
+  const bool c8 = DK > 128 || p.bmax <= 8;
+  if (DK == 64)
+    return c8 ? launch("requant", k_requant<64, 64, false, true>, p.B * p.H, 128, 0, st, p)
+              : launch("requant", k_requant<64, 64, false, false>, p.B * p.H, 128, 0, st, p);
+  if (DK == 256) return launch("requant", k_requant<256, 256, false, true>, p.B * p.H, 512, 0, st, p);
+  return c8 ? launch("requant", k_requant<128, 128, false, true>, p.B * p.H, 256, 0, st, p)
+            : launch("requant", k_requant<128, 128, false, false>, p.B * p.H, 256, 0, st, p);
 }
 
 hipError_t launch_prefill(KParams p, int C, hipStream_t st) {

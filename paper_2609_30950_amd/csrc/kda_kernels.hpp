@@ -41,6 +41,10 @@ hipError_t launch_step(const KParams& p, hipStream_t st);
 hipError_t launch_step_outputs(const KParams& p, hipStream_t st);
 hipError_t launch_step_writeback(const KParams& p, hipStream_t st);
 hipError_t launch_prefill(KParams p, int C, hipStream_t st);
+// Allocation and requantisation of one prefill write-back from the float32
+// state, per-slice row maxima (nsl per row), Gamma and rate codes in the
+// workspace.
+hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st);
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st);
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,

@@ -85,6 +85,14 @@ typedef struct {
   int32_t no_erase;       /* 1: no erasure, a_t = 0 in eq. rule (Mamba-2):
                              S = D S + beta k v^T and no erase term in the
                              rate statistics and weights; 0: KDA/GDN erase */
+  int32_t chunked;        /* kda_prefill only.  0: token-sequential float32
+                             recurrence (bit-reproducible contract); 1: each
+                             write-back interval in the chunked (WY/UT) form
+                             of eq. rule on bf16 MFMA with float32
+                             accumulation: the same state and outputs up to
+                             bf16 operand rounding, with C <= 64 and
+                             d_k <= 128.  The write-back quantiser is the
+                             same in both modes.                              */
 } kda_config;
 
 /* Bytes of one (sequence, head) record slot; 0 if the config is invalid.
@@ -193,7 +201,10 @@ int kda_step_outputs(const kda_config* cfg, void* records, const float* q,
 int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* stream);
 
 /* Prefill of T tokens with a write-back after every C-th token and after the
- * last one (Sec. 2: once per prefill chunk).
+ * last one (Sec. 2: once per prefill chunk).  With cfg->chunked, C must be
+ * at most 64 (KDA_ERR_ARG otherwise) and the workspace (kda_workspace_bytes
+ * of the same config) also holds the per-chunk records of up to 16 chunks
+ * per head (about 93 KB per chunk and head at d_k = 128).
  * In:  q, k [B][T][H][d_k] bf16 (raw 16-bit patterns); v [B][T][H][d_v] bf16;
  *      s [B][T][H][d_k] f32 (or [B][T][H]); beta [B][T][H] f32; gamma as in
  *      kda_step.  In/out: records.  Out: o [B][T][H][d_v] f32. */

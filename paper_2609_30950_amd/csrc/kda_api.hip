@@ -15,7 +15,7 @@ namespace {
 using kda::KParams;
 
 struct WsLayout {
-  size_t c_off, zr_off, bits_off, s32_off, rpart_off, gam_off, hv_off, total;
+  size_t c_off, zr_off, bits_off, s32_off, rpart_off, gam_off, hv_off, chunk_off, total;
 };
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
@@ -32,7 +32,12 @@ WsLayout ws_layout(const kda_config* cfg) {
   w.gam_off = up256(w.rpart_off + rows * (size_t)(cfg->d_v / 64) * sizeof(float));
   // decode: the token's vectors w (d_v), a and g (d_k) per head
   w.hv_off = up256(w.gam_off + rows * sizeof(double));
-  w.total = up256(w.hv_off + (size_t)cfg->B * cfg->H * (cfg->d_v + 2 * cfg->d_k) * sizeof(float));
+  w.chunk_off = up256(w.hv_off + (size_t)cfg->B * cfg->H * (cfg->d_v + 2 * cfg->d_k) * sizeof(float));
+  // chunked prefill: the records of one group of chunks
+  const int nbh = cfg->B * cfg->H;
+  const size_t chunk =
+      cfg->chunked ? (size_t)kda::chunk_group(nbh) * nbh * kda::chunk_record_bytes(cfg->d_k) : 0;
+  w.total = up256(w.chunk_off + chunk);
   return w;
 }
 
@@ -45,6 +50,8 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg->decay_per_head != 0 && cfg->decay_per_head != 1) return KDA_ERR_ARG;
   if (cfg->state32 != 0 && cfg->state32 != 1) return KDA_ERR_ARG;
   if (cfg->no_erase != 0 && cfg->no_erase != 1) return KDA_ERR_ARG;
+  if (cfg->chunked != 0 && cfg->chunked != 1) return KDA_ERR_ARG;
+  if (cfg->chunked && (cfg->d_k > 128 || cfg->state32)) return KDA_ERR_UNSUPPORTED;
   if (cfg->state32) {
     if (need) *need = 0;
     return KDA_OK;
@@ -108,6 +115,7 @@ void set_ws(KParams& p, const kda_config* cfg, void* ws) {
   p.ws_rpart = (float*)(base + w.rpart_off);
   p.ws_gam = (double*)(base + w.gam_off);
   p.ws_hv = (float*)(base + w.hv_off);
+  p.ws_chunk = cfg->chunked ? base + w.chunk_off : nullptr;
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KDA_OK : KDA_ERR_HIP; }
@@ -280,6 +288,10 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, cons
   p.T = T;
   p.in_bf16 = 1;
   if (!cfg->state32) set_ws(p, cfg, ws);
+  if (cfg->chunked) {
+    if (C > 64) return KDA_ERR_ARG;
+    return hip_status(kda::launch_prefill_chunked(p, C, (hipStream_t)stream));
+  }
   return hip_status(kda::launch_prefill(p, C, (hipStream_t)stream));
 }
 

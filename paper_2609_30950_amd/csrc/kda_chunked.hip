@@ -1,0 +1,598 @@
+// Chunked prefill on MFMA: the gated delta rule (eq. rule, Sec. 2) over one
+// write-back interval in its WY/UT form.
+//
+// Within a chunk of n <= 64 tokens starting from the dequantised state S0
+// (d_k x d_v), with c_j = sum_{tau<=j} s_tau per row (cumulative decay) and
+// gamma_j = exp(-c_j), the recurrence S_j = (I - beta_j k_j k_j^T) D_j
+// S_{j-1} + beta_j k_j v_j^T unrolls to (derivation in the commit that
+// introduced this file and in the design notes):
+//
+//   L[j][tau] = sum_i k_ji k_taui exp(c_taui - c_ji)      (tau < j)
+//   A[j][tau] = sum_i q_ji k_taui exp(c_taui - c_ji)      (tau <= j)
+//   T         = (I + diag(beta) L)^-1                      (unit lower triangular)
+//   U         = T diag(beta) (V - Khat S0),  Khat_j = k_j * gamma_j
+//   O         = Qhat S0 + A U,               Qhat_j = q_j * gamma_j
+//   S_n       = gamma_{n-1} * S0 + Ktil^T U, Ktil_tau = k_tau * exp(c_tau - c_{n-1})
+//
+// Without erasure L = 0 and U = diag(beta) V.  Everything but the three
+// products with S0 depends on the chunk's inputs only, so it is formed for
+// many chunks at once (k_chunk_prep, one block per chunk and head, spread
+// over the whole GPU) and stored in a per-chunk record; the write-back loop
+// then runs k_chunk_apply (W = Wk S0, U = Uv - W, O, S_n; bf16 MFMA with
+// float32 accumulation) followed by the allocation and requantisation
+// kernels of the token-sequential path.
+//
+// The pairwise decay factors are split as exp(c_tau - c_r) exp(c_r - c_j)
+// around the last token r of the previous 16-token block, which keeps every
+// factor of an off-diagonal block at most 1; a diagonal block whose decay
+// span within the block stays below 80 uses the same split (factors within
+// [e^-80, e^80], finite in bf16 and float32), otherwise it is formed on the
+// vector ALUs with one exponential per pair and row.
+//
+// EMA statistics over the chunk (Sec. 3, running statistics) are affine in
+// their value at the chunk start: m_n = (1 - alpha)^n m_0 + Q with Q the
+// same recursion started from 0 (a fresh record starts from m_0 = its first
+// sample).  k_chunk_prep forms Q, k_chunk_apply applies it to the record's
+// stored value.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kda_device.hpp"
+#include "kda_kernels.hpp"
+#include "kda_profile.hpp"
+#include "kda_record.hpp"
+
+namespace kda {
+
+namespace {
+
+constexpr int CT = 64;          // tokens of a (padded) chunk
+constexpr int NT = 256;         // threads per block: four waves
+constexpr float SPLIT_SPAN = 80.f;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// float -> bf16 bits, round to nearest even (finite inputs)
+__device__ __forceinline__ uint16_t bf16_rne(float x) {
+  uint32_t u = __builtin_bit_cast(uint32_t, x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_f32(uint16_t h) {
+  return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  return (uint32_t)bf16_rne(a) | ((uint32_t)bf16_rne(b) << 16);
+}
+
+// D += A B for 16x16 tiles, K = 32: lane l supplies row l % 16 of A and
+// column l % 16 of B, each at k = 8 (l / 16) .. 8 (l / 16) + 7 (eight bf16
+// in one 16-byte register quad); it receives D rows 4 (l / 16) + r, r < 4,
+// of column l % 16.
+__device__ __forceinline__ f32x4 mma(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float max16(float m) {
+  // maximum over the 16 lanes of a row group (l / 16 fixed)
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
+  return m;
+}
+
+}  // namespace
+
+// Byte layout of one chunk's record (per chunk and head), 256-byte aligned
+// fields; DV == DK.
+template <int DK>
+struct ChunkWs {
+  static constexpr size_t wk = 0;                         // bf16 [CT][DK]: T diag(beta) Khat
+  static constexpr size_t qh = wk + (size_t)CT * DK * 2;  // bf16 [CT][DK]: Qhat
+  static constexpr size_t ktt = qh + (size_t)CT * DK * 2; // bf16 [DK][CT]: Ktil^T
+  static constexpr size_t am = ktt + (size_t)DK * CT * 2; // bf16 [CT][CT]: A (lower, with diagonal)
+  static constexpr size_t uv = am + (size_t)CT * CT * 2;  // f32 [CT][DK]: T diag(beta) V
+  static constexpr size_t gend = uv + (size_t)CT * DK * 4;// f32 [DK]: gamma_{n-1}
+  static constexpr size_t ema = gend + (size_t)DK * 4;    // f64 [4][DK]: Q_m, Q_e, first samples
+  static constexpr size_t bytes = (ema + (size_t)4 * DK * 8 + 255) / 256 * 256;
+};
+
+template <int DK>
+struct PrepSmem {
+  static constexpr int CS = DK + 4;   // float row stride (16-byte aligned rows)
+  static constexpr int KS = DK + 8;   // bf16 row stride
+  static constexpr int LS = CT + 4;
+  static constexpr int TS = CT + 8;
+  union {
+    float c[CT][CS];                  // cumulative decay exponents
+    double ema[2][16][DK];            // EMA samples of 16 tokens (after c is dead)
+  } u0;
+  union {
+    struct {
+      uint16_t k[CT][KS], q[CT][KS];
+    } kq;
+    uint16_t vt[DK][TS];              // V^T
+  } u1;
+  float L[CT][LS];
+  float A[CT][LS];
+  uint16_t tb[CT][TS];                // T diag(beta)
+  uint16_t kht[DK][TS];               // Khat^T
+  float beta[CT];
+};
+
+template <int DK>
+__global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cws) {
+  using CW = ChunkWs<DK>;
+  using SM = PrepSmem<DK>;
+  __shared__ SM sm;
+  const int nbh = p.B * p.H;
+  const int cg = blockIdx.x / nbh, bh = blockIdx.x % nbh;
+  const int b = bh / p.H, h = bh % p.H;
+  const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
+  const int tok0 = p.tok0 + cg * C;
+  const int n = min(C, p.T - tok0);
+  uint8_t* out = cws + ((size_t)cg * nbh + bh) * CW::bytes;
+  auto th = [&](int j) { return ((size_t)b * p.T + tok0 + j) * p.H + h; };
+
+  // keys and queries (zero past the chunk's end), beta, cumulative decay
+  constexpr int V8 = DK / 8;
+  for (int e = t; e < CT * V8; e += NT) {
+    const int j = e / V8, g = e % V8;
+    uint4 kv = make_uint4(0u, 0u, 0u, 0u), qv = kv;
+    if (j < n) {
+      kv = ((const uint4*)p.k)[th(j) * V8 + g];
+      qv = ((const uint4*)p.q)[th(j) * V8 + g];
+    }
+    *(uint4*)&sm.u1.kq.k[j][8 * g] = kv;
+    *(uint4*)&sm.u1.kq.q[j][8 * g] = qv;
+  }
+  if (t < CT) sm.beta[t] = t < n ? p.beta[th(t)] : 0.f;
+  if (t < DK) {
+    float c = 0.f;
+    for (int j0 = 0; j0 < CT; j0 += 16) {
+      float sv[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int j = j0 + u;
+        sv[u] = j < n ? (p.per_head ? p.s[th(j)] : p.s[th(j) * DK + t]) : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        c += sv[u];
+        sm.u0.c[j0 + u][t] = c;
+      }
+    }
+  }
+  __syncthreads();
+
+  // Qhat (row-major), Khat^T (LDS), Ktil^T and gamma_{n-1}
+  {
+    uint16_t* qh = (uint16_t*)(out + CW::qh);
+    for (int e = t; e < CT * DK; e += NT) {
+      const int j = e / DK, i = e % DK;
+      qh[e] = bf16_rne(bf16_f32(sm.u1.kq.q[j][i]) * __expf(-sm.u0.c[j][i]));
+    }
+    uint16_t* ktt = (uint16_t*)(out + CW::ktt);
+    for (int e = t; e < CT * DK; e += NT) {
+      const int i = e / CT, j = e % CT;
+      const float c = sm.u0.c[j][i], ce = sm.u0.c[CT - 1][i];
+      const float kk = bf16_f32(sm.u1.kq.k[j][i]);
+      sm.kht[i][j] = bf16_rne(kk * __expf(-c));
+      ktt[e] = bf16_rne(kk * __expf(c - ce));
+    }
+    if (t < DK) ((float*)(out + CW::gend))[t] = (float)exp(-(double)sm.u0.c[CT - 1][t]);
+  }
+
+  // L and A, block row J = w (tokens 16J .. 16J + 15): tiles (J, T <= J)
+  const bool erase = !p.no_erase;
+  {
+    const int J = w;
+    const int k8 = 8 * (lane >> 4);
+    const int jr = 16 * J + (lane & 15);
+    bool wide = false;
+    for (int i = lane; i < DK; i += WAVE) {
+      const float cr = J ? sm.u0.c[16 * J - 1][i] : 0.f;
+      wide = wide || (sm.u0.c[16 * J + 15][i] - cr > SPLIT_SPAN);
+    }
+    const bool diag_valu = __ballot(wide) != 0;
+    f32x4 accL[4], accA[4];
+#pragma unroll
+    for (int T = 0; T < 4; ++T) {
+      accL[T] = f32x4{0.f, 0.f, 0.f, 0.f};
+      accA[T] = accL[T];
+    }
+    for (int ks = 0; ks < DK / 32; ++ks) {
+      const int i0 = 32 * ks + k8;
+      float fl[8], cr[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        cr[e] = J ? sm.u0.c[16 * J - 1][i0 + e] : 0.f;
+        fl[e] = __expf(cr[e] - sm.u0.c[jr][i0 + e]);
+      }
+      uint32_t ak[4], aq[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ak[e] = pack2(bf16_f32(sm.u1.kq.k[jr][i0 + 2 * e]) * fl[2 * e],
+                      bf16_f32(sm.u1.kq.k[jr][i0 + 2 * e + 1]) * fl[2 * e + 1]);
+        aq[e] = pack2(bf16_f32(sm.u1.kq.q[jr][i0 + 2 * e]) * fl[2 * e],
+                      bf16_f32(sm.u1.kq.q[jr][i0 + 2 * e + 1]) * fl[2 * e + 1]);
+      }
+      const uint4 AK = make_uint4(ak[0], ak[1], ak[2], ak[3]);
+      const uint4 AQ = make_uint4(aq[0], aq[1], aq[2], aq[3]);
+#pragma unroll
+      for (int T = 0; T < 4; ++T) {
+        if (T > J || (T == J && diag_valu)) continue;
+        const int jt = 16 * T + (lane & 15);
+        float fr[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) fr[e] = __expf(sm.u0.c[jt][i0 + e] - cr[e]);
+        uint32_t bk[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          bk[e] = pack2(bf16_f32(sm.u1.kq.k[jt][i0 + 2 * e]) * fr[2 * e],
+                        bf16_f32(sm.u1.kq.k[jt][i0 + 2 * e + 1]) * fr[2 * e + 1]);
+        const uint4 BK = make_uint4(bk[0], bk[1], bk[2], bk[3]);
+        if (erase) accL[T] = mma(AK, BK, accL[T]);
+        accA[T] = mma(AQ, BK, accA[T]);
+      }
+    }
+#pragma unroll
+    for (int T = 0; T < 4; ++T) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = 16 * J + 4 * (lane >> 4) + r, tau = 16 * T + (lane & 15);
+        if (T > J) {
+          sm.L[j][tau] = 0.f;
+          sm.A[j][tau] = 0.f;
+        } else if (T < J || !diag_valu) {
+          sm.L[j][tau] = tau < j ? accL[T][r] : 0.f;
+          sm.A[j][tau] = tau <= j ? accA[T][r] : 0.f;
+        }
+      }
+    }
+    if (diag_valu) {
+      // one exponential per pair and row: exp(c_tau - c_j) <= 1 for tau <= j
+      for (int pr = lane; pr < 256; pr += WAVE) {
+        const int j = 16 * J + pr / 16, tau = 16 * J + pr % 16;
+        float l = 0.f, a = 0.f;
+        if (tau <= j) {
+          for (int i = 0; i < DK; ++i) {
+            const float kt = bf16_f32(sm.u1.kq.k[tau][i]) * __expf(sm.u0.c[tau][i] - sm.u0.c[j][i]);
+            l = fmaf(bf16_f32(sm.u1.kq.k[j][i]), kt, l);
+            a = fmaf(bf16_f32(sm.u1.kq.q[j][i]), kt, a);
+          }
+        }
+        sm.L[j][tau] = (tau < j && erase) ? l : 0.f;
+        sm.A[j][tau] = tau <= j ? a : 0.f;
+      }
+    }
+  }
+  __syncthreads();
+
+  {
+    uint16_t* am = (uint16_t*)(out + CW::am);
+    for (int e = t; e < CT * CT; e += NT) am[e] = bf16_rne(sm.A[e / CT][e % CT]);
+  }
+  if (w == 0) {
+    // T = (I + diag(beta) L)^-1 by forward substitution, column m per lane;
+    // stored as T diag(beta)
+    const int m = lane;
+    float Tc[CT];
+#pragma unroll
+    for (int j = 0; j < CT; ++j) {
+      float acc = 0.f;
+#pragma unroll
+      for (int tau = 0; tau < j; ++tau) acc = fmaf(sm.L[j][tau], Tc[tau], acc);
+      Tc[j] = j == m ? 1.f : (j > m ? -sm.beta[j] * acc : 0.f);
+    }
+    const float bm = sm.beta[m];
+#pragma unroll
+    for (int j = 0; j < CT; ++j) sm.tb[j][m] = bf16_rne(Tc[j] * bm);
+  } else {
+    // V^T (the keys and queries are no longer needed)
+    for (int e = t - WAVE; e < CT * V8; e += NT - WAVE) {
+      const int j = e / V8, g = e % V8;
+      uint4 vv = make_uint4(0u, 0u, 0u, 0u);
+      if (j < n) vv = ((const uint4*)p.v)[th(j) * V8 + g];
+      const uint32_t x[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        sm.u1.vt[8 * g + 2 * u][j] = (uint16_t)(x[u] & 0xFFFFu);
+        sm.u1.vt[8 * g + 2 * u + 1][j] = (uint16_t)(x[u] >> 16);
+      }
+    }
+  }
+  __syncthreads();
+
+  // Uv = T diag(beta) V and Wk = T diag(beta) Khat: token tile w, all columns
+  {
+    const int J = w;
+    const int k8 = 8 * (lane >> 4);
+    f32x4 au[DK / 16], aw[DK / 16];
+#pragma unroll
+    for (int ct = 0; ct < DK / 16; ++ct) {
+      au[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      aw[ct] = au[ct];
+    }
+#pragma unroll
+    for (int ks = 0; ks < CT / 32; ++ks) {
+      if (32 * ks > 16 * J + 15) break;   // T is lower triangular
+      const uint4 a = *(const uint4*)&sm.tb[16 * J + (lane & 15)][32 * ks + k8];
+#pragma unroll
+      for (int ct = 0; ct < DK / 16; ++ct) {
+        const uint4 bv = *(const uint4*)&sm.u1.vt[16 * ct + (lane & 15)][32 * ks + k8];
+        au[ct] = mma(a, bv, au[ct]);
+        if (erase) {
+          const uint4 bk = *(const uint4*)&sm.kht[16 * ct + (lane & 15)][32 * ks + k8];
+          aw[ct] = mma(a, bk, aw[ct]);
+        }
+      }
+    }
+    float* uv = (float*)(out + CW::uv);
+    uint16_t* wk = (uint16_t*)(out + CW::wk);
+#pragma unroll
+    for (int ct = 0; ct < DK / 16; ++ct) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = 16 * J + 4 * (lane >> 4) + r, i = 16 * ct + (lane & 15);
+        uv[j * DK + i] = au[ct][r];
+        wk[j * DK + i] = bf16_rne(aw[ct][r]);
+      }
+    }
+  }
+
+  // EMA sums from zero over the chunk, in token order (double)
+  {
+    double qm = 0.0, qe = 0.0, z0 = 0.0, y0 = 0.0;
+    for (int j0 = 0; j0 < n; j0 += 16) {
+      __syncthreads();   // c (first batch) or the previous batch is consumed
+      for (int e = t; e < 16 * DK; e += NT) {
+        const int u = e / DK, i = e % DK, j = j0 + u;
+        if (j < n) {
+          const float sv = p.per_head ? p.s[th(j)] : p.s[th(j) * DK + i];
+          sm.u0.ema[0][u][i] = decay_sample(sv);
+          sm.u0.ema[1][u][i] =
+              erase ? erase_sample(in_f32<true>(p.k, th(j) * DK + i), p.beta[th(j)]) : 0.0;
+        }
+      }
+      __syncthreads();
+      if (t < DK) {
+        if (j0 == 0) {
+          z0 = sm.u0.ema[0][0][t];
+          y0 = sm.u0.ema[1][0][t];
+        }
+        const int nb = min(16, n - j0);
+        for (int u = 0; u < nb; ++u) {
+          qm = p.one_minus_alpha * qm + p.alpha * sm.u0.ema[0][u][t];
+          qe = p.one_minus_alpha * qe + p.alpha * sm.u0.ema[1][u][t];
+        }
+      }
+    }
+    if (t < DK) {
+      double* ema = (double*)(out + CW::ema);
+      ema[t] = qm;
+      ema[DK + t] = qe;
+      ema[2 * DK + t] = z0;
+      ema[3 * DK + t] = y0;
+    }
+  }
+}
+
+template <int DK>
+struct ApplySmem {
+  static constexpr int SS = DK + 8;
+  static constexpr int US = CT + 8;
+  uint16_t s0t[SLICE][SS];   // S0 of the slice, transposed, bf16
+  uint16_t ut[SLICE][US];    // U of the slice, transposed, bf16
+};
+
+// One write-back interval of one 64-column slice of one head: tokens
+// [p.tok0, p.tok0 + p.ntk) from the record's state; writes the outputs, the
+// float32 state, its per-slice row maxima and (slice 0) Gamma and the rate
+// codes, as the token-sequential stats kernel does.
+template <int DK>
+__global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw) {
+  using CW = ChunkWs<DK>;
+  constexpr int RT = DK / 64;            // 16-row state tiles per wave
+  const int nsl = p.dv / SLICE;
+  const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
+  const int b = bh / p.H, h = bh % p.H;
+  const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
+  const int n = p.ntk;
+  const int k8 = 8 * (lane >> 4), l16 = lane & 15;
+  const uint8_t* in = cw + (size_t)bh * CW::bytes;
+  const Layout L = p.L;
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ ApplySmem<DK> sm;
+  extern __shared__ uint4 dyn_lds[];
+  uint32_t* words = (uint32_t*)dyn_lds;
+  {
+    // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
+    const uint4* src = (const uint4*)(rec + L.codes_off);
+    constexpr int Q = SLICE / 4;
+    const int n4 = L.wc * Q;
+    for (int e = t; e < n4; e += NT) ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
+  }
+  load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
+
+  // S0 at this lane's state-tile positions: float32 gamma_{n-1} * S0 as the
+  // accumulator of S_n, bf16 S0^T in LDS for the products with S0
+  const float* gend = (const float*)(in + CW::gend);
+  f32x4 acc[RT][4];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * (RT * w + rt) + 4 * (lane >> 4) + r;
+      const uint4 d = meta.desc[i];
+      const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
+      const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
+      const float ge = gend[i];
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        const int c = 16 * ct + l16;
+        const uint32_t lo = words[d.x + c], hi = words[d.x + SLICE + c];
+        const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
+        const float x = ((float)code + add) * mul;
+        acc[rt][ct][r] = ge * x;
+        sm.s0t[c][i] = bf16_rne(x);
+      }
+    }
+  }
+  __syncthreads();
+
+  // W = Wk S0 and O = Qhat S0 for token tile w
+  const uint16_t* wk = (const uint16_t*)(in + CW::wk);
+  const uint16_t* qh = (const uint16_t*)(in + CW::qh);
+  const int jrow = 16 * w + l16;
+  f32x4 aw[4], ao[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    aw[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    ao[ct] = aw[ct];
+  }
+  const bool erase = !p.no_erase;
+#pragma unroll
+  for (int ks = 0; ks < DK / 32; ++ks) {
+    const uint4 a1 = *(const uint4*)&wk[jrow * DK + 32 * ks + k8];
+    const uint4 a2 = *(const uint4*)&qh[jrow * DK + 32 * ks + k8];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const uint4 bs = *(const uint4*)&sm.s0t[16 * ct + l16][32 * ks + k8];
+      if (erase) aw[ct] = mma(a1, bs, aw[ct]);
+      ao[ct] = mma(a2, bs, ao[ct]);
+    }
+  }
+  // U = Uv - W, transposed into LDS as bf16
+  const float* uv = (const float*)(in + CW::uv);
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = 16 * w + 4 * (lane >> 4) + r, c = 16 * ct + l16;
+      sm.ut[c][j] = bf16_rne(uv[j * DK + SLICE * sl + c] - aw[ct][r]);
+    }
+  }
+  __syncthreads();
+
+  // O += A U (A is lower triangular: k-steps up to the tile's last token)
+  const uint16_t* am = (const uint16_t*)(in + CW::am);
+#pragma unroll
+  for (int ks = 0; ks < CT / 32; ++ks) {
+    if (32 * ks > 16 * w + 15) break;
+    const uint4 a = *(const uint4*)&am[jrow * CT + 32 * ks + k8];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const uint4 bu = *(const uint4*)&sm.ut[16 * ct + l16][32 * ks + k8];
+      ao[ct] = mma(a, bu, ao[ct]);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int j = 16 * w + 4 * (lane >> 4) + r;
+    if (j < n) {
+      float* orow = p.o + (((size_t)b * p.T + p.tok0 + j) * p.H + h) * p.dv + SLICE * sl;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) orow[16 * ct + l16] = ao[ct][r];
+    }
+  }
+
+  // S_n += Ktil^T U
+  const uint16_t* ktt = (const uint16_t*)(in + CW::ktt);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int irow = 16 * (RT * w + rt) + l16;
+#pragma unroll
+    for (int ks = 0; ks < CT / 32; ++ks) {
+      const uint4 a = *(const uint4*)&ktt[irow * CT + 32 * ks + k8];
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        const uint4 bu = *(const uint4*)&sm.ut[16 * ct + l16][32 * ks + k8];
+        acc[rt][ct] = mma(a, bu, acc[rt][ct]);
+      }
+    }
+  }
+  // float32 state and per-slice row maxima
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * (RT * w + rt) + 4 * (lane >> 4) + r;
+      float* srow = p.ws_s32 + ((size_t)bh * DK + i) * p.dv + SLICE * sl;
+      float m = 0.f;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        const float x = acc[rt][ct][r];
+        srow[16 * ct + l16] = x;
+        m = fmaxf(m, fabsf(x));
+      }
+      m = max16(m);
+      if (l16 == 0) p.ws_rpart[((size_t)bh * DK + i) * nsl + sl] = m;
+    }
+  }
+  if (sl == 0 && t < DK) {
+    // EMA rates after the chunk: m = (1 - alpha)^n m_0 + Q
+    const double* ema = (const double*)(in + CW::ema);
+    double m0, e0;
+    if (meta.ntok == 0) {
+      m0 = ema[2 * DK + t];
+      e0 = ema[3 * DK + t];
+    } else {
+      m0 = exp(-2.0 * logq_decode(meta.z[t]));
+      e0 = 2.0 * (double)f16_to_f32(meta.r16[t]);
+    }
+    double P = 1.0;
+    for (int j = 0; j < n; ++j) P *= p.one_minus_alpha;
+    const double m_run = P * m0 + ema[t];
+    const double e_run = P * e0 + ema[DK + t];
+    const double s_hat = -0.5 * log(m_run);
+    const double r = 0.5 * e_run;
+    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
+  }
+}
+
+size_t chunk_record_bytes(int dk) {
+  return dk == 64 ? ChunkWs<64>::bytes : ChunkWs<128>::bytes;
+}
+
+int chunk_group(int nbh) {
+  const int g = 4096 / nbh;
+  return g < 1 ? 1 : (g > 16 ? 16 : g);
+}
+
+template <int DK>
+static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
+  const int nbh = p.B * p.H, nsl = p.dv / SLICE;
+  const int nch = (p.T + C - 1) / C;
+  const int gc = chunk_group(nbh);
+  const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
+  for (int g0 = 0; g0 < nch; g0 += gc) {
+    const int ng = nch - g0 < gc ? nch - g0 : gc;
+    p.tok0 = g0 * C;
+    hipError_t e = launch("prep", k_chunk_prep<DK>, nbh * ng, NT, 0, st, p, C, p.ws_chunk);
+    if (e != hipSuccess) return e;
+    for (int c = 0; c < ng; ++c) {
+      p.tok0 = (g0 + c) * C;
+      p.ntk = (p.T - p.tok0) < C ? (p.T - p.tok0) : C;
+      e = launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p,
+                 (const uint8_t*)(p.ws_chunk + (size_t)c * nbh * ChunkWs<DK>::bytes));
+      if (e != hipSuccess) return e;
+      e = launch_chunk_writeback(p, nsl, st);
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st) {
+  if (p.dk == 64) return run_chunked<64>(p, C, st);
+  return run_chunked<128>(p, C, st);
+}
+
+}  // namespace kda

@@ -25,76 +25,11 @@
 #include "kda_device.hpp"
 #include "kda_kernels.hpp"
 #include "kda_profile.hpp"
+#include "kda_record.hpp"
 
 namespace kda {
 
 // ------------------------------------------------------------ helpers ---
-
-__device__ __forceinline__ const uint8_t* slot_ptr(const void* recs, long long slot, int bh) {
-  return (const uint8_t*)recs + slot * (long long)bh;
-}
-
-template <int DK>
-struct MetaSmem {
-  // per-row decode descriptor, read by whole waves as one broadcast:
-  // {first word index * d_v, bit shift | width << 8, mul, add} (see unpack_cols)
-  uint4 desc[DK];
-  uint8_t w[DK];      // widths of the stored record
-  int P[DK + 1];      // prefix sums of widths (row bit offsets)
-  float sc[DK];       // stored scales (FP16 -> float)
-  uint16_t z[DK];     // stored rate codes
-  uint16_t r16[DK];   // stored erase rates
-  unsigned ntok;
-};
-
-// Load widths/scales/stat codes of a record and form the row offsets.
-// Widths above b_max (never written by this library) are clamped so that a
-// damaged record cannot address code words outside its slot.
-template <int DK, int DV>
-__device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
-  const int tid = threadIdx.x;
-  if (tid < DK / 2) {
-    const uint8_t byte = rec[L.w_off + tid];
-    m.w[2 * tid] = (uint8_t)min((byte & 15) + 1, bmax);
-    m.w[2 * tid + 1] = (uint8_t)min((byte >> 4) + 1, bmax);
-  }
-  if (tid < DK) {
-    m.sc[tid] = f16_to_f32(((const uint16_t*)(rec + L.sc_off))[tid]);
-    m.z[tid] = ((const uint16_t*)(rec + L.z_off))[tid];
-    m.r16[tid] = ((const uint16_t*)(rec + L.r_off))[tid];
-  }
-  if (tid == 0) m.ntok = *(const unsigned*)rec;
-  __syncthreads();
-  if (tid < WAVE) {
-    constexpr int PER = (DK + WAVE - 1) / WAVE;
-    int loc[PER], sum = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int i = tid * PER + q;
-      loc[q] = i < DK ? m.w[i] : 0;
-      sum += loc[q];
-    }
-    const int incl = wave_incl_scan(sum);
-    int run = incl - sum;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int i = tid * PER + q;
-      if (i < DK) {
-        m.P[i] = run;
-        // x^ = (code + add) mul: (Delta, 0) for b >= 2, (2 mu, 1/2) for one bit
-        const int b = loc[q];
-        const float sc = m.sc[i];
-        const float mul = b == 1 ? 2.0f * sc : sc;
-        const float add = b == 1 ? 0.5f : 0.0f;
-        m.desc[i] = make_uint4((uint32_t)((run >> 5) * DV), (uint32_t)((run & 31) | (b << 8)),
-                               __builtin_bit_cast(uint32_t, mul), __builtin_bit_cast(uint32_t, add));
-      }
-      run += loc[q];
-    }
-    if (tid == WAVE - 1) m.P[DK] = incl;
-  }
-  __syncthreads();
-}
 
 // Per-row scalars of one token for the recurrence.
 template <int DK>
@@ -102,12 +37,6 @@ struct RowSmem {
   float2 ak[DK];   // {fl32(exp(-s)), k}: first pass of the recurrence
   float2 gq[DK];   // {fl32(beta * k), q}: second pass
 };
-
-template <bool BF16>
-__device__ __forceinline__ float in_f32(const void* base, size_t idx) {
-  if constexpr (BF16) return __builtin_bit_cast(float, (uint32_t)((const uint16_t*)base)[idx] << 16);
-  return ((const float*)base)[idx];
-}
 
 // Inputs of row t for the rate statistics: decay rate, key, beta.
 struct RowIn {
@@ -1159,8 +1088,6 @@ __global__ void __launch_bounds__(DK * (DK / 32)) k_exact_gamma(int W, int H, in
 // parity) and combines the outputs of the staged tokens together.  Slice 0
 // also carries the EMA statistics.  Row maxima leave per slice;
 // k_alloc_slices combines them into the weights and allocates.
-
-constexpr int SLICE = 64;
 
 template <int DK>
 constexpr int pf_tokens() { return DK > 128 ? 8 : 16; }

@@ -34,6 +34,7 @@ struct KParams {
   float* ws_rpart;          // prefill: row maxima per 64-column slice, [B][H][dk][dv/64]
   double* ws_gam;           // prefill: row weights Gamma, [B][H][dk]
   float* ws_hv;             // decode: token vectors per head {w[dv], a[dk], g[dk]}
+  uint8_t* ws_chunk;        // chunked prefill: per-chunk records of a group of chunks
   unsigned long long* diag_fit;  // profiling: candidate evaluations (or null)
 };
 
@@ -45,6 +46,12 @@ hipError_t launch_prefill(KParams p, int C, hipStream_t st);
 // state, per-slice row maxima (nsl per row), Gamma and rate codes in the
 // workspace.
 hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st);
+// Chunked prefill (WY/UT form on MFMA), d_k = d_v in {64, 128}, C <= 64.
+hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st);
+// Bytes of one chunk record (per chunk and head) and chunks per group for
+// B*H heads.
+size_t chunk_record_bytes(int dk);
+int chunk_group(int nbh);
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st);
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,

@@ -42,17 +42,10 @@ SEG_COLS = 64
 FINAL_OPS_PER_ELEMENT = 6
 
 
-KERNEL_SOURCES = ("kda_alloc.hpp", "kda_device.hpp", "kda_kernels.hip", "kda_kernels.hpp")
-
-
 def kernel_source_hash():
     """Hash of the device-kernel sources (what the counter summaries describe)."""
-    import hashlib
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_30950_amd", "csrc")
-    for f in KERNEL_SOURCES:
-            h.update(open(os.path.join(csrc, f), "rb").read())
-    return h.hexdigest()[:16]
+    from paper_2609_30950_amd.pmc_summary import source_hash
+    return source_hash()
 
 
 def committed_traffic(kernel, workload):
@@ -133,12 +126,33 @@ def run_state32_reference(w, args, K, torch):
                 hbm_frac=step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, bytes_per_step=step_bytes)
 
 
+# Chunked prefill: one chunk record per chunk and head (bytes at d_k = d_v =
+# 128: Wk, Qhat, Ktil^T bf16 [64][128], A bf16 [64][64], Uv f32 [64][128],
+# gamma f32 [128], EMA sums f64 [4][128]).
+CHUNK_RECORD_BYTES = 3 * 64 * 128 * 2 + 64 * 64 * 2 + 64 * 128 * 4 + 128 * 4 + 4 * 128 * 8
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def chunk_mfma_flops(dk):
+    """bf16 MFMA flops issued per chunk and head (16x16x32 tiles, 16384 flops
+    each): prep forms L and A on the ten tiles of the lower 16-token blocks
+    (d_k / 32 steps each) and T diag(beta) [V | Khat] on six tile rows x
+    2 d_k / 16 columns; apply forms Wk S0 and Qhat S0 (4 x d_v/16 tiles,
+    d_k / 32 steps), A U (six tile rows) and Ktil^T U (d_k/16 x d_v/16 tiles,
+    two steps)."""
+    t = 16 * 16 * 32 * 2
+    prep = 10 * 2 * (dk // 32) * t + 6 * (2 * dk // 16) * t
+    apply_ = (2 * 4 * (dk // 16) * (dk // 32) + 6 * (dk // 16) + (dk // 16) * (dk // 16) * 2) * t
+    return prep, apply_
+
+
 def run_prefill(args, K, torch):
     """Prefill of the bf16 workload (B=4 H=32 d=128 T=8192, write-back every
-    64 tokens) from the empty state: one kda_prefill call per pass."""
+    64 tokens) from the empty state: one kda_prefill call per pass; with
+    --chunked, in the chunked (WY/UT, bf16 MFMA) form."""
     w = W.WORKLOADS["prefill"]
     cfg = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
-                   b_min=w.b_min, b_max=w.b_max)
+                   b_min=w.b_min, b_max=w.b_max, chunked=int(args.chunked))
     t0 = time.time()
     xs = W.tokens(w, 0, w.T)
     print(f"# prefill inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
@@ -190,14 +204,37 @@ def run_prefill(args, K, torch):
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": f"prefill B={w.B} H={w.H} d_k=d_v={w.dk} T={w.T} C={w.C}, bf16 "
                                f"q/k/v, mean {w.mean_bits} bits, widths [{w.b_min},{w.b_max}], "
-                               f"groups of {w.G} rows, layer budget, from the empty state"},
+                               f"groups of {w.G} rows, layer budget, from the empty state"
+                               + (", chunked (WY/UT) form on bf16 MFMA" if args.chunked else
+                                  ", token-sequential float32 recurrence")},
         "hbm_GBps_step": total / (ms * 1e-3) / 1e9,
         "hbm_frac_step": total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": total,
         "kernels": kern,
         "kernel_source_hash": kernel_source_hash(),
     }
-    if t_stats:
+    if args.chunked and "apply" in prof:
+        # apply moves per head: its chunk record, the record's code words at
+        # the budgeted payload and metadata, the outputs and the float32 state
+        nch = -(-w.T // w.C)
+        per_head = (CHUNK_RECORD_BYTES + w.mean_bits * w.dk * w.dv / 8 + meta
+                    + w.C * w.dv * 4 + w.dk * w.dv * 4)
+        t_apply = prof["apply"][0] / prof["apply"][1] * 1e-3
+        ach = nbh * per_head / t_apply / 1e9
+        out["roofline"] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBPS, unit="GB/s",
+                               frac=ach / HBM_PEAK_GBPS, traffic=committed_traffic("apply", "prefill_chunked"),
+                               kernel="apply", bytes_per_launch=nbh * per_head)
+        fp, fa = chunk_mfma_flops(w.dk)
+        t_prep = prof["prep"][0] / prof["prep"][1] * 1e-3
+        chunks_per_prep = nbh * nch / prof["prep"][1]
+        out["mfma"] = {
+            "prep": dict(tflops=fp * chunks_per_prep / t_prep / 1e12,
+                         frac=fp * chunks_per_prep / t_prep / 1e12 / MFMA_BF16_PEAK_TFLOPS),
+            "apply": dict(tflops=fa * nbh / t_apply / 1e12,
+                          frac=fa * nbh / t_apply / 1e12 / MFMA_BF16_PEAK_TFLOPS),
+            "peak_tflops": MFMA_BF16_PEAK_TFLOPS}
+        out["metric"] = out["metric"].replace("prefill", "chunked prefill")
+    elif t_stats:
         ach = rec_ops / t_stats / 1e12
         out["roofline"] = dict(bound="alu", achieved=ach, peak=VALU_PEAK_TOPS, unit="TOP/s",
                                frac=ach / VALU_PEAK_TOPS, traffic=committed_traffic("stats", "prefill"),
@@ -292,6 +329,8 @@ def main():
                     help="skip the untimed counting replay (e.g. under a profiler)")
     ap.add_argument("--no-ref32", action="store_true",
                     help="skip the 32-bit-mode reference step")
+    ap.add_argument("--chunked", action="store_true",
+                    help="prefill workload: chunked (WY/UT) form on bf16 MFMA")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "

@@ -3,9 +3,12 @@
 //
 // Within a chunk of n <= 64 tokens starting from the dequantised state S0
 // (d_k x d_v), with c_j = sum_{tau<=j} s_tau per row (cumulative decay) and
-// gamma_j = exp(-c_j), the recurrence S_j = (I - beta_j k_j k_j^T) D_j
-// S_{j-1} + beta_j k_j v_j^T unrolls to (derivation in the commit that
-// introduced this file and in the design notes):
+// gamma_j = exp(-c_j), the substitution S_j = diag(gamma_j) Z_j turns the
+// recurrence S_j = (I - beta_j k_j k_j^T) D_j S_{j-1} + beta_j k_j v_j^T
+// into Z_j = Z_{j-1} + (k_j / gamma_j) u_j^T with
+// u_j = beta_j (v_j - Z_{j-1}^T (gamma_j k_j)); collecting the u_j as rows of
+// U gives a unit lower-triangular system, and the outputs and the state at
+// the chunk's end follow:
 //
 //   L[j][tau] = sum_i k_ji k_taui exp(c_taui - c_ji)      (tau < j)
 //   A[j][tau] = sum_i q_ji k_taui exp(c_taui - c_ji)      (tau <= j)
@@ -32,8 +35,10 @@
 // EMA statistics over the chunk (Sec. 3, running statistics) are affine in
 // their value at the chunk start: m_n = (1 - alpha)^n m_0 + Q with Q the
 // same recursion started from 0 (a fresh record starts from m_0 = its first
-// sample).  k_chunk_prep forms Q, k_chunk_apply applies it to the record's
-// stored value.
+// sample).  k_chunk_prep forms Q over token segments (each in token order,
+// combined in order with the powers of 1 - alpha), k_chunk_apply applies it
+// to the record's stored value.  The results differ from the token-order
+// recursion by rounding in the last bits of a double.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -48,7 +53,8 @@ namespace kda {
 namespace {
 
 constexpr int CT = 64;          // tokens of a (padded) chunk
-constexpr int NT = 256;         // threads per block: four waves
+constexpr int NT = 256;         // threads per apply block: four waves
+constexpr int NTP = 512;        // threads per prep block: eight waves
 constexpr float SPLIT_SPAN = 80.f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -107,27 +113,34 @@ struct PrepSmem {
   static constexpr int KS = DK + 8;   // bf16 row stride
   static constexpr int LS = CT + 4;
   static constexpr int TS = CT + 8;
+  static constexpr int SEGS = NTP / DK;  // token segments of the decay scan
   union {
     float c[CT][CS];                  // cumulative decay exponents
-    double ema[2][16][DK];            // EMA samples of 16 tokens (after c is dead)
-  } u0;
-  union {
     struct {
-      uint16_t k[CT][KS], q[CT][KS];
-    } kq;
-    uint16_t vt[DK][TS];              // V^T
-  } u1;
-  float L[CT][LS];
-  float A[CT][LS];
-  uint16_t tb[CT][TS];                // T diag(beta)
+      float T[CT][LS];                // (I + diag(beta) L)^-1
+      float X[4][16][20];             // per-wave 16x16 products
+    } t;
+  } u0;
+  uint16_t k[CT][KS], q[CT][KS];      // keys and queries
+  uint16_t vt[DK][TS];                // V^T
   uint16_t kht[DK][TS];               // Khat^T
+  union {
+    float L[CT][LS];                  // strictly lower L
+    struct {
+      float csum[SEGS][DK];           // decay sums of the segments
+      double em[SEGS][2][DK];         // EMA sums of the segments (from zero)
+      double first[2][DK];            // first samples of the chunk
+    } seg;
+  } u1;
+  uint16_t tb[CT][TS];                // T diag(beta), bf16
   float beta[CT];
 };
 
 template <int DK>
-__global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cws) {
+__global__ void __launch_bounds__(NTP) k_chunk_prep(KParams p, int C, uint8_t* cws) {
   using CW = ChunkWs<DK>;
   using SM = PrepSmem<DK>;
+  constexpr int SEGS = SM::SEGS, SEGL = CT / SEGS;
   __shared__ SM sm;
   const int nbh = p.B * p.H;
   const int cg = blockIdx.x / nbh, bh = blockIdx.x % nbh;
@@ -137,34 +150,90 @@ __global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cw
   const int n = min(C, p.T - tok0);
   uint8_t* out = cws + ((size_t)cg * nbh + bh) * CW::bytes;
   auto th = [&](int j) { return ((size_t)b * p.T + tok0 + j) * p.H + h; };
+  const bool erase = !p.no_erase;
 
-  // keys and queries (zero past the chunk's end), beta, cumulative decay
+  // inputs: keys, queries and V^T (zero past the chunk's end), beta, and the
+  // decay rates of this thread's row and token segment in registers
   constexpr int V8 = DK / 8;
-  for (int e = t; e < CT * V8; e += NT) {
+  const int ri = t % DK, sg = t / DK;
+  float sv[SEGL];
+#pragma unroll
+  for (int u = 0; u < SEGL; ++u) {
+    const int j = sg * SEGL + u;
+    sv[u] = j < n ? (p.per_head ? p.s[th(j)] : p.s[th(j) * DK + ri]) : 0.f;
+  }
+  for (int e = t; e < CT * V8; e += NTP) {
     const int j = e / V8, g = e % V8;
     uint4 kv = make_uint4(0u, 0u, 0u, 0u), qv = kv;
     if (j < n) {
       kv = ((const uint4*)p.k)[th(j) * V8 + g];
       qv = ((const uint4*)p.q)[th(j) * V8 + g];
     }
-    *(uint4*)&sm.u1.kq.k[j][8 * g] = kv;
-    *(uint4*)&sm.u1.kq.q[j][8 * g] = qv;
+    *(uint4*)&sm.k[j][8 * g] = kv;
+    *(uint4*)&sm.q[j][8 * g] = qv;
+  }
+  for (int e = t; e < CT * V8; e += NTP) {
+    const int j = e % CT, g = e / CT;   // consecutive lanes: consecutive tokens
+    uint4 vv = make_uint4(0u, 0u, 0u, 0u);
+    if (j < n) vv = ((const uint4*)p.v)[th(j) * V8 + g];
+    const uint32_t x[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      sm.vt[8 * g + 2 * u][j] = (uint16_t)(x[u] & 0xFFFFu);
+      sm.vt[8 * g + 2 * u + 1][j] = (uint16_t)(x[u] >> 16);
+    }
   }
   if (t < CT) sm.beta[t] = t < n ? p.beta[th(t)] : 0.f;
-  if (t < DK) {
-    float c = 0.f;
-    for (int j0 = 0; j0 < CT; j0 += 16) {
-      float sv[16];
+  __syncthreads();
+
+  // decay scan and EMA sums over this thread's segment (token order, double)
+  {
+    float cs = 0.f;
+    double qm = 0.0, qe = 0.0;
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int j = j0 + u;
-        sv[u] = j < n ? (p.per_head ? p.s[th(j)] : p.s[th(j) * DK + t]) : 0.f;
+    for (int u = 0; u < SEGL; ++u) {
+      const int j = sg * SEGL + u;
+      cs += sv[u];
+      sm.u0.c[j][ri] = cs;
+      if (j < n) {
+        const double z = decay_sample(sv[u]);
+        const double y = erase ? erase_sample(bf16_f32(sm.k[j][ri]), sm.beta[j]) : 0.0;
+        if (j == 0) {
+          sm.u1.seg.first[0][ri] = z;
+          sm.u1.seg.first[1][ri] = y;
+        }
+        qm = p.one_minus_alpha * qm + p.alpha * z;
+        qe = p.one_minus_alpha * qe + p.alpha * y;
       }
+    }
+    sm.u1.seg.csum[sg][ri] = cs;
+    sm.u1.seg.em[sg][0][ri] = qm;
+    sm.u1.seg.em[sg][1][ri] = qe;
+  }
+  __syncthreads();
+  {
+    // later segments start from the sum of the earlier ones
+    float off = 0.f;
+    for (int s2 = 0; s2 < sg; ++s2) off += sm.u1.seg.csum[s2][ri];
+    if (sg > 0) {
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        c += sv[u];
-        sm.u0.c[j0 + u][t] = c;
+      for (int u = 0; u < SEGL; ++u) sm.u0.c[sg * SEGL + u][ri] += off;
+    }
+    if (sg == 0) {
+      // EMA over the chunk: segment sums combined in token order
+      double qm = sm.u1.seg.em[0][0][ri], qe = sm.u1.seg.em[0][1][ri];
+      for (int s2 = 1; s2 < SEGS; ++s2) {
+        const int nv = min(max(n - s2 * SEGL, 0), SEGL);
+        double P = 1.0;
+        for (int u = 0; u < nv; ++u) P *= p.one_minus_alpha;
+        qm = P * qm + sm.u1.seg.em[s2][0][ri];
+        qe = P * qe + sm.u1.seg.em[s2][1][ri];
       }
+      double* ema = (double*)(out + CW::ema);
+      ema[ri] = qm;
+      ema[DK + ri] = qe;
+      ema[2 * DK + ri] = sm.u1.seg.first[0][ri];
+      ema[3 * DK + ri] = sm.u1.seg.first[1][ri];
     }
   }
   __syncthreads();
@@ -172,25 +241,35 @@ __global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cw
   // Qhat (row-major), Khat^T (LDS), Ktil^T and gamma_{n-1}
   {
     uint16_t* qh = (uint16_t*)(out + CW::qh);
-    for (int e = t; e < CT * DK; e += NT) {
-      const int j = e / DK, i = e % DK;
-      qh[e] = bf16_rne(bf16_f32(sm.u1.kq.q[j][i]) * __expf(-sm.u0.c[j][i]));
+    for (int e = t; e < CT * V8; e += NTP) {
+      const int j = e / V8, i0 = 8 * (e % V8);
+      const uint4 qv = *(const uint4*)&sm.q[j][i0];
+      const float4 c0 = *(const float4*)&sm.u0.c[j][i0], c1 = *(const float4*)&sm.u0.c[j][i0 + 4];
+      const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+      const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        o[u] = pack2(bf16_f32((uint16_t)(qw[u] & 0xFFFFu)) * __expf(-cc[2 * u]),
+                     bf16_f32((uint16_t)(qw[u] >> 16)) * __expf(-cc[2 * u + 1]));
+      *(uint4*)&qh[j * DK + i0] = make_uint4(o[0], o[1], o[2], o[3]);
     }
     uint16_t* ktt = (uint16_t*)(out + CW::ktt);
-    for (int e = t; e < CT * DK; e += NT) {
+    for (int e = t; e < CT * DK; e += NTP) {
       const int i = e / CT, j = e % CT;
       const float c = sm.u0.c[j][i], ce = sm.u0.c[CT - 1][i];
-      const float kk = bf16_f32(sm.u1.kq.k[j][i]);
+      const float kk = bf16_f32(sm.k[j][i]);
       sm.kht[i][j] = bf16_rne(kk * __expf(-c));
       ktt[e] = bf16_rne(kk * __expf(c - ce));
     }
     if (t < DK) ((float*)(out + CW::gend))[t] = (float)exp(-(double)sm.u0.c[CT - 1][t]);
   }
 
-  // L and A, block row J = w (tokens 16J .. 16J + 15): tiles (J, T <= J)
-  const bool erase = !p.no_erase;
+  // L (LDS) and A (global, bf16), block row J = w % 4: tiles (J, T <= J)
+  // of parity w / 4
   {
-    const int J = w;
+    uint16_t* am = (uint16_t*)(out + CW::am);
+    const int J = w & 3, par = w >> 2;
     const int k8 = 8 * (lane >> 4);
     const int jr = 16 * J + (lane & 15);
     bool wide = false;
@@ -207,34 +286,42 @@ __global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cw
     }
     for (int ks = 0; ks < DK / 32; ++ks) {
       const int i0 = 32 * ks + k8;
-      float fl[8], cr[8];
+      float cr[8];
+      if (J) {
+        const float4 a0 = *(const float4*)&sm.u0.c[16 * J - 1][i0];
+        const float4 a1 = *(const float4*)&sm.u0.c[16 * J - 1][i0 + 4];
+        cr[0] = a0.x; cr[1] = a0.y; cr[2] = a0.z; cr[3] = a0.w;
+        cr[4] = a1.x; cr[5] = a1.y; cr[6] = a1.z; cr[7] = a1.w;
+      } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        cr[e] = J ? sm.u0.c[16 * J - 1][i0 + e] : 0.f;
-        fl[e] = __expf(cr[e] - sm.u0.c[jr][i0 + e]);
+        for (int e = 0; e < 8; ++e) cr[e] = 0.f;
       }
+      const float4 j0 = *(const float4*)&sm.u0.c[jr][i0], j1 = *(const float4*)&sm.u0.c[jr][i0 + 4];
+      const float cj[8] = {j0.x, j0.y, j0.z, j0.w, j1.x, j1.y, j1.z, j1.w};
+      const uint4 kv = *(const uint4*)&sm.k[jr][i0], qv = *(const uint4*)&sm.q[jr][i0];
+      const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w}, qw[4] = {qv.x, qv.y, qv.z, qv.w};
       uint32_t ak[4], aq[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        ak[e] = pack2(bf16_f32(sm.u1.kq.k[jr][i0 + 2 * e]) * fl[2 * e],
-                      bf16_f32(sm.u1.kq.k[jr][i0 + 2 * e + 1]) * fl[2 * e + 1]);
-        aq[e] = pack2(bf16_f32(sm.u1.kq.q[jr][i0 + 2 * e]) * fl[2 * e],
-                      bf16_f32(sm.u1.kq.q[jr][i0 + 2 * e + 1]) * fl[2 * e + 1]);
+        const float f0 = __expf(cr[2 * e] - cj[2 * e]), f1 = __expf(cr[2 * e + 1] - cj[2 * e + 1]);
+        ak[e] = pack2(bf16_f32((uint16_t)(kw[e] & 0xFFFFu)) * f0, bf16_f32((uint16_t)(kw[e] >> 16)) * f1);
+        aq[e] = pack2(bf16_f32((uint16_t)(qw[e] & 0xFFFFu)) * f0, bf16_f32((uint16_t)(qw[e] >> 16)) * f1);
       }
       const uint4 AK = make_uint4(ak[0], ak[1], ak[2], ak[3]);
       const uint4 AQ = make_uint4(aq[0], aq[1], aq[2], aq[3]);
 #pragma unroll
       for (int T = 0; T < 4; ++T) {
-        if (T > J || (T == J && diag_valu)) continue;
+        if ((T & 1) != par || T > J || (T == J && diag_valu)) continue;
         const int jt = 16 * T + (lane & 15);
-        float fr[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) fr[e] = __expf(sm.u0.c[jt][i0 + e] - cr[e]);
+        const float4 t0 = *(const float4*)&sm.u0.c[jt][i0], t1 = *(const float4*)&sm.u0.c[jt][i0 + 4];
+        const float ct[8] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
+        const uint4 tv = *(const uint4*)&sm.k[jt][i0];
+        const uint32_t tw[4] = {tv.x, tv.y, tv.z, tv.w};
         uint32_t bk[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          bk[e] = pack2(bf16_f32(sm.u1.kq.k[jt][i0 + 2 * e]) * fr[2 * e],
-                        bf16_f32(sm.u1.kq.k[jt][i0 + 2 * e + 1]) * fr[2 * e + 1]);
+          bk[e] = pack2(bf16_f32((uint16_t)(tw[e] & 0xFFFFu)) * __expf(ct[2 * e] - cr[2 * e]),
+                        bf16_f32((uint16_t)(tw[e] >> 16)) * __expf(ct[2 * e + 1] - cr[2 * e + 1]));
         const uint4 BK = make_uint4(bk[0], bk[1], bk[2], bk[3]);
         if (erase) accL[T] = mma(AK, BK, accL[T]);
         accA[T] = mma(AQ, BK, accA[T]);
@@ -242,79 +329,107 @@ __global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cw
     }
 #pragma unroll
     for (int T = 0; T < 4; ++T) {
+      if ((T & 1) != par) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int j = 16 * J + 4 * (lane >> 4) + r, tau = 16 * T + (lane & 15);
         if (T > J) {
-          sm.L[j][tau] = 0.f;
-          sm.A[j][tau] = 0.f;
+          sm.u1.L[j][tau] = 0.f;
+          am[j * CT + tau] = 0;
         } else if (T < J || !diag_valu) {
-          sm.L[j][tau] = tau < j ? accL[T][r] : 0.f;
-          sm.A[j][tau] = tau <= j ? accA[T][r] : 0.f;
+          sm.u1.L[j][tau] = tau < j ? accL[T][r] : 0.f;
+          am[j * CT + tau] = tau <= j ? bf16_rne(accA[T][r]) : (uint16_t)0;
         }
       }
     }
-    if (diag_valu) {
+    if (diag_valu && (J & 1) == par) {
       // one exponential per pair and row: exp(c_tau - c_j) <= 1 for tau <= j
       for (int pr = lane; pr < 256; pr += WAVE) {
         const int j = 16 * J + pr / 16, tau = 16 * J + pr % 16;
         float l = 0.f, a = 0.f;
         if (tau <= j) {
           for (int i = 0; i < DK; ++i) {
-            const float kt = bf16_f32(sm.u1.kq.k[tau][i]) * __expf(sm.u0.c[tau][i] - sm.u0.c[j][i]);
-            l = fmaf(bf16_f32(sm.u1.kq.k[j][i]), kt, l);
-            a = fmaf(bf16_f32(sm.u1.kq.q[j][i]), kt, a);
+            const float kt = bf16_f32(sm.k[tau][i]) * __expf(sm.u0.c[tau][i] - sm.u0.c[j][i]);
+            l = fmaf(bf16_f32(sm.k[j][i]), kt, l);
+            a = fmaf(bf16_f32(sm.q[j][i]), kt, a);
           }
         }
-        sm.L[j][tau] = (tau < j && erase) ? l : 0.f;
-        sm.A[j][tau] = tau <= j ? a : 0.f;
+        sm.u1.L[j][tau] = (tau < j && erase) ? l : 0.f;
+        am[j * CT + tau] = tau <= j ? bf16_rne(a) : (uint16_t)0;
       }
     }
   }
   __syncthreads();
 
-  {
-    uint16_t* am = (uint16_t*)(out + CW::am);
-    for (int e = t; e < CT * CT; e += NT) am[e] = bf16_rne(sm.A[e / CT][e % CT]);
-  }
-  if (w == 0) {
-    // T = (I + diag(beta) L)^-1 by forward substitution, column m per lane;
-    // stored as T diag(beta)
-    const int m = lane;
-    float Tc[CT];
+  // T = (I + N)^-1 with N = diag(beta) L, by 16-row blocks.  Diagonal
+  // blocks: forward substitution, column m of block w on lane m.
+  if (w < 4 && lane < 16) {
+    const int J = w, m = lane;
+    float Tc[16];
 #pragma unroll
-    for (int j = 0; j < CT; ++j) {
+    for (int j = 0; j < 16; ++j) {
       float acc = 0.f;
 #pragma unroll
-      for (int tau = 0; tau < j; ++tau) acc = fmaf(sm.L[j][tau], Tc[tau], acc);
-      Tc[j] = j == m ? 1.f : (j > m ? -sm.beta[j] * acc : 0.f);
+      for (int tau = 0; tau < j; ++tau) acc = fmaf(sm.u1.L[16 * J + j][16 * J + tau], Tc[tau], acc);
+      Tc[j] = j == m ? 1.f : (j > m ? -sm.beta[16 * J + j] * acc : 0.f);
     }
-    const float bm = sm.beta[m];
 #pragma unroll
-    for (int j = 0; j < CT; ++j) sm.tb[j][m] = bf16_rne(Tc[j] * bm);
-  } else {
-    // V^T (the keys and queries are no longer needed)
-    for (int e = t - WAVE; e < CT * V8; e += NT - WAVE) {
-      const int j = e / V8, g = e % V8;
-      uint4 vv = make_uint4(0u, 0u, 0u, 0u);
-      if (j < n) vv = ((const uint4*)p.v)[th(j) * V8 + g];
-      const uint32_t x[4] = {vv.x, vv.y, vv.z, vv.w};
+    for (int j = 0; j < 16; ++j) sm.u0.t.T[16 * J + j][16 * J + m] = Tc[j];
+  }
+  // off-diagonal blocks by distance d: T_JK = -T_JJ sum_{M=K}^{J-1} N_JM T_MK
+  for (int d = 1; d < 4; ++d) {
+    __syncthreads();
+    const int J = w, K = w - d;
+    const int a = lane / 4, b4 = 4 * (lane % 4);   // output row, four columns
+    if (w < 4 && K >= 0) {
+      float x[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int M = K; M < J; ++M) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        sm.u1.vt[8 * g + 2 * u][j] = (uint16_t)(x[u] & 0xFFFFu);
-        sm.u1.vt[8 * g + 2 * u + 1][j] = (uint16_t)(x[u] >> 16);
+        for (int tau = 0; tau < 16; ++tau) {
+          const float nv = sm.u1.L[16 * J + a][16 * M + tau];
+          const float4 tv = *(const float4*)&sm.u0.t.T[16 * M + tau][16 * K + b4];
+          x[0] = fmaf(nv, tv.x, x[0]);
+          x[1] = fmaf(nv, tv.y, x[1]);
+          x[2] = fmaf(nv, tv.z, x[2]);
+          x[3] = fmaf(nv, tv.w, x[3]);
+        }
       }
+      const float bj = sm.beta[16 * J + a];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sm.u0.t.X[w][a][b4 + u] = bj * x[u];
+    }
+    __syncthreads();
+    if (w < 4 && K >= 0) {
+      float y[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int tau = 0; tau < 16; ++tau) {
+        const float tv = sm.u0.t.T[16 * J + a][16 * J + tau];
+        const float4 xv = *(const float4*)&sm.u0.t.X[w][tau][b4];
+        y[0] = fmaf(tv, xv.x, y[0]);
+        y[1] = fmaf(tv, xv.y, y[1]);
+        y[2] = fmaf(tv, xv.z, y[2]);
+        y[3] = fmaf(tv, xv.w, y[3]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sm.u0.t.T[16 * J + a][16 * K + b4 + u] = -y[u];
     }
   }
   __syncthreads();
+  for (int e = t; e < CT * CT; e += NTP) {
+    const int j = e / CT, m = e % CT;
+    sm.tb[j][m] = m <= j ? bf16_rne(sm.u0.t.T[j][m] * sm.beta[m]) : (uint16_t)0;
+  }
+  __syncthreads();
 
-  // Uv = T diag(beta) V and Wk = T diag(beta) Khat: token tile w, all columns
+  // Uv = T diag(beta) V and Wk = T diag(beta) Khat: token tile w % 4,
+  // column half w / 4
   {
-    const int J = w;
+    constexpr int NC = DK / 32;   // 16-column tiles per half
+    const int J = w & 3, c0 = (w >> 2) * NC;
     const int k8 = 8 * (lane >> 4);
-    f32x4 au[DK / 16], aw[DK / 16];
+    f32x4 au[NC], aw[NC];
 #pragma unroll
-    for (int ct = 0; ct < DK / 16; ++ct) {
+    for (int ct = 0; ct < NC; ++ct) {
       au[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
       aw[ct] = au[ct];
     }
@@ -323,11 +438,11 @@ __global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cw
       if (32 * ks > 16 * J + 15) break;   // T is lower triangular
       const uint4 a = *(const uint4*)&sm.tb[16 * J + (lane & 15)][32 * ks + k8];
 #pragma unroll
-      for (int ct = 0; ct < DK / 16; ++ct) {
-        const uint4 bv = *(const uint4*)&sm.u1.vt[16 * ct + (lane & 15)][32 * ks + k8];
+      for (int ct = 0; ct < NC; ++ct) {
+        const uint4 bv = *(const uint4*)&sm.vt[16 * (c0 + ct) + (lane & 15)][32 * ks + k8];
         au[ct] = mma(a, bv, au[ct]);
         if (erase) {
-          const uint4 bk = *(const uint4*)&sm.kht[16 * ct + (lane & 15)][32 * ks + k8];
+          const uint4 bk = *(const uint4*)&sm.kht[16 * (c0 + ct) + (lane & 15)][32 * ks + k8];
           aw[ct] = mma(a, bk, aw[ct]);
         }
       }
@@ -335,49 +450,13 @@ __global__ void __launch_bounds__(NT) k_chunk_prep(KParams p, int C, uint8_t* cw
     float* uv = (float*)(out + CW::uv);
     uint16_t* wk = (uint16_t*)(out + CW::wk);
 #pragma unroll
-    for (int ct = 0; ct < DK / 16; ++ct) {
+    for (int ct = 0; ct < NC; ++ct) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int j = 16 * J + 4 * (lane >> 4) + r, i = 16 * ct + (lane & 15);
+        const int j = 16 * J + 4 * (lane >> 4) + r, i = 16 * (c0 + ct) + (lane & 15);
         uv[j * DK + i] = au[ct][r];
         wk[j * DK + i] = bf16_rne(aw[ct][r]);
       }
-    }
-  }
-
-  // EMA sums from zero over the chunk, in token order (double)
-  {
-    double qm = 0.0, qe = 0.0, z0 = 0.0, y0 = 0.0;
-    for (int j0 = 0; j0 < n; j0 += 16) {
-      __syncthreads();   // c (first batch) or the previous batch is consumed
-      for (int e = t; e < 16 * DK; e += NT) {
-        const int u = e / DK, i = e % DK, j = j0 + u;
-        if (j < n) {
-          const float sv = p.per_head ? p.s[th(j)] : p.s[th(j) * DK + i];
-          sm.u0.ema[0][u][i] = decay_sample(sv);
-          sm.u0.ema[1][u][i] =
-              erase ? erase_sample(in_f32<true>(p.k, th(j) * DK + i), p.beta[th(j)]) : 0.0;
-        }
-      }
-      __syncthreads();
-      if (t < DK) {
-        if (j0 == 0) {
-          z0 = sm.u0.ema[0][0][t];
-          y0 = sm.u0.ema[1][0][t];
-        }
-        const int nb = min(16, n - j0);
-        for (int u = 0; u < nb; ++u) {
-          qm = p.one_minus_alpha * qm + p.alpha * sm.u0.ema[0][u][t];
-          qe = p.one_minus_alpha * qe + p.alpha * sm.u0.ema[1][u][t];
-        }
-      }
-    }
-    if (t < DK) {
-      double* ema = (double*)(out + CW::ema);
-      ema[t] = qm;
-      ema[DK + t] = qe;
-      ema[2 * DK + t] = z0;
-      ema[3 * DK + t] = y0;
     }
   }
 }
@@ -398,12 +477,14 @@ template <int DK>
 __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw) {
   using CW = ChunkWs<DK>;
   constexpr int RT = DK / 64;            // 16-row state tiles per wave
+  constexpr int KS = DK / 32;            // k-steps over the state's rows
   const int nsl = p.dv / SLICE;
   const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
   const int b = bh / p.H, h = bh % p.H;
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
   const int n = p.ntk;
   const int k8 = 8 * (lane >> 4), l16 = lane & 15;
+  const int jrow = 16 * w + l16;
   const uint8_t* in = cw + (size_t)bh * CW::bytes;
   const Layout L = p.L;
   const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
@@ -411,6 +492,40 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   __shared__ ApplySmem<DK> sm;
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
+
+  // the chunk record's operands of this lane, loaded before the state's
+  // record so that both round trips overlap
+  const uint16_t* wk = (const uint16_t*)(in + CW::wk);
+  const uint16_t* qh = (const uint16_t*)(in + CW::qh);
+  const uint16_t* am = (const uint16_t*)(in + CW::am);
+  const uint16_t* ktt = (const uint16_t*)(in + CW::ktt);
+  const float* uv = (const float*)(in + CW::uv);
+  const float* gend = (const float*)(in + CW::gend);
+  const bool erase = !p.no_erase;
+  uint4 fw[KS], fq[KS], fa[CT / 32], fk[RT][CT / 32];
+  float fu[4][4], fg[RT][4];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    fw[ks] = erase ? *(const uint4*)&wk[jrow * DK + 32 * ks + k8] : make_uint4(0u, 0u, 0u, 0u);
+    fq[ks] = *(const uint4*)&qh[jrow * DK + 32 * ks + k8];
+  }
+#pragma unroll
+  for (int ks = 0; ks < CT / 32; ++ks)
+    fa[ks] = 32 * ks <= 16 * w + 15 ? *(const uint4*)&am[jrow * CT + 32 * ks + k8]
+                                    : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int ks = 0; ks < CT / 32; ++ks)
+      fk[rt][ks] = *(const uint4*)&ktt[(16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+  }
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) fu[ct][r] = uv[(16 * w + 4 * (lane >> 4) + r) * DK + SLICE * sl + 16 * ct + l16];
+
   {
     // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
     const uint4* src = (const uint4*)(rec + L.codes_off);
@@ -422,7 +537,6 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
 
   // S0 at this lane's state-tile positions: float32 gamma_{n-1} * S0 as the
   // accumulator of S_n, bf16 S0^T in LDS for the products with S0
-  const float* gend = (const float*)(in + CW::gend);
   f32x4 acc[RT][4];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -432,14 +546,13 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
       const uint4 d = meta.desc[i];
       const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
       const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
-      const float ge = gend[i];
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
         const int c = 16 * ct + l16;
         const uint32_t lo = words[d.x + c], hi = words[d.x + SLICE + c];
         const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
         const float x = ((float)code + add) * mul;
-        acc[rt][ct][r] = ge * x;
+        acc[rt][ct][r] = fg[rt][r] * x;
         sm.s0t[c][i] = bf16_rne(x);
       }
     }
@@ -447,49 +560,40 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   __syncthreads();
 
   // W = Wk S0 and O = Qhat S0 for token tile w
-  const uint16_t* wk = (const uint16_t*)(in + CW::wk);
-  const uint16_t* qh = (const uint16_t*)(in + CW::qh);
-  const int jrow = 16 * w + l16;
   f32x4 aw[4], ao[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
     aw[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     ao[ct] = aw[ct];
   }
-  const bool erase = !p.no_erase;
 #pragma unroll
-  for (int ks = 0; ks < DK / 32; ++ks) {
-    const uint4 a1 = *(const uint4*)&wk[jrow * DK + 32 * ks + k8];
-    const uint4 a2 = *(const uint4*)&qh[jrow * DK + 32 * ks + k8];
+  for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
       const uint4 bs = *(const uint4*)&sm.s0t[16 * ct + l16][32 * ks + k8];
-      if (erase) aw[ct] = mma(a1, bs, aw[ct]);
-      ao[ct] = mma(a2, bs, ao[ct]);
+      if (erase) aw[ct] = mma(fw[ks], bs, aw[ct]);
+      ao[ct] = mma(fq[ks], bs, ao[ct]);
     }
   }
   // U = Uv - W, transposed into LDS as bf16
-  const float* uv = (const float*)(in + CW::uv);
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int j = 16 * w + 4 * (lane >> 4) + r, c = 16 * ct + l16;
-      sm.ut[c][j] = bf16_rne(uv[j * DK + SLICE * sl + c] - aw[ct][r]);
+      sm.ut[c][j] = bf16_rne(fu[ct][r] - aw[ct][r]);
     }
   }
   __syncthreads();
 
   // O += A U (A is lower triangular: k-steps up to the tile's last token)
-  const uint16_t* am = (const uint16_t*)(in + CW::am);
 #pragma unroll
   for (int ks = 0; ks < CT / 32; ++ks) {
     if (32 * ks > 16 * w + 15) break;
-    const uint4 a = *(const uint4*)&am[jrow * CT + 32 * ks + k8];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
       const uint4 bu = *(const uint4*)&sm.ut[16 * ct + l16][32 * ks + k8];
-      ao[ct] = mma(a, bu, ao[ct]);
+      ao[ct] = mma(fa[ks], bu, ao[ct]);
     }
   }
 #pragma unroll
@@ -503,17 +607,14 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   }
 
   // S_n += Ktil^T U
-  const uint16_t* ktt = (const uint16_t*)(in + CW::ktt);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    const int irow = 16 * (RT * w + rt) + l16;
 #pragma unroll
     for (int ks = 0; ks < CT / 32; ++ks) {
-      const uint4 a = *(const uint4*)&ktt[irow * CT + 32 * ks + k8];
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
         const uint4 bu = *(const uint4*)&sm.ut[16 * ct + l16][32 * ks + k8];
-        acc[rt][ct] = mma(a, bu, acc[rt][ct]);
+        acc[rt][ct] = mma(fk[rt][ks], bu, acc[rt][ct]);
       }
     }
   }
@@ -575,7 +676,7 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
   for (int g0 = 0; g0 < nch; g0 += gc) {
     const int ng = nch - g0 < gc ? nch - g0 : gc;
     p.tok0 = g0 * C;
-    hipError_t e = launch("prep", k_chunk_prep<DK>, nbh * ng, NT, 0, st, p, C, p.ws_chunk);
+    hipError_t e = launch("prep", k_chunk_prep<DK>, nbh * ng, NTP, 0, st, p, C, p.ws_chunk);
     if (e != hipSuccess) return e;
     for (int c = 0; c < ng; ++c) {
       p.tok0 = (g0 + c) * C;

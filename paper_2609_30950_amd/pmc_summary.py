@@ -26,7 +26,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 
 
-KERNEL_SOURCES = ("kda_alloc.hpp", "kda_device.hpp", "kda_kernels.hip", "kda_kernels.hpp")
+# device-kernel sources that the counter summaries describe
+KERNEL_SOURCES = ("kda_alloc.hpp", "kda_chunked.hip", "kda_device.hpp", "kda_kernels.hip",
+                  "kda_kernels.hpp", "kda_record.hpp")
 
 
 def source_hash():
@@ -48,6 +50,9 @@ def per_kernel(d, counter):
 
 
 def short(name):
+    for k in ("k_chunk_prep", "k_chunk_apply"):
+        if "kda::" + k in name:
+            return k[8:]
     for k in ("k_requant", "k_chunk", "k_alloc", "k_step32", "k_pack", "k_unpack"):
         if "kda::" + k in name:
             return {"k_chunk": "stats", "k_requant": "requant", "k_alloc": "alloc"}.get(k, k[2:])

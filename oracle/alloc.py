@@ -19,6 +19,11 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
   (then the lower l).  Slot values of one row fall with l, so granted slots
   form a prefix and b_i = b_min + (slots granted to row i).  Keys are compared
   exactly as (exponent - 2l, mantissa) pairs.
+* ``head_weights``: the key of a head unit (Sec. 3, Allocation units: one
+  width per head, R~ = 1 so only decay sets widths).  Rows sharing one width
+  b contribute (sum_i Gamma_i) 2^(-2b) to the proxy, so the head's key is the
+  mean Gamma of its rows (sequential float64 sum in row order, / d_k); heads
+  are then allocated like rows.
 * ``allocate_bruteforce``: exhaustive search over all width vectors, tiny N.
 * ``real_allocation`` / ``am_gm_gain``: eq. alloc and the AM/GM distortion
   ratio quoted after it.
@@ -88,6 +93,16 @@ def allocate(c, mean_bits, b_min, b_max):
     b = np.full(N, b_min, np.int64)
     np.add.at(b, rows[chosen], 1)
     return b
+
+
+def head_weights(gamma):
+    """gamma: [..., dk] float64 -> [...] mean over the rows."""
+    gamma = np.asarray(gamma, F64)
+    dk = gamma.shape[-1]
+    acc = np.zeros(gamma.shape[:-1], F64)
+    for i in range(dk):
+        acc = acc + gamma[..., i]
+    return acc / F64(dk)
 
 
 def proxy(c, b):

@@ -21,6 +21,12 @@ stores the sign and the row's mean absolute value.  Float32 contract:
 
 Dequantisation: x^ = fl32(c * Delta) (b >= 2), +-mu (b = 1).
 
+Head units (Sec. 3, Allocation units: one width per head and scales per block
+of 32 key channels): ``quantize_blocks`` applies the same levels and clip-factor
+fit to every scale group of 32 consecutive rows of one column, R the group's
+absolute maximum, the error summed over the group's rows in row order
+(sequential fma32 from 0); widths are at least 2.
+
 Parity: pinned (P13 single write-back MSE, P14 codec rules, P16 brute-force
 argmin with rational arithmetic) in ``tests/test_oracle_quant.py``.
 """
@@ -30,6 +36,7 @@ from .fp import fma32, fp16_sat, halving_tree, F32, F64
 
 N_FIT = 16
 SEG = 64
+BLOCK = 32
 
 
 def levels(b):
@@ -129,3 +136,45 @@ def dequantize_rows(codes, scale, b):
         mu = sc[one][:, None]
         out[one] = np.where(codes[one] != 0, -mu, mu)
     return out
+
+
+def quantize_blocks(x, b):
+    """x: [dk, dv] float32 (one head), b >= 2 the head's width.
+
+    Returns codes int32 [dk, dv], scale float16 [dk/32, dv] and mstar
+    [dk/32, dv]; scale group (k, j) is rows 32k .. 32k+31 of column j.
+    """
+    x = np.asarray(x, F32)
+    dk, dv = x.shape
+    assert b >= 2 and dk % BLOCK == 0
+    g = x.reshape(dk // BLOCK, BLOCK, dv)
+    R = np.max(np.abs(g), axis=1).astype(F32)
+    n = levels(b)
+    phi = phi_table(b)
+    best_err = None
+    for m in range(N_FIT):
+        delta = fp16_sat((R * phi[m]).astype(F32)).astype(F32)
+        with np.errstate(divide="ignore"):
+            inv = np.where(delta > 0, (F32(1.0) / delta).astype(F32), F32(0.0)).astype(F32)
+        c = np.clip(np.rint((g * inv[:, None, :]).astype(F32)), -n, n).astype(F32)
+        e = fma32(-c, np.broadcast_to(delta[:, None, :], g.shape), g)
+        err = np.zeros(R.shape, F32)
+        for r in range(BLOCK):
+            err = fma32(e[:, r, :], e[:, r, :], err)
+        if best_err is None:
+            best_err, best_c, best_d, best_m = err, c, delta, np.zeros(R.shape, np.int64)
+            continue
+        better = err < best_err          # strict: keeps the smallest m on ties
+        best_err = np.where(better, err, best_err)
+        best_c = np.where(better[:, None, :], c, best_c)
+        best_d = np.where(better, delta, best_d)
+        best_m = np.where(better, m, best_m)
+    return best_c.reshape(dk, dv).astype(np.int32), best_d.astype(np.float16), best_m
+
+
+def dequantize_blocks(codes, scale):
+    """codes [..., dk, dv] int, scale float16 [..., dk/32, dv] -> float32."""
+    codes = np.asarray(codes)
+    sc = np.asarray(scale, np.float16).astype(F32)
+    rep = np.repeat(sc, BLOCK, axis=-2)
+    return (codes.astype(F32) * rep).astype(F32)

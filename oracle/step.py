@@ -17,6 +17,11 @@ At a write-back, per sequence:
   4. per-row fitted quantiser; the rates are stored as a 16-bit log code and
      the erase rate as FP16; the EMAs continue from the decoded values.
 
+Head units (Cfg.unit = "head", Sec. 3, Allocation units: Gated DeltaNet with
+per-head decay and normalisation): R~ = 1, each head's key is the mean Gamma
+of its rows, one width per head from the layer budget over the H heads, and
+the block quantiser (scales per 32 rows of a column).
+
 State is handled as a dict of decoded record fields with a leading [B, H]
 (see ``record.py`` for the bytes).  ``mirror_*`` use the float32 contract of
 ``recurrence.mirror_step``; ``truth_outputs`` gives float64 outputs from the
@@ -43,9 +48,16 @@ class Cfg:
     b_max: int = 8
     span: int = 64
     erase: bool = True              # False: no erasure (Mamba-2)
+    unit: str = "row"               # "row" (a width per row) or "head" (block scales)
 
 
 def zero_state(B, H, cfg):
+    if cfg.unit == "head":
+        return dict(ntok=np.zeros((B, H), np.int64), width=np.zeros((B, H), np.int64),
+                    bscale=np.zeros((B, H, cfg.dk // quant.BLOCK, cfg.dv), np.float16),
+                    z=np.zeros((B, H, cfg.dk), np.uint16),
+                    r16=np.zeros((B, H, cfg.dk), np.float16),
+                    codes=np.zeros((B, H, cfg.dk, cfg.dv), np.int64))
     return dict(ntok=np.zeros((B, H), np.int64),
                 widths=np.ones((B, H, cfg.dk), np.int64),
                 scale=np.zeros((B, H, cfg.dk), np.float16),
@@ -55,6 +67,8 @@ def zero_state(B, H, cfg):
 
 
 def dequantize(state):
+    if "bscale" in state:
+        return quant.dequantize_blocks(state["codes"], state["bscale"])
     B, H, dk, dv = state["codes"].shape
     x = quant.dequantize_rows(state["codes"].reshape(-1, dv),
                               state["scale"].reshape(-1),
@@ -83,8 +97,32 @@ def allocate_widths(c, cfg):
     return out
 
 
+def write_back_heads(S, m, e, ntok, cfg, gamma=None):
+    """Head units: one width per head from the mean Gamma of its rows, block
+    scales.  Same arguments and results as write_back."""
+    B, H, dk, dv = S.shape
+    s_hat, r = stats.ema_rates(m, e)
+    g = stats.gamma_hat(s_hat, r) if gamma is None else np.asarray(gamma, F64)
+    ch = alloc.head_weights(g)
+    width = np.stack([alloc.allocate(ch[b], cfg.mean_bits, cfg.b_min, cfg.b_max)
+                      for b in range(B)])
+    codes = np.zeros((B, H, dk, dv), np.int64)
+    bscale = np.zeros((B, H, dk // quant.BLOCK, dv), np.float16)
+    mstar = np.zeros((B, H, dk // quant.BLOCK, dv), np.int64)
+    for b in range(B):
+        for h in range(H):
+            c, sc, ms = quant.quantize_blocks(S[b, h], int(width[b, h]))
+            codes[b, h], bscale[b, h], mstar[b, h] = c, sc, ms
+    state = dict(ntok=np.asarray(ntok, np.int64), width=width, bscale=bscale,
+                 z=stats.logq_encode(s_hat), r16=stats.r_encode(r), codes=codes)
+    diag = dict(S=S, c=ch, gamma=g, s_hat=s_hat, r=r, mstar=mstar)
+    return state, diag
+
+
 def write_back(S, m, e, ntok, cfg, gamma=None):
     """Quantise float32 S [B,H,dk,dv] with EMA states m, e -> (state, diag)."""
+    if cfg.unit == "head":
+        return write_back_heads(S, m, e, ntok, cfg, gamma)
     B, H, dk, dv = S.shape
     s_hat, r = stats.ema_rates(m, e)
     g = stats.gamma_hat(s_hat, r) if gamma is None else np.asarray(gamma, F64)

@@ -93,6 +93,21 @@ typedef struct {
                              bf16 operand rounding, with C <= 64 and
                              d_k <= 128.  The write-back quantiser is the
                              same in both modes.                              */
+  int32_t head_units;     /* 1: allocation units are heads (Sec. 3, Allocation
+                             units, Gated DeltaNet): one width per head from
+                             the layer budget over the H heads of a sequence
+                             (key: mean Gamma of the head's rows; R~ = 1),
+                             FP16 scales per block of 32 rows of a column;
+                             needs group_rows = d_k, KDA_SCOPE_SEQUENCE and
+                             2 <= b_min <= b_max <= 8.  kda_step and
+                             kda_prefill only (the two-phase step, pack,
+                             unpack and kda_alloc_bits return
+                             KDA_ERR_UNSUPPORTED).  Record layout: u32
+                             tokens; u32 width (0 = zero state); 8 reserved
+                             bytes; rate code u16 [d_k]; erase rate FP16
+                             [d_k]; block scales FP16 [d_k/32][d_v]; at the
+                             next multiple of 256 the code words as below
+                             with every row of width b (row i at bit i b). */
 } kda_config;
 
 /* Bytes of one (sequence, head) record slot; 0 if the config is invalid.

@@ -17,7 +17,7 @@ class kda_config(ctypes.Structure):
         ("mean_bits", ctypes.c_double), ("b_min", ctypes.c_int32), ("b_max", ctypes.c_int32),
         ("ema_span", ctypes.c_int32), ("decay_per_head", ctypes.c_int32),
         ("state32", ctypes.c_int32), ("no_erase", ctypes.c_int32),
-        ("chunked", ctypes.c_int32),
+        ("chunked", ctypes.c_int32), ("head_units", ctypes.c_int32),
     ]
 
 

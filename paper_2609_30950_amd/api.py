@@ -27,12 +27,13 @@ class Config:
     state32: int = 0
     no_erase: int = 0          # 1: Mamba-2 style recurrence without erasure
     chunked: int = 0           # 1: chunked (WY/UT) prefill on MFMA
+    head_units: int = 0        # 1: one width per head, block scales (Gated DeltaNet)
 
     def c(self):
         return kda_config(self.B, self.H, self.d_k, self.d_v, self.group_rows, self.scope,
                           float(self.mean_bits), self.b_min, self.b_max, self.ema_span,
                           self.decay_per_head, self.state32, self.no_erase,
-                          self.chunked)
+                          self.chunked, self.head_units)
 
 
 def _ptr(t, dtype=None, numel=None, name="tensor"):

@@ -52,6 +52,20 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg->no_erase != 0 && cfg->no_erase != 1) return KDA_ERR_ARG;
   if (cfg->chunked != 0 && cfg->chunked != 1) return KDA_ERR_ARG;
   if (cfg->chunked && (cfg->d_k > 128 || cfg->state32)) return KDA_ERR_UNSUPPORTED;
+  if (cfg->head_units != 0 && cfg->head_units != 1) return KDA_ERR_ARG;
+  if (cfg->head_units) {
+    // one width per head, block scales: per-head normalisation, the layer
+    // budget over the heads of a sequence, widths 2..8
+    if (cfg->state32 || cfg->chunked) return KDA_ERR_UNSUPPORTED;
+    if (cfg->group_rows != cfg->d_k || cfg->scope != KDA_SCOPE_SEQUENCE) return KDA_ERR_ARG;
+    if (cfg->b_min < 2 || cfg->b_max < cfg->b_min || cfg->b_max > 8) return KDA_ERR_ARG;
+    if (cfg->ema_span < 1 || !std::isfinite(cfg->mean_bits)) return KDA_ERR_ARG;
+    if (cfg->H > 4096) return KDA_ERR_UNSUPPORTED;
+    const long long K = (long long)std::floor(cfg->mean_bits * (double)cfg->H + 0.5);
+    if (K < (long long)cfg->H * cfg->b_min || K > (long long)cfg->H * cfg->b_max) return KDA_ERR_ARG;
+    if (need) *need = (int)(K - (long long)cfg->H * cfg->b_min);
+    return KDA_OK;
+  }
   if (cfg->state32) {
     if (need) *need = 0;
     return KDA_OK;
@@ -95,7 +109,8 @@ KParams make_params(const kda_config* cfg, int need) {
   p.need = need;
   p.alpha = 2.0 / (double)(cfg->ema_span + 1);
   p.one_minus_alpha = 1.0 - p.alpha;
-  p.L = kda::make_layout(cfg->d_k, cfg->d_v, cfg->b_max < 1 ? 1 : cfg->b_max);
+  p.L = cfg->head_units ? kda::make_head_layout(cfg->d_k, cfg->d_v, cfg->b_max)
+                        : kda::make_layout(cfg->d_k, cfg->d_v, cfg->b_max < 1 ? 1 : cfg->b_max);
   p.diag_fit = kda::prof_counter();
   for (int b = 0; b <= kda::MAX_B; ++b)
     for (int m = 0; m < kda::N_FIT; ++m) {
@@ -130,6 +145,7 @@ extern "C" {
 size_t kda_record_bytes(const kda_config* cfg) {
   if (check_cfg(cfg, nullptr) != KDA_OK) return 0;
   if (cfg->state32) return (size_t)cfg->d_k * cfg->d_v * sizeof(float);
+  if (cfg->head_units) return (size_t)kda::make_head_layout(cfg->d_k, cfg->d_v, cfg->b_max).slot;
   return (size_t)kda::make_layout(cfg->d_k, cfg->d_v, cfg->b_max).slot;
 }
 
@@ -179,6 +195,7 @@ int kda_alloc_bits(const kda_config* cfg, const double* gamma, const float* R, u
   int st = check_cfg(cfg, &need);
   if (st != KDA_OK) return st;
   if (cfg->state32) return KDA_ERR_ARG;
+  if (cfg->head_units) return KDA_ERR_UNSUPPORTED;
   if (!gamma || !R || !bits) return KDA_ERR_ARG;
   if (!ws) return KDA_ERR_WORKSPACE;
   KParams p = make_params(cfg, need);
@@ -192,6 +209,7 @@ int kda_pack_state(const kda_config* cfg, const float* S, const uint8_t* bits, c
   int st = check_cfg(cfg, &need);
   if (st != KDA_OK) return st;
   if (cfg->state32) return KDA_ERR_ARG;
+  if (cfg->head_units) return KDA_ERR_UNSUPPORTED;
   if (!S || !bits || !s_hat || !r || !records) return KDA_ERR_ARG;
   if (!aligned16(S) || !aligned16(records)) return KDA_ERR_ARG;
   KParams p = make_params(cfg, need);
@@ -205,6 +223,7 @@ int kda_unpack_state(const kda_config* cfg, const void* records, float* S, uint8
   int st = check_cfg(cfg, &need);
   if (st != KDA_OK) return st;
   if (!records || !aligned16(records)) return KDA_ERR_ARG;
+  if (cfg->head_units) return KDA_ERR_UNSUPPORTED;
   if (cfg->state32 && (bits || s_hat || r)) return KDA_ERR_ARG;
   KParams p = make_params(cfg, need);
   p.records = const_cast<void*>(records);
@@ -246,6 +265,7 @@ int kda_step(const kda_config* cfg, void* records, const float* q, const float* 
   KParams p;
   const int st = step_params(cfg, records, q, k, v, s, beta, gamma, o, ws, 3, &p);
   if (st != KDA_OK) return st;
+  if (cfg->head_units) return hip_status(kda::launch_step_heads(p, (hipStream_t)stream));
   return hip_status(kda::launch_step(p, (hipStream_t)stream));
 }
 
@@ -255,6 +275,7 @@ int kda_step_outputs(const kda_config* cfg, void* records, const float* q, const
   KParams p;
   const int st = step_params(cfg, records, q, k, v, s, beta, gamma, o, ws, 1, &p);
   if (st != KDA_OK) return st;
+  if (cfg->head_units) return KDA_ERR_UNSUPPORTED;
   return hip_status(kda::launch_step_outputs(p, (hipStream_t)stream));
 }
 
@@ -263,6 +284,7 @@ int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* str
   const int st = step_params(cfg, records, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                              nullptr, ws, 2, &p);
   if (st != KDA_OK) return st;
+  if (cfg->head_units) return KDA_ERR_UNSUPPORTED;
   return hip_status(kda::launch_step_writeback(p, (hipStream_t)stream));
 }
 
@@ -292,6 +314,7 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, cons
     if (C > 64) return KDA_ERR_ARG;
     return hip_status(kda::launch_prefill_chunked(p, C, (hipStream_t)stream));
   }
+  if (cfg->head_units) return hip_status(kda::launch_prefill_heads(p, C, (hipStream_t)stream));
   return hip_status(kda::launch_prefill(p, C, (hipStream_t)stream));
 }
 

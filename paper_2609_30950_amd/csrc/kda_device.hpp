@@ -38,6 +38,23 @@ __host__ __device__ inline Layout make_layout(int dk, int dv, int bmax) {
   return L;
 }
 
+// Record layout of a head allocation unit (one width per head, FP16 scales
+// per block of 32 rows of one column): u32 tokens, u32 width at w_off = 4,
+// 8 reserved bytes, rate codes u16[dk], erase rates FP16[dk], block scales
+// FP16[dk/32][dv] at sc_off, code words at the next multiple of 256.
+__host__ __device__ inline Layout make_head_layout(int dk, int dv, int bmax) {
+  Layout L;
+  L.w_off = 4;
+  L.z_off = 16;
+  L.r_off = L.z_off + 2 * dk;
+  L.sc_off = L.r_off + 2 * dk;
+  L.meta_end = L.sc_off + (dk / 32) * dv * 2;
+  L.codes_off = round_up(L.meta_end, 256);
+  L.wc = (dk * bmax + 31) / 32;
+  L.slot = round_up(L.codes_off + L.wc * dv * 4, 256);
+  return L;
+}
+
 // ---------------------------------------------------------------- FP16 ---
 // float -> FP16 bits, round to nearest even (v_cvt_f16_f32), saturating
 // at the largest finite value 65504 (0x7BFF) instead of overflowing to inf.

@@ -26,40 +26,11 @@
 #include "kda_kernels.hpp"
 #include "kda_profile.hpp"
 #include "kda_record.hpp"
+#include "kda_recur.hpp"
 
 namespace kda {
 
 // ------------------------------------------------------------ helpers ---
-
-// Per-row scalars of one token for the recurrence.
-template <int DK>
-struct RowSmem {
-  float2 ak[DK];   // {fl32(exp(-s)), k}: first pass of the recurrence
-  float2 gq[DK];   // {fl32(beta * k), q}: second pass
-};
-
-// Inputs of row t for the rate statistics: decay rate, key, beta.
-struct RowIn {
-  float s, k, beta;
-};
-
-// Per-row scalars of token `tok` of head bh into LDS (threads t < DK); returns
-// the row's own inputs for the rate statistics.
-template <int DK, bool BF16>
-__device__ __forceinline__ RowIn load_rows(RowSmem<DK>& rs, const KParams& p, int bh, int tok) {
-  const int t = threadIdx.x;
-  RowIn in = {0.f, 0.f, 0.f};
-  if (t < DK) {
-    const int b = bh / p.H, h = bh % p.H;
-    const size_t th = ((size_t)b * p.T + tok) * p.H + h;       // (b, tok, h)
-    in.s = p.per_head ? p.s[th] : p.s[th * DK + t];
-    in.beta = p.beta[th];
-    in.k = in_f32<BF16>(p.k, th * DK + t);
-    rs.ak[t] = make_float2((float)exp(-(double)in.s), in.k);
-    rs.gq[t] = make_float2(in.beta * in.k, in_f32<BF16>(p.q, th * DK + t));
-  }
-  return in;
-}
 
 // Copy the meaningful code words of a record (ceil(sum b / 32) words per
 // column) into LDS with coalesced 16-byte loads.  All threads must call.
@@ -110,137 +81,6 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
       for (int q = r - 3; q <= r; ++q)
 #pragma unroll
         for (int c = 0; c < CPL; ++c) asm volatile("" : "+v"(X[q][c])::"memory");
-    }
-  }
-}
-
-// Row scalars reach the lanes by DPP row broadcasts folded into the
-// arithmetic: lane l of wave w holds the scalars of rows 32w + l % 16 (block
-// 0) and 32w + 16 + l % 16 (block 1), replicated in the four 16-lane rows,
-// and row_newbcast:r hands lane r's value of each 16-lane row to all of its
-// lanes as the first operand.  Sixteen rows per asm block; the leading s_nop
-// covers a vector write of a broadcast source just before the block.
-#define KDA_P1(r)                                                                   \
-  "v_mul_f32_dpp %" #r ", %17, %" #r " row_newbcast:" #r                           \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
-  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
-#define KDA_P2(r)                                                                   \
-  "v_fmac_f32_dpp %" #r ", %17, %19 row_newbcast:" #r                              \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"                                       \
-  "v_fmac_f32_dpp %16, %18, %" #r " row_newbcast:" #r                              \
-  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
-#define KDA_X16(X, o, c)                                                             \
-  "+v"(X[o + 0][c]), "+v"(X[o + 1][c]), "+v"(X[o + 2][c]), "+v"(X[o + 3][c]),       \
-      "+v"(X[o + 4][c]), "+v"(X[o + 5][c]), "+v"(X[o + 6][c]), "+v"(X[o + 7][c]),   \
-      "+v"(X[o + 8][c]), "+v"(X[o + 9][c]), "+v"(X[o + 10][c]), "+v"(X[o + 11][c]), \
-      "+v"(X[o + 12][c]), "+v"(X[o + 13][c]), "+v"(X[o + 14][c]), "+v"(X[o + 15][c])
-
-// First pass over rows O..O+15 of column C: X_r = a_r X_r; acc = fma(k_r, X_r, acc)
-// in row order.
-template <int O, int C, int CPL>
-__device__ __forceinline__ void pass1_16(float (&X)[ROW_BLOCK][CPL], float& acc, float A, float K) {
-  asm("s_nop 1\n" KDA_P1(0) KDA_P1(1) KDA_P1(2) KDA_P1(3) KDA_P1(4) KDA_P1(5) KDA_P1(6) KDA_P1(7)
-      KDA_P1(8) KDA_P1(9) KDA_P1(10) KDA_P1(11) KDA_P1(12) KDA_P1(13) KDA_P1(14) KDA_P1(15)
-      : KDA_X16(X, O, C), "+v"(acc)
-      : "v"(A), "v"(K));
-}
-
-// Second pass over rows O..O+15 of column C: X_r = fma(g_r, w, X_r);
-// acc = fma(q_r, X_r, acc).
-template <int O, int C, int CPL>
-__device__ __forceinline__ void pass2_16(float (&X)[ROW_BLOCK][CPL], float& acc, float G, float Q,
-                                         float wv) {
-  asm("s_nop 1\n" KDA_P2(0) KDA_P2(1) KDA_P2(2) KDA_P2(3) KDA_P2(4) KDA_P2(5) KDA_P2(6) KDA_P2(7)
-      KDA_P2(8) KDA_P2(9) KDA_P2(10) KDA_P2(11) KDA_P2(12) KDA_P2(13) KDA_P2(14) KDA_P2(15)
-      : KDA_X16(X, O, C), "+v"(acc)
-      : "v"(G), "v"(Q), "v"(wv));
-}
-
-template <int DK, int DV>
-struct RecSmem {
-  float up[DK / ROW_BLOCK][DV];
-  float op[DK / ROW_BLOCK][DV];
-};
-
-// Halving combine of the per-wave partials of column col.
-template <int DK, int DV>
-__device__ __forceinline__ float combine_col(const float (&P)[DK / ROW_BLOCK][DV], int col) {
-  constexpr int NWV = DK / ROW_BLOCK;
-  float v[NWV];
-#pragma unroll
-  for (int p = 0; p < NWV; ++p) v[p] = P[p][col];
-#pragma unroll
-  for (int Lh = NWV / 2; Lh >= 1; Lh >>= 1) {
-#pragma unroll
-    for (int p = 0; p < Lh; ++p) v[p] = v[p] + v[p + Lh];
-  }
-  return v[0];
-}
-
-// One token of the gated delta rule on column-layout registers (eq. rule,
-// KDA erase/write): S' = a S; u = S'^T k; S = S' + (beta k)(v - u)^T;
-// o = S^T q.  Writes o to o_out (if non-null).  All threads must call.
-template <int DK, int DV, bool BF16>
-__device__ __forceinline__ void recur_token(float (&X)[ROW_BLOCK][DV / WAVE], const RowSmem<DK>& rs,
-                            RecSmem<DK, DV>& sm, const void* v, size_t v_off, float* o_out,
-                            bool erase, float* w_out = nullptr) {
-  constexpr int CPL = DV / WAVE;
-  static_assert(CPL <= 4, "columns per lane");
-  const int w = threadIdx.x / WAVE, lane = lane_id();
-  // row scalars of rows 32w + lane % 16 and 32w + 16 + lane % 16 (DPP sources)
-  const float2 ak0 = rs.ak[w * ROW_BLOCK + (lane & 15)], ak1 = rs.ak[w * ROW_BLOCK + 16 + (lane & 15)];
-  const float2 gq0 = rs.gq[w * ROW_BLOCK + (lane & 15)], gq1 = rs.gq[w * ROW_BLOCK + 16 + (lane & 15)];
-  float vin[CPL];   // this lane's columns of v, loaded before the row sweep
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) vin[c] = in_f32<BF16>(v, v_off + lane + WAVE * c);
-  float acc[CPL];
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
-  pass1_16<0, 0, CPL>(X, acc[0], ak0.x, ak0.y);
-  pass1_16<16, 0, CPL>(X, acc[0], ak1.x, ak1.y);
-  if constexpr (CPL > 1) {
-    pass1_16<0, 1, CPL>(X, acc[1], ak0.x, ak0.y);
-    pass1_16<16, 1, CPL>(X, acc[1], ak1.x, ak1.y);
-  }
-  if constexpr (CPL > 2) {
-    pass1_16<0, 2, CPL>(X, acc[2], ak0.x, ak0.y);
-    pass1_16<16, 2, CPL>(X, acc[2], ak1.x, ak1.y);
-    pass1_16<0, 3, CPL>(X, acc[3], ak0.x, ak0.y);
-    pass1_16<16, 3, CPL>(X, acc[3], ak1.x, ak1.y);
-  }
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) sm.up[w][lane + WAVE * c] = acc[c];
-  __syncthreads();
-  float wv[CPL];
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const int col = lane + WAVE * c;
-    const float u = combine_col<DK, DV>(sm.up, col);
-    wv[c] = erase ? vin[c] - u : vin[c];   // no erasure: w = v
-    acc[c] = 0.f;
-    if (w_out != nullptr && w == 0) w_out[col] = wv[c];
-  }
-  pass2_16<0, 0, CPL>(X, acc[0], gq0.x, gq0.y, wv[0]);
-  pass2_16<16, 0, CPL>(X, acc[0], gq1.x, gq1.y, wv[0]);
-  if constexpr (CPL > 1) {
-    pass2_16<0, 1, CPL>(X, acc[1], gq0.x, gq0.y, wv[1]);
-    pass2_16<16, 1, CPL>(X, acc[1], gq1.x, gq1.y, wv[1]);
-  }
-  if constexpr (CPL > 2) {
-    pass2_16<0, 2, CPL>(X, acc[2], gq0.x, gq0.y, wv[2]);
-    pass2_16<16, 2, CPL>(X, acc[2], gq1.x, gq1.y, wv[2]);
-    pass2_16<0, 3, CPL>(X, acc[3], gq0.x, gq0.y, wv[3]);
-    pass2_16<16, 3, CPL>(X, acc[3], gq1.x, gq1.y, wv[3]);
-  }
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) sm.op[w][lane + WAVE * c] = acc[c];
-  __syncthreads();
-  if (o_out != nullptr && w == 0) {
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      const int col = lane + WAVE * c;
-      o_out[col] = combine_col<DK, DV>(sm.op, col);
     }
   }
 }

@@ -52,6 +52,10 @@ hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st);
 // B*H heads.
 size_t chunk_record_bytes(int dk);
 int chunk_group(int nbh);
+// Head allocation units with block scales: a decode step (C = 1) and a
+// prefill with a write-back every C tokens.
+hipError_t launch_step_heads(KParams p, hipStream_t st);
+hipError_t launch_prefill_heads(KParams p, int C, hipStream_t st);
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st);
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,

@@ -76,3 +76,21 @@ def test_null_pointers_rejected_before_launch():
     assert lib.kda_weights_exact(ctypes.byref(wide.c()), 4, 1, one, one, one, one, one,
                                  one) == 3   # rejected before any launch
     assert lib.kda_status_str(3).decode() == "unsupported configuration"
+
+
+def test_head_unit_configs():
+    base = dict(B=1, H=16, d_k=256, d_v=256, group_rows=256, b_min=2, b_max=8, mean_bits=2.0,
+                decay_per_head=1, head_units=1)
+    from oracle import record as rec
+    assert K.record_bytes(K.Config(**base)) == rec.record_bytes_heads(256, 256, 8)
+    for kw in (dict(b_min=1), dict(b_max=9), dict(group_rows=64), dict(scope=1),
+               dict(mean_bits=1.5), dict(head_units=2)):
+        cfg = dict(base)
+        cfg.update(kw)
+        assert K.record_bytes(K.Config(**cfg)) == 0, kw
+    lib = K.load()
+    cfg = K.Config(**base)
+    one = ctypes.c_void_p(16)
+    assert lib.kda_pack_state(ctypes.byref(cfg.c()), one, one, one, one, 0, one, None) == 3
+    assert lib.kda_unpack_state(ctypes.byref(cfg.c()), one, one, None, None, None, None) == 3
+    assert lib.kda_alloc_bits(ctypes.byref(cfg.c()), one, one, one, one, None) == 3

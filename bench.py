@@ -61,13 +61,15 @@ def committed_traffic(kernel, workload):
     return e["hbm_bytes_per_launch"]
 
 
-def cpu_baseline(name, budget_s=12.0, warm_tokens=32):
+def cpu_baseline(name, budget_s=12.0, warm_tokens=32, head_units=False):
     """CPU oracle decode steps on one sequence (all its heads) for about
     budget_s seconds, after a short oracle warm-up of its own."""
     from oracle import step
     w = W.WORKLOADS[name]
+    if head_units:
+        w = W.sized(w, b_min=2, G=w.dk)
     oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
-                  erase=w.erase)
+                  erase=w.erase, unit="head" if head_units else "row")
     base = W.base_rates(w)
     xs = {n: [] for n in ("q", "k", "v", "s", "beta")}
     for t in range(warm_tokens):
@@ -321,7 +323,7 @@ def main():
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode",
-                    choices=["decode", "prefill", "mamba2", "weights"])
+                    choices=["decode", "prefill", "mamba2", "weights", "gdn2", "gdn6"])
     ap.add_argument("--layers", type=int, default=20)
     ap.add_argument("--warm-tokens", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -329,6 +331,8 @@ def main():
                     help="skip the untimed counting replay (e.g. under a profiler)")
     ap.add_argument("--no-ref32", action="store_true",
                     help="skip the 32-bit-mode reference step")
+    ap.add_argument("--head-units", action="store_true",
+                    help="decode workloads: one width per head with block scales")
     ap.add_argument("--chunked", action="store_true",
                     help="prefill workload: chunked (WY/UT) form on bf16 MFMA")
     args = ap.parse_args()
@@ -349,7 +353,10 @@ def main():
         run_weights(args, K, torch)
         return
     w = W.WORKLOADS[args.workload]
-    cfg = kcfg(K, w)
+    if args.head_units:
+        # one width per head, block scales: per-head normalisation, b_min = 2
+        w = W.sized(w, b_min=2, G=w.dk)
+    cfg = kcfg(K, w, head_units=int(args.head_units))
     ws = K.new_workspace(cfg)
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
     base = W.base_rates(w)
@@ -419,6 +426,8 @@ def main():
     # algorithmic HBM bytes of one step: records read and written (metadata
     # plus the budgeted code bits), inputs q, k, v, s, beta and outputs o
     meta = 16 + w.dk // 2 + 6 * w.dk
+    if args.head_units:
+        meta = 16 + 4 * w.dk + (w.dk // 32) * w.dv * 2   # rate codes, erase rates, block scales
     code_bytes = w.mean_bits * elems / 8
     s_elems = 1 if w.decay == "head" else w.dk
     io = w.B * w.H * (4 * (w.dk * 2 + s_elems + w.dv) + 4 + 4 * w.dv)   # q k s v beta, o
@@ -443,7 +452,7 @@ def main():
                     traffic=committed_traffic(dom, args.workload), kernel=dom)
 
     out = {
-        "metric": "state-tokens/s (B·H·T) and achieved HBM GB/s, KDA step w/ 4-bit mixed state",
+        "metric": f"state-tokens/s (B·H·T) and achieved HBM GB/s, KDA step w/ {w.mean_bits:g}-bit mixed state",
         "value": w.B * w.H / (ms * 1e-3),
         "unit": "state-tokens/s",
         "n_gpus": 1,
@@ -460,8 +469,10 @@ def main():
                                f"{w.mean_bits} bits, widths [{w.b_min},{w.b_max}], groups of "
                                f"{w.G} rows, layer budget, "
                                f"{'per-head' if w.decay == 'head' else 'per-channel'} decay, "
-                               f"{'KDA erase' if w.erase else 'no erasure'}, prior state after "
-                               f"{args.warm_tokens} warm-up decode tokens",
+                               f"{'KDA erase' if w.erase else 'no erasure'}, "
+                               + ("head units (one width per head, FP16 scales per 32 rows "
+                                  "of a column), " if args.head_units else "")
+                               + f"prior state after {args.warm_tokens} warm-up decode tokens",
                    "layers_rotated": L},
         "hbm_GBps_step": hbm,
         "hbm_frac_step": hbm / HBM_PEAK_GBPS,
@@ -474,7 +485,7 @@ def main():
         del layers
         out["state32_reference"] = run_state32_reference(w, args, K, torch)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload)
+        out["cpu_baseline"] = cpu_baseline(args.workload, head_units=args.head_units)
     print(json.dumps(out), flush=True)
 
 

@@ -10,6 +10,9 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
   row order in float64 (each R_j^2 is exact); RMS = sqrt(sum / G); a group with
   RMS 0 gives R~ = 0.
 * ``weights``: c_i = Gamma_i * (R~_i * R~_i)  (eq. weight).
+* ``mode_weights``: the key for the ablated weight variants: R~^2 for the
+  normalised modes, raw R^2 for "range" and "gamma_raw", 1 for "uniform"
+  (the rows' factors from ``stats.mode_gamma``).
 * ``allocate``: minimise the high-rate proxy sum_i c_i 2^(-2 b_i) over integer
   widths in [b_min, b_max] with sum b_i = K = round(mean_bits * N) (Sec. 3:
   round, clip and adjust to the layer budget).  Written as its greedy
@@ -65,6 +68,17 @@ def normalized_ranges(R, G):
 def weights(gamma, Rt):
     Rt = np.asarray(Rt, F64)
     return np.asarray(gamma, F64) * (Rt * Rt)
+
+
+def mode_weights(gamma, R, Rt, mode="ema"):
+    """gamma: row factors; R: float32 row maxima; Rt: normalised ranges."""
+    gamma = np.asarray(gamma, F64)
+    if mode == "uniform":
+        return np.ones_like(gamma)
+    if mode in ("range", "gamma_raw"):
+        Rr = np.asarray(R, np.float32).astype(F64)
+        return gamma * (Rr * Rr)
+    return weights(gamma, Rt)
 
 
 def allocate(c, mean_bits, b_min, b_max):

@@ -15,6 +15,14 @@ through one may differ in the last float64 bit.
   interval C sees the same estimates.  s_hat = -log(m)/2, r = e/2.
 * ``gamma_hat``: eq. weight, 1 / expm1(2 (s_hat + r)), with s_hat + r clamped
   below at 1e-12 (the paper requires s > 0).
+* ``mode_gamma``: the row factor of the allocation key for the weight
+  variants the paper ablates (Sec. 5, Table ablate): "ema" (ours, eq.
+  weight), "gamma_raw" (the same factor, raw ranges), "range" and
+  "rel_range" and "uniform" (factor 1), "persist" (DAMP's uncapped
+  persistence w^(1) = 1/(1 - a^2) with a = exp(-s_hat), Related work),
+  "writeback" (h^(C) = 1/(1 - exp(-2 C s_hat)), Choice of persistence
+  factor), "no_erase_rate" (eq. weight with r = 0).  Rates are clamped below
+  at 1e-12 as in gamma_hat.
 * ``window_gamma``: eq. gram restricted to a window of W tokens with the
   diagonal erase approximation of Sec. 2 (Approximate erasure rate): per row,
   lambda_t = exp(-2 s_t - beta_t (2 - beta_t) k_t^2)  (no erase term
@@ -83,6 +91,24 @@ def ema_rates(m, e):
 def gamma_hat(s_hat, r):
     t = np.maximum(np.asarray(s_hat, F64) + np.asarray(r, F64), GAMMA_FLOOR)
     return F64(1.0) / np.expm1(F64(2.0) * t)
+
+
+WEIGHT_MODES = ("ema", "range", "gamma_raw", "rel_range", "persist", "writeback",
+                "no_erase_rate", "uniform")
+
+
+def mode_gamma(s_hat, r, mode="ema", C=1):
+    s_hat = np.asarray(s_hat, F64)
+    if mode in ("ema", "gamma_raw"):
+        return gamma_hat(s_hat, r)
+    if mode == "no_erase_rate":
+        return gamma_hat(s_hat, np.zeros_like(s_hat))
+    if mode == "persist":
+        return F64(1.0) / -np.expm1(F64(-2.0) * np.maximum(s_hat, GAMMA_FLOOR))
+    if mode == "writeback":
+        return F64(1.0) / -np.expm1((F64(-2.0) * F64(C)) * np.maximum(s_hat, GAMMA_FLOOR))
+    assert mode in ("range", "rel_range", "uniform"), mode
+    return np.ones_like(s_hat)
 
 
 def logq_encode(s_hat):

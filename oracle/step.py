@@ -49,6 +49,7 @@ class Cfg:
     span: int = 64
     erase: bool = True              # False: no erasure (Mamba-2)
     unit: str = "row"               # "row" (a width per row) or "head" (block scales)
+    weight: str = "ema"             # allocation key variant (stats.WEIGHT_MODES)
 
 
 def zero_state(B, H, cfg):
@@ -97,12 +98,13 @@ def allocate_widths(c, cfg):
     return out
 
 
-def write_back_heads(S, m, e, ntok, cfg, gamma=None):
+def write_back_heads(S, m, e, ntok, cfg, gamma=None, C=1):
     """Head units: one width per head from the mean Gamma of its rows, block
     scales.  Same arguments and results as write_back."""
     B, H, dk, dv = S.shape
     s_hat, r = stats.ema_rates(m, e)
-    g = stats.gamma_hat(s_hat, r) if gamma is None else np.asarray(gamma, F64)
+    g = (stats.mode_gamma(s_hat, r, cfg.weight, C) if gamma is None
+         else np.asarray(gamma, F64))
     ch = alloc.head_weights(g)
     width = np.stack([alloc.allocate(ch[b], cfg.mean_bits, cfg.b_min, cfg.b_max)
                       for b in range(B)])
@@ -119,20 +121,22 @@ def write_back_heads(S, m, e, ntok, cfg, gamma=None):
     return state, diag
 
 
-def write_back(S, m, e, ntok, cfg, gamma=None):
-    """Quantise float32 S [B,H,dk,dv] with EMA states m, e -> (state, diag)."""
+def write_back(S, m, e, ntok, cfg, gamma=None, C=1):
+    """Quantise float32 S [B,H,dk,dv] with EMA states m, e -> (state, diag).
+    C is the write-back interval (used by the "writeback" weight variant)."""
     if cfg.unit == "head":
-        return write_back_heads(S, m, e, ntok, cfg, gamma)
+        return write_back_heads(S, m, e, ntok, cfg, gamma, C)
     B, H, dk, dv = S.shape
     s_hat, r = stats.ema_rates(m, e)
-    g = stats.gamma_hat(s_hat, r) if gamma is None else np.asarray(gamma, F64)
+    g = (stats.mode_gamma(s_hat, r, cfg.weight, C) if gamma is None
+         else np.asarray(gamma, F64))
     R = np.max(np.abs(S), axis=-1).astype(F32)
     if cfg.G <= dk:
         Rt = alloc.normalized_ranges(R, cfg.G)
     else:
         # groups of G rows across consecutive heads of a sequence
         Rt = alloc.normalized_ranges(R.reshape(B, H * dk), cfg.G).reshape(B, H, dk)
-    c = alloc.weights(g, Rt)
+    c = alloc.mode_weights(g, R, Rt, cfg.weight)
     widths = allocate_widths(c, cfg)
     codes, scale, mstar = quant.quantize_rows(S.reshape(-1, dv), widths.reshape(-1))
     state = dict(ntok=np.asarray(ntok, np.int64), widths=widths,
@@ -185,7 +189,7 @@ def mirror_prefill(state, q, k, v, s, beta, C, cfg, gamma=None):
         if (t + 1) % C == 0 or t == T - 1:
             ntok = ntok + since
             since = 0
-            state, diag = write_back(X, m, e, ntok, cfg, gamma)
+            state, diag = write_back(X, m, e, ntok, cfg, gamma, C)
             diags.append(diag)
             X = dequantize(state)
             m, e = ema_start(state)

@@ -62,6 +62,24 @@ typedef enum {
 enum { KDA_SCOPE_SEQUENCE = 0, KDA_SCOPE_HEAD = 1 };
 
 /* Problem and quantiser configuration (host memory, plain old data). */
+/* Allocation-key variants (Sec. 5, Table ablate).  Gamma^ = 1/expm1(2 (s^ +
+ * r)) (eq. weight), R~ the normalised range, R the raw row maximum, rates
+ * clamped below at 1e-12; given weights (`gamma` arguments) replace the
+ * factor in front of the range term. */
+typedef enum {
+  KDA_WEIGHT_EMA = 0,           /* Gamma^ R~^2 (the paper's method)            */
+  KDA_WEIGHT_RANGE = 1,         /* R^2 (range alone)                           */
+  KDA_WEIGHT_GAMMA_RANGE = 2,   /* Gamma^ R^2 (raw range)                      */
+  KDA_WEIGHT_REL_RANGE = 3,     /* R~^2 (relative range)                       */
+  KDA_WEIGHT_PERSISTENCE = 4,   /* w1 R~^2, w1 = 1/(1 - exp(-2 s^)) (DAMP's
+                                   uncapped persistence, Related work)        */
+  KDA_WEIGHT_WRITEBACK = 5,     /* h R~^2, h = 1/(1 - exp(-2 C s^)) with C the
+                                   write-back interval (1 for kda_step)        */
+  KDA_WEIGHT_NO_ERASE_RATE = 6, /* Gamma^ with r = 0, times R~^2              */
+  KDA_WEIGHT_UNIFORM = 7        /* equal keys: uniform widths (the remainder
+                                   of the budget to the lowest rows)          */
+} kda_weight_mode;
+
 typedef struct {
   int32_t B;              /* sequences                                        */
   int32_t H;              /* heads per layer                                  */
@@ -108,6 +126,11 @@ typedef struct {
                              [d_k]; block scales FP16 [d_k/32][d_v]; at the
                              next multiple of 256 the code words as below
                              with every row of width b (row i at bit i b). */
+  int32_t weight_mode;    /* allocation key (Sec. 5, Table ablate), a
+                             kda_weight_mode; KDA_WEIGHT_EMA (0) is the
+                             paper's method.  With head_units only the modes
+                             that need no ranges (EMA, PERSISTENCE,
+                             WRITEBACK, NO_ERASE_RATE, UNIFORM).            */
 } kda_config;
 
 /* Bytes of one (sequence, head) record slot; 0 if the config is invalid.

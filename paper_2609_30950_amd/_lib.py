@@ -18,6 +18,7 @@ class kda_config(ctypes.Structure):
         ("ema_span", ctypes.c_int32), ("decay_per_head", ctypes.c_int32),
         ("state32", ctypes.c_int32), ("no_erase", ctypes.c_int32),
         ("chunked", ctypes.c_int32), ("head_units", ctypes.c_int32),
+        ("weight_mode", ctypes.c_int32),
     ]
 
 

@@ -28,12 +28,13 @@ class Config:
     no_erase: int = 0          # 1: Mamba-2 style recurrence without erasure
     chunked: int = 0           # 1: chunked (WY/UT) prefill on MFMA
     head_units: int = 0        # 1: one width per head, block scales (Gated DeltaNet)
+    weight_mode: int = 0       # allocation key variant (WEIGHT_MODES)
 
     def c(self):
         return kda_config(self.B, self.H, self.d_k, self.d_v, self.group_rows, self.scope,
                           float(self.mean_bits), self.b_min, self.b_max, self.ema_span,
                           self.decay_per_head, self.state32, self.no_erase,
-                          self.chunked, self.head_units)
+                          self.chunked, self.head_units, self.weight_mode)
 
 
 def _ptr(t, dtype=None, numel=None, name="tensor"):
@@ -176,6 +177,10 @@ def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None):
         _ptr(o, torch.float32, cfg.B * T * cfg.H * cfg.d_v, "o"), _ptr(ws, torch.uint8, None, "ws"),
         _stream()))
 
+
+# kda_weight_mode values, in the order of the oracle's stats.WEIGHT_MODES
+WEIGHT_MODES = ("ema", "range", "gamma_raw", "rel_range", "persist", "writeback",
+                "no_erase_rate", "uniform")
 
 PROFILE_EVENTS = 1
 PROFILE_COUNTERS = 2

@@ -53,6 +53,12 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg->chunked != 0 && cfg->chunked != 1) return KDA_ERR_ARG;
   if (cfg->chunked && (cfg->d_k > 128 || cfg->state32)) return KDA_ERR_UNSUPPORTED;
   if (cfg->head_units != 0 && cfg->head_units != 1) return KDA_ERR_ARG;
+  if (cfg->weight_mode < KDA_WEIGHT_EMA || cfg->weight_mode > KDA_WEIGHT_UNIFORM) return KDA_ERR_ARG;
+  // head widths come from the statistics alone (R~ = 1): no range variants
+  if (cfg->head_units && (cfg->weight_mode == KDA_WEIGHT_RANGE ||
+                          cfg->weight_mode == KDA_WEIGHT_GAMMA_RANGE ||
+                          cfg->weight_mode == KDA_WEIGHT_REL_RANGE))
+    return KDA_ERR_UNSUPPORTED;
   if (cfg->head_units) {
     // one width per head, block scales: per-head normalisation, the layer
     // budget over the heads of a sequence, widths 2..8
@@ -106,6 +112,8 @@ KParams make_params(const kda_config* cfg, int need) {
   p.per_head = cfg->decay_per_head;
   p.state32 = cfg->state32;
   p.no_erase = cfg->no_erase;
+  p.weight_mode = cfg->weight_mode;
+  p.wb_C = 1;
   p.need = need;
   p.alpha = 2.0 / (double)(cfg->ema_span + 1);
   p.one_minus_alpha = 1.0 - p.alpha;
@@ -309,6 +317,7 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, cons
   p.o = o;
   p.T = T;
   p.in_bf16 = 1;
+  p.wb_C = C;
   if (!cfg->state32) set_ws(p, cfg, ws);
   if (cfg->chunked) {
     if (C > 64) return KDA_ERR_ARG;

@@ -653,7 +653,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     const double e_run = P * e0 + ema[DK + t];
     const double s_hat = -0.5 * log(m_run);
     const double r = 0.5 * e_run;
-    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
 }

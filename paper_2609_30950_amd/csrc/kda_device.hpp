@@ -215,4 +215,38 @@ __device__ __forceinline__ double gamma_hat(double s_hat, double r) {
   return 1.0 / expm1(2.0 * t);
 }
 
+// Allocation-key variants of the weight ablations (Sec. 5, Table ablate);
+// the values of kda_config.weight_mode.
+enum WeightMode {
+  WM_EMA = 0,            // Gamma^ R~^2 (eq. weight)
+  WM_RANGE = 1,          // R^2, raw range alone
+  WM_GAMMA_RAW = 2,      // Gamma^ R^2
+  WM_REL_RANGE = 3,      // R~^2
+  WM_PERSIST = 4,        // w^(1) R~^2, w^(1) = 1/(1 - exp(-2 s^)) (DAMP, uncapped)
+  WM_WRITEBACK = 5,      // h^(C) R~^2, h^(C) = 1/(1 - exp(-2 C s^))
+  WM_NO_ERASE_RATE = 6,  // Gamma^ with r = 0, times R~^2
+  WM_UNIFORM = 7,        // equal keys: uniform widths
+};
+
+// Row factor of the key; rates clamped below at 1e-12 as in gamma_hat.
+__device__ __forceinline__ double mode_gamma(int mode, double s_hat, double r, int C) {
+  if (mode == WM_EMA || mode == WM_GAMMA_RAW) return gamma_hat(s_hat, r);
+  if (mode == WM_NO_ERASE_RATE) return gamma_hat(s_hat, 0.0);
+  const double s = s_hat < 1e-12 ? 1e-12 : s_hat;
+  if (mode == WM_PERSIST) return 1.0 / -expm1(-2.0 * s);
+  if (mode == WM_WRITEBACK) return 1.0 / -expm1((-2.0 * (double)C) * s);
+  return 1.0;   // range, relative range, uniform
+}
+
+// Key c of a row from its factor, row maximum and group RMS.
+__device__ __forceinline__ double mode_key(int mode, double gam, float R, double rms) {
+  if (mode == WM_UNIFORM) return 1.0;
+  if (mode == WM_RANGE || mode == WM_GAMMA_RAW) {
+    const double Rr = (double)R;
+    return gam * (Rr * Rr);
+  }
+  const double Rt = rms > 0.0 ? (double)R / rms : 0.0;
+  return gam * (Rt * Rt);
+}
+
 }  // namespace kda

@@ -88,7 +88,7 @@ __global__ void __launch_bounds__(DK) k_head_weights(KParams p) {
   }
   const double s_hat = -0.5 * log(m_run);
   const double r = 0.5 * e_run;
-  gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+  gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
   p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   __syncthreads();
   if (t == 0) {

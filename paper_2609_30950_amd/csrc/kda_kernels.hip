@@ -416,7 +416,7 @@ __device__ __forceinline__ void row_rates(const KParams& p, int bh, StatSmem<DK>
   if (t < DK) {
     const double s_hat = -0.5 * log(m_run);
     const double r = 0.5 * e_run;
-    st.gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    st.gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
 }
@@ -448,9 +448,7 @@ __device__ __forceinline__ void row_weights(const KParams& p, int bh, StatSmem<D
   }
   __syncthreads();
   if (t < DK) {
-    const double rms = st.rms[t / p.G];
-    const double Rt = rms > 0.0 ? (double)st.R[t] / rms : 0.0;
-    const double c = st.gam[t] * (Rt * Rt);
+    const double c = mode_key(p.weight_mode, st.gam[t], st.R[t], st.rms[t / p.G]);
     st.c[t] = c;
     p.ws_c[(size_t)bh * DK + t] = c;
   }
@@ -1065,7 +1063,7 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
   if (ema_here) {
     const double s_hat = -0.5 * log(m_run);
     const double r = 0.5 * e_run;
-    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
 }
@@ -1284,7 +1282,7 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_cols(KParams p) {
   if (ema_here) {
     const double s_hat = -0.5 * log(m_run);
     const double r = 0.5 * e_run;
-    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : gamma_hat(s_hat, r);
+    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
 }
@@ -1331,9 +1329,7 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
   }
   __syncthreads();
   for (int n = tid; n < N; n += nt) {
-    const double rm = rms[n / G];
-    const double Rt = rm > 0.0 ? (double)R[n] / rm : 0.0;
-    c[n] = gam[row0 + n] * (Rt * Rt);
+    c[n] = mode_key(p.weight_mode, gam[row0 + n], R[n], rms[n / G]);
   }
   __syncthreads();
   block_allocate<ALLOC_MAX_N / 1024>([&](int n) { return c[n]; }, N, p.need, p.bmin, p.bmax,

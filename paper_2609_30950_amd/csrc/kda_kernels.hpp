@@ -12,6 +12,8 @@ namespace kda {
 struct KParams {
   int B, H, dk, dv, G, scope, bmin, bmax, per_head, state32;
   int no_erase;             // 1: no erasure (w = v, no erase statistic)
+  int weight_mode;          // allocation-key variant (WeightMode)
+  int wb_C;                 // write-back interval of the call (weight variant h^(C))
   int need;                 // granted slots per scope unit: K - N * b_min
   double alpha, one_minus_alpha;
   Layout L;

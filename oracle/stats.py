@@ -34,6 +34,9 @@ through one may differ in the last float64 bit.
   O = F^T (Q + O) F for a constant transition); for pins only.
 * ``logq_encode`` / ``logq_decode``: rates coded with levels uniform in
   log s (Sec. 3, Decay-gate quantization), 16 bits over [2^-20, 2^5].
+* ``gate_quantize``: per-token gate quantisation with 2^b levels uniform in
+  log s (or, for comparison, in g = -s) over the range of a head's channels
+  at that token (Sec. 3, Decay-gate quantization).
 
 Parity: pinned (P5 closed form, P6 worked example, P7 fixed-key series, P8
 bound, P17 codes, P18 EMA) in ``tests/test_oracle_stats.py``.
@@ -190,3 +193,27 @@ def stationary_gamma(F, Q, C=1):
     from scipy.linalg import solve_discrete_lyapunov
     O = solve_discrete_lyapunov(F.T, F.T @ Q @ F)
     return np.diag(O) / C
+
+
+def gate_quantize(s, bits, mode="log"):
+    """Per-token decay-gate quantisation (Sec. 3, Decay-gate quantization):
+    s [..., dk] float32 rates of one token and head; levels uniform in log s
+    (mode "log") or in g = -s (mode "linear") over the range of the head's
+    channels at that token; 2^bits levels, nearest level (ties to even).
+    float64 arithmetic; returns the dequantised rates as float32.
+
+        x = log(s) (or s), lo = min x, hi = max x over the channels,
+        n = 2^bits - 1, step = (hi - lo) / n,
+        code = clamp(rne((x - lo) / step), 0, n)  (0 when step = 0),
+        x^ = lo + code step, s^ = fl32(exp(x^)) (or fl32(x^)).
+    """
+    s = np.asarray(s, F32).astype(F64)
+    x = np.log(s) if mode == "log" else s
+    lo = np.min(x, axis=-1, keepdims=True)
+    hi = np.max(x, axis=-1, keepdims=True)
+    n = F64((1 << bits) - 1)
+    step = (hi - lo) / n
+    with np.errstate(divide="ignore", invalid="ignore"):
+        code = np.where(step > 0, np.clip(np.rint((x - lo) / step), 0, n), 0.0)
+    xh = lo + code * step
+    return (np.exp(xh) if mode == "log" else xh).astype(F32)

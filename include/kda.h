@@ -238,6 +238,20 @@ int kda_step_outputs(const kda_config* cfg, void* records, const float* q,
                      void* stream);
 int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* stream);
 
+/* Per-token decay-gate quantisation (Sec. 3, Decay-gate quantization): for
+ * every (sequence, token, head), the d_k rates are coded with 2^bits levels
+ * uniform in log s (KDA_GATES_LOG) or in g = -s (KDA_GATES_LINEAR, the
+ * comparison of that passage) over the range of the head's channels at that
+ * token, and replaced by their dequantised values (float64 arithmetic:
+ * x = log s or s, step = (max x - min x) / (2^bits - 1), code =
+ * clamp(rne((x - min x) / step), 0, 2^bits - 1), x^ = min x + code step).
+ * In: s [B][T][H][d_k] f32 (per-row decay; decay_per_head is unsupported),
+ * 1 <= bits <= 16.  Out: s_out, same layout (may equal s).  The quantised
+ * gates feed kda_prefill / kda_step like any rates. */
+enum { KDA_GATES_LOG = 0, KDA_GATES_LINEAR = 1 };
+int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode, const float* s,
+                   float* s_out, void* stream);
+
 /* Prefill of T tokens with a write-back after every C-th token and after the
  * last one (Sec. 2: once per prefill chunk).  With cfg->chunked, C must be
  * at most 64 (KDA_ERR_ARG otherwise) and the workspace (kda_workspace_bytes

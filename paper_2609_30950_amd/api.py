@@ -182,6 +182,14 @@ def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None):
 WEIGHT_MODES = ("ema", "range", "gamma_raw", "rel_range", "persist", "writeback",
                 "no_erase_rate", "uniform")
 
+def kda_gate_quant(cfg, T, bits, s, s_out, mode="log"):
+    """Per-token decay-gate quantisation; mode "log" or "linear"."""
+    n = cfg.B * T * cfg.H * cfg.d_k
+    _check(load().kda_gate_quant(
+        ctypes.byref(cfg.c()), int(T), int(bits), 0 if mode == "log" else 1,
+        _ptr(s, torch.float32, n, "s"), _ptr(s_out, torch.float32, n, "s_out"), _stream()))
+
+
 PROFILE_EVENTS = 1
 PROFILE_COUNTERS = 2
 

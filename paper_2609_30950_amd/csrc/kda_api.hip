@@ -296,6 +296,23 @@ int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* str
   return hip_status(kda::launch_step_writeback(p, (hipStream_t)stream));
 }
 
+int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode, const float* s,
+                   float* s_out, void* stream) {
+  if (cfg == nullptr) return KDA_ERR_ARG;
+  if (cfg->B < 1 || cfg->H < 1 || T < 1) return KDA_ERR_SHAPE;
+  if (cfg->d_k != 64 && cfg->d_k != 128 && cfg->d_k != 256) return KDA_ERR_UNSUPPORTED;
+  if (cfg->decay_per_head) return KDA_ERR_UNSUPPORTED;
+  if (bits < 1 || bits > 16 || (mode != KDA_GATES_LOG && mode != KDA_GATES_LINEAR)) return KDA_ERR_ARG;
+  if (!s || !s_out) return KDA_ERR_ARG;
+  KParams p;
+  std::memset(&p, 0, sizeof(p));
+  p.B = cfg->B;
+  p.H = cfg->H;
+  p.dk = cfg->d_k;
+  return hip_status(kda::launch_gate_quant(p, T, bits, mode == KDA_GATES_LINEAR, s, s_out,
+                                           (hipStream_t)stream));
+}
+
 int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, const uint16_t* q,
                 const uint16_t* k, const uint16_t* v, const float* s, const float* beta,
                 const double* gamma, float* o, void* ws, void* stream) {

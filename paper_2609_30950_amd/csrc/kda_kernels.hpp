@@ -58,6 +58,9 @@ int chunk_group(int nbh);
 // prefill with a write-back every C tokens.
 hipError_t launch_step_heads(KParams p, hipStream_t st);
 hipError_t launch_prefill_heads(KParams p, int C, hipStream_t st);
+// Per-token decay-gate quantisation of s [B][T][H][d_k] into out.
+hipError_t launch_gate_quant(const KParams& p, int T, int bits, int linear, const float* s,
+                             float* out, hipStream_t st);
 hipError_t launch_pack(const KParams& p, const float* S, const uint8_t* bits, const double* s_hat,
                        const double* r, unsigned ntok, hipStream_t st);
 hipError_t launch_unpack(const KParams& p, float* S, uint8_t* bits, double* s_hat, double* r,

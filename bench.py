@@ -331,6 +331,8 @@ def main():
                     help="skip the untimed counting replay (e.g. under a profiler)")
     ap.add_argument("--no-ref32", action="store_true",
                     help="skip the 32-bit-mode reference step")
+    ap.add_argument("--graph", action="store_true",
+                    help="decode workloads: also time the steps replayed from one HIP graph")
     ap.add_argument("--head-units", action="store_true",
                     help="decode workloads: one width per head with block scales")
     ap.add_argument("--chunked", action="store_true",
@@ -407,6 +409,29 @@ def main():
     # pass B: the same steps from the same records without events -> value
     layers.copy_(snapshot)
     ms = timed()
+    ms_graph = None
+    if args.graph:
+        # pass G: the same steps captured in one HIP graph and replayed
+        layers.copy_(snapshot)
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            run(args.warmup)                   # warm-up launch outside the capture
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        layers.copy_(snapshot)
+        with torch.cuda.graph(g):
+            for i in range(args.warmup, n_tok):
+                run(i)
+        torch.cuda.synchronize()
+        layers.copy_(snapshot)
+        ev0.record()
+        g.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        ms_graph = ev0.elapsed_time(ev1) / args.steps
+        del g
     # pass C (untimed): the same launches once more with the quantiser's
     # evaluation counter on, for the algorithmic work of pass A's launches
     fit_evals = None
@@ -460,6 +485,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms,
         "ms_per_step_with_kernel_events": ms_events,
+        "ms_per_step_hip_graph": ms_graph,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

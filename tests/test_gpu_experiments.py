@@ -1,9 +1,13 @@
-"""The paper's synthetic claim on the erase approximation (Sec. 2, Approximate
-erasure rate), run on the library's entry points (kda_weights,
-kda_weights_exact, kda_alloc_bits): with diverse keys the diagonal
-approximation's allocation stays within 3 % of the exact-Gramian allocation's
-distortion; with a persistent key it is clearly worse (errors orthogonal to a
-repeated key are never erased)."""
+"""The paper's synthetic claims run on the library's entry points.
+
+* Erase approximation (Sec. 2, Approximate erasure rate; kda_weights,
+  kda_weights_exact, kda_alloc_bits): with diverse keys the diagonal
+  approximation's allocation stays within 3 % of the exact-Gramian
+  allocation's distortion; with a persistent key it is clearly worse (errors
+  orthogonal to a repeated key are never erased).
+* Readout error (Sec. 3, State bit allocation; kda_prefill in 32-bit and
+  quantised modes, kda_weights_exact): the EMA weights come within a few
+  percent of exact-Gramian allocation, and both beat uniform widths."""
 import numpy as np
 import pytest
 
@@ -23,3 +27,11 @@ def test_erase_approximation_diverse_vs_persistent_keys():
     assert np.all(div >= -1e-12) and np.all(per >= -1e-12)   # the exact allocation is optimal
     assert div.max() <= 0.03
     assert per.mean() > 5 * div.mean() and per.max() > 0.05
+
+
+def test_readout_error_ema_vs_exact_and_uniform():
+    e_ema, e_ex, e_uni = experiments.readout_error(heads=16, tokens=512, C=16, mean_bits=3.0)
+    say(f"readout error: ema {e_ema:.5f} exact {e_ex:.5f} uniform {e_uni:.5f}")
+    assert 0 < e_ex and 0 < e_ema
+    assert abs(e_ema / e_ex - 1) <= 0.05
+    assert e_ema < 0.8 * e_uni and e_ex < 0.8 * e_uni

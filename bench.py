@@ -323,7 +323,7 @@ def main():
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode",
-                    choices=["decode", "prefill", "mamba2", "weights", "gdn2", "gdn6"])
+                    choices=["decode", "prefill", "mamba2", "weights", "gdn2", "gdn6", "long"])
     ap.add_argument("--layers", type=int, default=20)
     ap.add_argument("--warm-tokens", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -30,7 +30,7 @@ import workloads as W  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
 # 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz: one VALU lane-op per lane per clock
-# (packed float32 issue is not used: it is disabled in this build)
+# (packed float32 issue is not used: the library is compiled without it)
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 # Algorithmic lane-ops of the requantisation kernel: every evaluated clip
 # factor costs 5 per element of its 64-column row segment (scale, round,
@@ -339,8 +339,8 @@ def main():
                     help="prefill workload: chunked (WY/UT) form on bf16 MFMA")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(sequences shard across GPUs without communication; see DESIGN.md)",
+        print("bench.py measures one GPU: the library has no multi-GPU path "
+              "(sequences shard across GPUs without communication)",
               file=sys.stderr)
         sys.exit(2)
 

@@ -54,7 +54,7 @@ typedef enum {
   KDA_OK = 0,
   KDA_ERR_ARG = 1,          /* bad pointer, size or numeric parameter        */
   KDA_ERR_SHAPE = 2,        /* unsupported or inconsistent shape             */
-  KDA_ERR_UNSUPPORTED = 3,  /* valid request this build does not implement   */
+  KDA_ERR_UNSUPPORTED = 3,  /* valid request the library does not implement   */
   KDA_ERR_WORKSPACE = 4,    /* workspace pointer missing                     */
   KDA_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed    */
 } kda_status;

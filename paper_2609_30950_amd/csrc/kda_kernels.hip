@@ -706,32 +706,54 @@ k_requant(KParams p) {
   requant_head<DK, DV, COMPACT, CodeTile<C8>>(p, blockIdx.x, sm);
 }
 
-// Unquantised ("32-bit") state: load, one token, store.
-template <int DK, int DV, bool BF16>
+// Buffer resource over n bytes at base (word 3 of a gfx9 resource: untyped
+// 32-bit data); loads past n return 0 and stores past n are dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(void* base, int n) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, n, 0x00020000);
+}
+constexpr int BUF_NT = 2;   // cache policy of a buffer access: nontemporal
+
+// Unquantised ("32-bit") state: load, the interval's tokens, store.  Columns
+// are independent in the recurrence, so a block takes one 64-column slice of a
+// head (blockIdx.x = head * slices + slice): 32 state values per lane keep the
+// register count low enough for eight waves per SIMD, and the grid holds
+// twice as many, half-sized blocks, which keeps more of the state streaming.
+template <int DK, int DV, bool BF16, bool ONE>
 __global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
-  constexpr int CPL = DV / WAVE;
-  const int bh = blockIdx.x;
+  constexpr int NSL = DV / SLICE;
+  const int bh = blockIdx.x / NSL, col0 = (blockIdx.x % NSL) * SLICE;
   const int b = bh / p.H, h = bh % p.H;
   const int w = threadIdx.x / WAVE, lane = lane_id();
-  float* S = (float*)((uint8_t*)p.records + (long long)bh * DK * DV * 4);
+  // buffer addressing: the head's state as one resource, the lane's column as
+  // the only vector offset, the wave's row as a scalar one (plain 64-bit
+  // addresses cost two registers per row in flight)
+  const __amdgpu_buffer_rsrc_t S =
+      buf_rsrc((uint8_t*)p.records + (long long)bh * DK * DV * 4, DK * DV * 4);
+  const int voff = (col0 + lane) * 4;
+  const int soff = __builtin_amdgcn_readfirstlane(w) * ROW_BLOCK * DV * 4;
   __shared__ RowSmem<DK> rs;
-  __shared__ RecSmem<DK, DV> rsm;
-  float X[ROW_BLOCK][CPL];
-#pragma unroll
-  for (int r = 0; r < ROW_BLOCK; ++r)
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) X[r][c] = S[(w * ROW_BLOCK + r) * DV + lane + WAVE * c];
-  for (int j = 0; j < p.ntk; ++j) {
+  __shared__ RecSmem<DK, SLICE> rsm;
+  float X[ROW_BLOCK][1];
+  for (int j = 0; j < (ONE ? 1 : p.ntk); ++j) {
     const int tok = p.tok0 + j;
     load_rows<DK, BF16>(rs, p, bh, tok);
+    // first token: the state is loaded after the row scalars, so that the
+    // registers of their float64 exponentials are free again
+    if (j == 0) {
+#pragma unroll
+      for (int r = 0; r < ROW_BLOCK; ++r)
+        X[r][0] = __uint_as_float(
+            __builtin_amdgcn_raw_buffer_load_b32(S, voff, soff + r * DV * 4, BUF_NT));
+    }
     __syncthreads();
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV, BF16>(X, rs, rsm, p.v, th * DV, p.o + th * DV, !p.no_erase);
+    recur_token<DK, SLICE, BF16>(X, rs, rsm, p.v, th * DV + col0, p.o + th * DV + col0,
+                                 !p.no_erase);
   }
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r)
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) S[(w * ROW_BLOCK + r) * DV + lane + WAVE * c] = X[r][c];
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(X[r][0]), S, voff, soff + r * DV * 4,
+                                          BUF_NT);
 }
 
 // Standalone codec: quantise given states.
@@ -1345,8 +1367,12 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases
   const int nbh = p.B * p.H;
   if (p.state32) {
     if (!(phases & 1)) return hipSuccess;
-    if (p.in_bf16) return launch("step32", k_step32<DK, DV, true>, nbh, 2 * DK, 0, st, p);
-    return launch("step32", k_step32<DK, DV, false>, nbh, 2 * DK, 0, st, p);
+    const int nblk = nbh * (DV / SLICE);
+    if (p.ntk == 1)
+      return p.in_bf16 ? launch("step32", k_step32<DK, DV, true, true>, nblk, 2 * DK, 0, st, p)
+                       : launch("step32", k_step32<DK, DV, false, true>, nblk, 2 * DK, 0, st, p);
+    return p.in_bf16 ? launch("step32", k_step32<DK, DV, true, false>, nblk, 2 * DK, 0, st, p)
+                     : launch("step32", k_step32<DK, DV, false, false>, nblk, 2 * DK, 0, st, p);
   }
   hipError_t e = hipSuccess;
   if (phases & 1) {

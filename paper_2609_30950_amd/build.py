@@ -10,7 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkda.so")
-SOURCES = ["kda_api.hip", "kda_kernels.hip", "kda_chunked.hip", "kda_heads.hip", "kda_gates.hip", "kda_profile.hip"]
+SOURCES = ["kda_api.hip", "kda_kernels.hip", "kda_chunked.hip", "kda_heads.hip", "kda_gates.hip", "kda_gramian.hip",
+           "kda_profile.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -122,10 +122,19 @@ def run_state32_reference(w, args, K, torch):
     ms = ev0.elapsed_time(ev1) / args.steps
     nbh = w.B * w.H
     step_bytes = nbh * (2 * w.dk * w.dv * 4 + 4 * (3 * w.dk + w.dv) + 4 + 4 * w.dv)
+    # context: torch's device copy of the same state bytes (read + write), same rotation
+    half = layers.shape[1] // 2
+    ev0.record()
+    for i in range(args.steps):
+        layers[i % L, half:].copy_(layers[(i + 1) % L, :half])
+    ev1.record()
+    torch.cuda.synchronize()
+    copy_ms = ev0.elapsed_time(ev1) / args.steps
     del layers
     return dict(ms_per_step=ms, value=nbh / (ms * 1e-3), unit="state-tokens/s",
                 hbm_GBps=step_bytes / (ms * 1e-3) / 1e9,
-                hbm_frac=step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, bytes_per_step=step_bytes)
+                hbm_frac=step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, bytes_per_step=step_bytes,
+                device_copy_GBps=2 * half / (copy_ms * 1e-3) / 1e9)
 
 
 # Chunked prefill: one chunk record per chunk and head (bytes at d_k = d_v =

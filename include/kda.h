@@ -27,7 +27,9 @@
  *   Every call only enqueues work on `stream`: it never synchronises, never
  *   allocates device memory and never prints.
  * - Arguments are validated before anything is enqueued; on any error nothing
- *   is launched and a kda_status other than KDA_OK is returned.  A failed
+ *   is launched and a kda_status other than KDA_OK is returned.  Empty
+ *   requests are errors: B or H below 1 give KDA_ERR_SHAPE, a token count T,
+ *   window W or write-back interval C below 1 gives KDA_ERR_ARG.  A failed
  *   kernel launch returns KDA_ERR_HIP.  NaN/Inf in inputs are not checked.
  * - Records: one fixed-size slot of kda_record_bytes() per (sequence, head),
  *   slots ordered [B][H].  A zero-filled slot is the zero state (fresh EMA).

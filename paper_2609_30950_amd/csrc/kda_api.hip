@@ -299,7 +299,8 @@ int kda_step_writeback(const kda_config* cfg, void* records, void* ws, void* str
 int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode, const float* s,
                    float* s_out, void* stream) {
   if (cfg == nullptr) return KDA_ERR_ARG;
-  if (cfg->B < 1 || cfg->H < 1 || T < 1) return KDA_ERR_SHAPE;
+  if (cfg->B < 1 || cfg->H < 1) return KDA_ERR_SHAPE;
+  if (T < 1) return KDA_ERR_ARG;
   if (cfg->d_k != 64 && cfg->d_k != 128 && cfg->d_k != 256) return KDA_ERR_UNSUPPORTED;
   if (cfg->decay_per_head) return KDA_ERR_UNSUPPORTED;
   if (bits < 1 || bits > 16 || (mode != KDA_GATES_LOG && mode != KDA_GATES_LINEAR)) return KDA_ERR_ARG;

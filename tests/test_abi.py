@@ -100,3 +100,30 @@ def test_head_unit_configs():
         assert (K.record_bytes(c) > 0) == ok, mode
     bad = K.Config(B=1, H=2, d_k=64, d_v=64, weight_mode=8)
     assert K.record_bytes(bad) == 0
+
+
+def test_empty_requests_rejected_before_launch():
+    """Zero sequences, heads, tokens, window or interval: an error status, and
+    nothing launched (the calls return on a machine without a GPU)."""
+    lib = K.load()
+    one = ctypes.c_void_p(256)
+    for kw in (dict(B=0), dict(H=0), dict(B=-1)):
+        base = dict(B=1, H=2, d_k=64, d_v=64, group_rows=64)
+        base.update(kw)
+        cfg = K.Config(**base)
+        assert K.record_bytes(cfg) == 0 and K.workspace_bytes(cfg) == 0
+        assert lib.kda_step(ctypes.byref(cfg.c()), one, one, one, one, one, one, None, one, one,
+                            None) == 2
+        assert lib.kda_prefill(ctypes.byref(cfg.c()), 8, 4, one, one, one, one, one, one, None,
+                               one, one, None) == 2
+    cfg = K.Config(B=1, H=2, d_k=64, d_v=64, group_rows=64)
+    c = ctypes.byref(cfg.c())
+    for T, C in ((0, 4), (8, 0), (-3, 4)):
+        assert lib.kda_prefill(c, T, C, one, one, one, one, one, one, None, one, one, None) == 1
+    for W, C in ((0, 1), (16, 0)):
+        assert lib.kda_weights(c, W, C, one, one, one, one, one, None) == 1
+        assert lib.kda_weights_exact(c, W, C, one, one, one, one, one, None) == 1
+    assert lib.kda_gate_quant(c, 0, 4, 0, one, one, None) == 1
+    ch = K.Config(B=1, H=2, d_k=64, d_v=64, group_rows=64, chunked=1)
+    assert lib.kda_prefill(ctypes.byref(ch.c()), 128, 65, one, one, one, one, one, one, None, one,
+                           one, None) == 1   # chunked intervals hold at most 64 tokens

@@ -476,11 +476,11 @@ __host__ __device__ inline size_t stats_words_bytes(int wc, int dv) {
   return (size_t)(wc + 1) * dv * 4;
 }
 
-// Tokens [tok0, tok0 + ntk) of one head with the state resident in registers,
-// starting from the record: outputs o for every token, the float32 state after
-// the last token (to the workspace), row ranges and EMA rates, weights c and,
-// for the per-head scope, the widths (with alloc_sm as the allocator's LDS).
-// Decode is the one-token case.  All threads of the block (2 d_k) call it.
+// Decode token tok0 of one head with the state resident in registers,
+// starting from the record: the output o, the token's vectors (d_k <= 128) or
+// the float32 state after it (d_k = 256) for the requantisation, row ranges
+// and EMA rates, weights c and, for the per-head scope, the widths (with
+// alloc_sm as the allocator's LDS).  All threads of the block (2 d_k) call it.
 template <int DK, int DV, bool HEAD, bool BF16, bool COMPACT>
 __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK, DV>& sm,
                                            uint32_t* words, AllocSmem* alloc_sm) {
@@ -524,9 +524,8 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
   // record and the token's vectors a, g, w; else it reads the float32 state
   constexpr bool compact = COMPACT;
   float* hv = p.ws_hv + (size_t)bh * (DV + 2 * DK);
-  for (int j = 0; j < p.ntk; ++j) {
-    const int tok = p.tok0 + j;
-    if (j > 0) ema(load_rows<DK, BF16>(sm.rs, p, bh, tok));
+  {
+    const int tok = p.tok0;
     __syncthreads();
     if (compact && t < DK) {
       hv[DV + t] = sm.rs.ak[t].x;        // a = fl32(exp(-s))

@@ -215,6 +215,20 @@ __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, 
   __syncthreads();
 }
 
+// Sum of the per-segment partials of one row over its SEGS segment lanes,
+// which sit PAIRS lanes apart (PAIRS = 2: the two candidate lanes of a
+// segment are adjacent), in the halving order of seg_combine.
+template <int SEGS, int PAIRS>
+__device__ __forceinline__ float seg_combine_p(float v) {
+  if constexpr (PAIRS == 1) {
+    return seg_combine<SEGS>(v);
+  } else {
+    static_assert(SEGS <= 2, "candidate pairs with at most two segments per row");
+    if constexpr (SEGS == 2) v = v + dpp_f<0x4E>(v);   // lanes differing in bit 1
+    return v;
+  }
+}
+
 // Quantise the rows of a row-major float32 state S[DK][DV] (device memory)
 // with widths bits[] (method: see the top of this file and include/kda.h).
 // Thread t handles the 64-column segment t % (DV/64) of row
@@ -228,18 +242,31 @@ __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, 
 // grows as m falls.  Once that bound exceeds the best error no smaller f can
 // reach the minimum, so the scan stops; the result equals the exhaustive
 // first strict minimum over all 16 candidates.
-template <int DK, int DV, bool SYNC_AFTER_LOAD = false, typename LoadRow, typename CT>
+//
+// PAIRS = 2 (blocks of 4 d_k threads, for grids with few heads): two adjacent
+// lanes hold the same segment and evaluate the candidates m and m - 1 of one
+// step together.  The second one's bound is tested against the best error
+// before the first one's result, so it may be evaluated where the sequential
+// scan would have stopped; its error then exceeds the best (the bound is a
+// lower bound) and the scan ends at the next step: the same choice, at most
+// one evaluation more.
+template <int DK, int DV, bool SYNC_AFTER_LOAD = false, int PAIRS = 1, typename LoadRow,
+          typename CT>
 __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, const uint8_t* perm,
                          const float (*phi)[N_FIT], CT* Ct, uint16_t* scale_out,
                          unsigned long long* diag) {
   constexpr int LD = ct_ld<DK, CT>();
   constexpr int SEGS = DV / SEG;
-  constexpr int ITEMS = DK * SEGS;
+  constexpr int ITEMS = DK * SEGS * PAIRS;
+  static_assert(PAIRS == 1 || PAIRS == 2, "candidates per step");
+  static_assert(N_FIT % PAIRS == 0, "whole candidate pairs");
   const int tid = threadIdx.x, nt = blockDim.x;
   const int iters = (ITEMS + nt - 1) / nt;   // same count for every thread
   for (int rep = 0; rep < iters; ++rep) {
-  const int item = rep * nt + tid;
-  const bool valid = item < ITEMS;
+  const int unit = rep * nt + tid;
+  const bool valid = unit < ITEMS;
+  const int half = PAIRS == 2 ? (unit & 1) : 0;
+  const int item = unit / PAIRS;
   const int i = valid ? perm[item / SEGS] : 0;
   const int sg = item % SEGS;
   float x[SEG];
@@ -249,19 +276,25 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
   float mx = 0.f;
 #pragma unroll
   for (int j = 0; j < SEG; ++j) mx = fmaxf(mx, fabsf(x[j]));
-  if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0xB1>(mx));
-  if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
+  if constexpr (PAIRS == 1) {
+    if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0xB1>(mx));
+    if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
+  } else {
+    if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0x4E>(mx));
+  }
   const int b = bits[i];
   CT* dst = Ct + (size_t)(sg * SEG) * LD + i;
+  // the first lane of a candidate pair writes the codes and the scale
+  const bool writer = valid && half == 0;
   int evals = 0;
   if (b == 1) {
     float acc = 0.f;
 #pragma unroll
     for (int j = 0; j < SEG; ++j) acc = acc + fabsf(x[j]);
     // halving over segments: lanes differing in the top segment bit first
-    acc = seg_combine<SEGS>(acc);
+    acc = seg_combine_p<SEGS, PAIRS>(acc);
     const uint16_t mu = f32_to_f16_sat(acc * (1.0f / (float)DV));
-    if (valid) {
+    if (writer) {
 #pragma unroll
       for (int j = 0; j < SEG; ++j) dst[(size_t)j * LD] = (CT)(x[j] < 0.f ? 1 : 0);
       if (sg == 0) scale_out[i] = mu;
@@ -270,28 +303,55 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
     const float nf = (float)((1 << (b - 1)) - 1);
     float best = __builtin_inff();
     int mb = N_FIT - 1;
-    float ph = phi[b][N_FIT - 1];
-    for (int m = N_FIT - 1; m >= 0; --m) {
-      const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
-      ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
-      const float emax = __builtin_fmaf(-nf, d, mx);
-      if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
-      ++evals;
-      const float inv = d > 0.f ? 1.0f / d : 0.f;
-      float err = 0.f;
+    if constexpr (PAIRS == 1) {
+      float ph = phi[b][N_FIT - 1];
+      for (int m = N_FIT - 1; m >= 0; --m) {
+        const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
+        ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
+        const float emax = __builtin_fmaf(-nf, d, mx);
+        if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
+        ++evals;
+        const float inv = d > 0.f ? 1.0f / d : 0.f;
+        float err = 0.f;
 #pragma unroll
-      for (int j = 0; j < SEG; ++j) {
-        const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-        const float e = __builtin_fmaf(-c, d, x[j]);
-        err = __builtin_fmaf(e, e, err);
+        for (int j = 0; j < SEG; ++j) {
+          const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+          const float e = __builtin_fmaf(-c, d, x[j]);
+          err = __builtin_fmaf(e, e, err);
+        }
+        err = seg_combine<SEGS>(err);
+        if (err <= best) { best = err; mb = m; }
       }
-      err = seg_combine<SEGS>(err);
-      if (err <= best) { best = err; mb = m; }
+    } else {
+      for (int m0 = N_FIT - 1; m0 >= 1; m0 -= 2) {
+        const int m1 = m0 - 1;
+        const float d0 = f16_to_f32(f32_to_f16_sat(mx * phi[b][m0]));
+        const float d1 = f16_to_f32(f32_to_f16_sat(mx * phi[b][m1]));
+        const float e0 = __builtin_fmaf(-nf, d0, mx), e1 = __builtin_fmaf(-nf, d1, mx);
+        if (e0 >= 0.f && e0 * e0 > best) break;           // row-uniform decisions
+        const bool stop1 = e1 >= 0.f && e1 * e1 > best;
+        const float d = half ? d1 : d0;
+        if (!half || !stop1) ++evals;
+        const float inv = d > 0.f ? 1.0f / d : 0.f;
+        float err = 0.f;
+#pragma unroll
+        for (int j = 0; j < SEG; ++j) {
+          const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+          const float e = __builtin_fmaf(-c, d, x[j]);
+          err = __builtin_fmaf(e, e, err);
+        }
+        err = seg_combine_p<SEGS, 2>(err);
+        const float other = dpp_f<0xB1>(err);   // the partner lane's candidate
+        const float err0 = half ? other : err, err1 = half ? err : other;
+        if (err0 <= best) { best = err0; mb = m0; }
+        if (!stop1 && err1 <= best) { best = err1; mb = m1; }
+        if (stop1) break;
+      }
     }
     const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
     const float d = f16_to_f32(dh);
     const float inv = d > 0.f ? 1.0f / d : 0.f;
-    if (valid) {
+    if (writer) {
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
         const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
@@ -322,8 +382,10 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
   static_assert(DV == DK && DV % WAVE == 0, "one (column, half) per thread, halves wave-aligned");
   const int tid = threadIdx.x;
   const int col = tid % DV;
+  // threads past 2 d_v (blocks of the paired fit) only join the barrier
   const int half = __builtin_amdgcn_readfirstlane(tid / DV);
-  const int r0 = half * HALF;
+  const bool packer = half < 2;
+  const int r0 = (packer ? half : 0) * HALF;
   const int start = __builtin_amdgcn_readfirstlane(P[r0]);
   const int split = __builtin_amdgcn_readfirstlane(P[HALF]);
   // widths, four per LDS word (bits[] is 4-byte aligned), read as broadcasts
@@ -336,6 +398,8 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
   constexpr int CB = (int)sizeof(CT);   // bytes per code
   constexpr int CPR = 16 / CB;                  // codes per 16-byte read
   const CT* cc = Ct + (size_t)col * ct_ld<DK, CT>() + r0;
+  const bool shared = (split & 31) != 0;
+  if (packer) {
 #pragma unroll
   for (int i0 = 0; i0 < HALF; i0 += CPR) {
     const uint4 raw = *(const uint4*)(cc + i0);
@@ -364,10 +428,10 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
     }
   }
   // the lower half's last partial word goes to LDS when the upper half shares it
-  const bool shared = (split & 31) != 0;
   if (half == 0 && nb > 0) {
     if (shared) tail[col] = cur;
     else words[wi * DV + col] = cur;
+  }
   }
   __syncthreads();
   if (half == 1) {
@@ -621,13 +685,14 @@ struct RequantLds {
 };
 
 // Quantise the state after the write-back interval with the allocated widths
-// and pack it into the record in place.  COMPACT (a decode step): the state is
+// and pack it into the record in place (PAIRS: candidates per fit step, see
+// fit_rows).  COMPACT (a decode step): the state is
 // rebuilt row by row from the record and the token's vectors the stats pass
 // left in the workspace, S_ij = fma(g_i, w_j, fl32(a_i x^_ij)) with x^ the
 // record's dequantised value -- the same operations as the stats pass, so the
 // same float32 state.  Otherwise the stats pass left the float32 state itself.
 // All threads of the block (2 d_k) call it.
-template <int DK, int DV, bool COMPACT, typename CT>
+template <int DK, int DV, bool COMPACT, typename CT, int PAIRS = 1>
 __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLds<DK, DV, COMPACT, CT>& sm) {
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
@@ -686,8 +751,9 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
     __syncthreads();
     width_order<DK>(sm.nb, sm.perm, sm.os);
     const float* S = p.ws_s32 + (size_t)bh * DK * DV;
-    fit_rows<DK, DV>([&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(S, i, sg, x); }, sm.nb,
-                     sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
+    fit_rows<DK, DV, false, PAIRS>(
+        [&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(S, i, sg, x); }, sm.nb, sm.perm,
+        sm.phi, sm.Ct, sm.sc16, p.diag_fit);
   }
   __syncthreads();
   pack_cols<DK, DV>(sm.Ct, sm.nb, sm.os.P, (uint32_t*)(rec + L.codes_off), sm.tail);
@@ -698,11 +764,17 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
 template <bool C8>
 using CodeTile = typename std::conditional<C8, int8_t, int16_t>::type;
 
-template <int DK, int DV, bool COMPACT, bool C8>
-__global__ void __launch_bounds__(2 * DK) __attribute__((amdgpu_waves_per_eu(4)))
-k_requant(KParams p) {
+// Threads of a requantisation block: 2 d_k, or one per (row, segment,
+// candidate lane) when that is more.
+constexpr int requant_threads(int dk, int dv, int pairs) {
+  return 2 * dk > dk * (dv / SEG) * pairs ? 2 * dk : dk * (dv / SEG) * pairs;
+}
+
+template <int DK, int DV, bool COMPACT, bool C8, int PAIRS = 1>
+__global__ void __launch_bounds__(requant_threads(DK, DV, PAIRS))
+    __attribute__((amdgpu_waves_per_eu(4))) k_requant(KParams p) {
   __shared__ RequantLds<DK, DV, COMPACT, CodeTile<C8>> sm;
-  requant_head<DK, DV, COMPACT, CodeTile<C8>>(p, blockIdx.x, sm);
+  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS>(p, blockIdx.x, sm);
 }
 
 // Buffer resource over n bytes at base (word 3 of a gfx9 resource: untyped
@@ -1326,13 +1398,16 @@ hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st) {
   hipError_t e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl,
                         (const float*)p.ws_rpart, (const double*)p.ws_gam, p.ws_bits);
   if (e != hipSuccess) return e;
+  // d_v <= 128: the fit evaluates candidate pairs (twice the lanes per head;
+  // a prefill has few heads, so the grid alone would leave SIMDs idle)
   const bool c8 = DK > 128 || p.bmax <= 8;
+  constexpr int T64 = requant_threads(64, 64, 2), T128 = requant_threads(128, 128, 2);
   if (DK == 64)
-    return c8 ? launch("requant", k_requant<64, 64, false, true>, p.B * p.H, 128, 0, st, p)
-              : launch("requant", k_requant<64, 64, false, false>, p.B * p.H, 128, 0, st, p);
+    return c8 ? launch("requant", k_requant<64, 64, false, true, 2>, p.B * p.H, T64, 0, st, p)
+              : launch("requant", k_requant<64, 64, false, false, 2>, p.B * p.H, T64, 0, st, p);
   if (DK == 256) return launch("requant", k_requant<256, 256, false, true>, p.B * p.H, 512, 0, st, p);
-  return c8 ? launch("requant", k_requant<128, 128, false, true>, p.B * p.H, 256, 0, st, p)
-            : launch("requant", k_requant<128, 128, false, false>, p.B * p.H, 256, 0, st, p);
+  return c8 ? launch("requant", k_requant<128, 128, false, true, 2>, p.B * p.H, T128, 0, st, p)
+            : launch("requant", k_requant<128, 128, false, false, 2>, p.B * p.H, T128, 0, st, p);
 }
 
 hipError_t launch_prefill(KParams p, int C, hipStream_t st) {

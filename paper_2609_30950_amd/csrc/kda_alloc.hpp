@@ -78,10 +78,11 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
                                AllocSmem& sm) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id();
   const int L = bmax - bmin;
-  // rows n = tid + k * nt, k < RPT; the fraction bits of a row are
-  // recomputed from c_at(n) when the row is a boundary candidate
+  // rows n = tid + k * nt, k < RPT, their weights held in registers (read
+  // once: the radix passes and the ranking use them again)
   static_assert(RPT <= 32, "candidate mask");
   int E[RPT];
+  double Cv[RPT];
   for (int e = tid; e < EBINS; e += nt) sm.hist_e[e] = 0;
   for (int e = tid; e < 2 * 256; e += nt) sm.hist_d[e >> 8][e & 255] = 0;
   for (int n = tid; n < N; n += nt) sm.extra[n] = 0;
@@ -96,8 +97,10 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   for (int k = 0; k < RPT; ++k) {
     const int n = tid + k * nt;
     E[k] = E_ZERO;
+    Cv[k] = 0.0;
     if (n < N) {
       const double cv = c_at(n);
+      Cv[k] = cv;
       if (cv > 0.0) {
         int ei;
         frexp(cv, &ei);
@@ -214,10 +217,9 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     const int shift = pass < 6 ? 44 - 8 * pass : 0;
     const unsigned long long dmask = pass < 6 ? 255ull : 15ull;
     int* hd = sm.hist_d[pass & 1];
-    for (unsigned m = cand; m != 0u; m &= m - 1u) {
-      const int k = __builtin_ctz(m);
-      atomicAdd(&hd[(frac_bits(c_at(tid + k * nt)) >> shift) & dmask], 1);
-    }
+#pragma unroll
+    for (int k = 0; k < RPT; ++k)
+      if ((cand >> k) & 1u) atomicAdd(&hd[(frac_bits(Cv[k]) >> shift) & dmask], 1);
     __syncthreads();
     if (tid < WAVE) {
       // lane j covers bins 4j+3..4j of the descending order dmask..0
@@ -251,9 +253,10 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     }
     __syncthreads();
     const unsigned long long dg = (unsigned long long)sm.sel_digit;
-    for (unsigned m = cand; m != 0u; m &= m - 1u) {
-      const int k = __builtin_ctz(m);
-      const unsigned long long d = (frac_bits(c_at(tid + k * nt)) >> shift) & dmask;
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      if (!((cand >> k) & 1u)) continue;
+      const unsigned long long d = (frac_bits(Cv[k]) >> shift) & dmask;
       if (d > dg) {
         sm.extra[tid + k * nt] = 1;   // above the boundary digit: granted
         cand &= ~(1u << k);
@@ -279,10 +282,11 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     cand = 0u;
   }
   // stage 3: at most one wave of candidates left; rank them in wave 0
-  for (unsigned m = cand; m != 0u; m &= m - 1u) {
-    const int k = __builtin_ctz(m);
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    if (!((cand >> k) & 1u)) continue;
     const int pos = atomicAdd(&sm.cand_n, 1);
-    sm.cand_key[pos] = frac_bits(c_at(tid + k * nt));
+    sm.cand_key[pos] = frac_bits(Cv[k]);
     sm.cand_row[pos] = tid + k * nt;
   }
   __syncthreads();

@@ -40,6 +40,7 @@ VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 FIT_OPS_PER_ELEMENT = 5
 SEG_COLS = 64
 FINAL_OPS_PER_ELEMENT = 6
+BLOCK_ROWS = 32   # rows of one scale group of a head unit
 
 
 def kernel_source_hash():
@@ -479,6 +480,17 @@ def main():
                     traffic=committed_traffic("requant", args.workload), kernel="requant",
                     lane_ops_per_launch=ops,
                     candidates_per_row_segment=evals_per_launch / segs)
+    elif dom == "step" and args.head_units and fit_evals is not None:
+        # head units: the step kernel fits every (32-row block, column) group
+        # with the same candidates, 5 lane-ops per element each, then codes it
+        t_dom = kern[dom]["ms_avg"] * 1e-3
+        evals = fit_evals / max(1, kern[dom]["launches"])
+        ops = evals * BLOCK_ROWS * FIT_OPS_PER_ELEMENT + elems * FINAL_OPS_PER_ELEMENT
+        achieved = ops / t_dom / 1e12
+        roof = dict(bound="alu", achieved=achieved, peak=VALU_PEAK_TOPS, unit="TOP/s",
+                    frac=achieved / VALU_PEAK_TOPS, traffic=None, kernel="step",
+                    lane_ops_per_launch=ops,
+                    candidates_per_block=evals / (elems / BLOCK_ROWS))
     else:
         t_dom = kern[dom]["ms_avg"] * 1e-3
         roof = dict(bound="hbm", achieved=step_bytes / t_dom / 1e9, peak=HBM_PEAK_GBPS,

@@ -122,9 +122,10 @@ __device__ __forceinline__ void load_block(const uint32_t* codes, int dv, int w,
 
 // Fit column c of the block (the row quantiser's candidates, error in row
 // order, smallest clip factor among equal errors), pack its codes into B
-// words and store them with the block scale.
+// words and store them with the block scale.  Returns the number of
+// candidates evaluated.
 template <int B, int CPL>
-__device__ __forceinline__ void fit_pack_block(const float (&X)[ROW_BLOCK][CPL], int c,
+__device__ __forceinline__ int fit_pack_block(const float (&X)[ROW_BLOCK][CPL], int c,
                                                const float* phi, uint32_t* codes, int dv, int w,
                                                int col, uint16_t* scale_out) {
   constexpr int n = (1 << (B - 1)) - 1;
@@ -133,12 +134,13 @@ __device__ __forceinline__ void fit_pack_block(const float (&X)[ROW_BLOCK][CPL],
 #pragma unroll
   for (int r = 0; r < ROW_BLOCK; ++r) mx = fmaxf(mx, fabsf(X[r][c]));
   float best = __builtin_inff();
-  int mb = N_FIT - 1;
+  int mb = N_FIT - 1, evals = 0;
   for (int m = N_FIT - 1; m >= 0; --m) {
     const float d = f16_to_f32(f32_to_f16_sat(mx * phi[m]));
     // the row maximum's clip error bounds this and every smaller factor
     const float emax = __builtin_fmaf(-nf, d, mx);
     if (emax >= 0.f && emax * emax > best) break;
+    ++evals;
     const float inv = d > 0.f ? 1.0f / d : 0.f;
     float err = 0.f;
 #pragma unroll
@@ -169,18 +171,21 @@ __device__ __forceinline__ void fit_pack_block(const float (&X)[ROW_BLOCK][CPL],
 #pragma unroll
   for (int k = 0; k < B; ++k) codes[(size_t)(w * B + k) * dv + col] = wd[k];
   *scale_out = dh;
+  return evals;
 }
 
 // All of this lane's columns of the wave's block at width B.
 template <int B, int CPL>
-__device__ __forceinline__ void fit_pack_cols(const float (&X)[ROW_BLOCK][CPL], const float* phi,
-                                              uint32_t* codes, int dv, int w, int lane,
-                                              uint16_t* bscale) {
+__device__ __forceinline__ int fit_pack_cols(const float (&X)[ROW_BLOCK][CPL], const float* phi,
+                                             uint32_t* codes, int dv, int w, int lane,
+                                             uint16_t* bscale) {
+  int evals = 0;
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
     const int col = lane + WAVE * c;
-    fit_pack_block<B, CPL>(X, c, phi, codes, dv, w, col, bscale + w * dv + col);
+    evals += fit_pack_block<B, CPL>(X, c, phi, codes, dv, w, col, bscale + w * dv + col);
   }
+  return evals;
 }
 
 template <int DK>
@@ -257,14 +262,20 @@ __global__ void __launch_bounds__(2 * DK) k_head_step(KParams p) {
   }
   __syncthreads();   // every read of the old record and of sm.width is ordered before the writes
   const int wn = sm.width;
+  int evals;
   switch (wn) {
-    case 2: fit_pack_cols<2, CPL>(X, p.phi[2], codes, DV, w, lane, bscale); break;
-    case 3: fit_pack_cols<3, CPL>(X, p.phi[3], codes, DV, w, lane, bscale); break;
-    case 4: fit_pack_cols<4, CPL>(X, p.phi[4], codes, DV, w, lane, bscale); break;
-    case 5: fit_pack_cols<5, CPL>(X, p.phi[5], codes, DV, w, lane, bscale); break;
-    case 6: fit_pack_cols<6, CPL>(X, p.phi[6], codes, DV, w, lane, bscale); break;
-    case 7: fit_pack_cols<7, CPL>(X, p.phi[7], codes, DV, w, lane, bscale); break;
-    default: fit_pack_cols<8, CPL>(X, p.phi[8], codes, DV, w, lane, bscale); break;
+    case 2: evals = fit_pack_cols<2, CPL>(X, p.phi[2], codes, DV, w, lane, bscale); break;
+    case 3: evals = fit_pack_cols<3, CPL>(X, p.phi[3], codes, DV, w, lane, bscale); break;
+    case 4: evals = fit_pack_cols<4, CPL>(X, p.phi[4], codes, DV, w, lane, bscale); break;
+    case 5: evals = fit_pack_cols<5, CPL>(X, p.phi[5], codes, DV, w, lane, bscale); break;
+    case 6: evals = fit_pack_cols<6, CPL>(X, p.phi[6], codes, DV, w, lane, bscale); break;
+    case 7: evals = fit_pack_cols<7, CPL>(X, p.phi[7], codes, DV, w, lane, bscale); break;
+    default: evals = fit_pack_cols<8, CPL>(X, p.phi[8], codes, DV, w, lane, bscale); break;
+  }
+  if (p.diag_fit != nullptr) {
+    // profiling: candidate evaluations of the block fits (one block-column per lane and column)
+    const int tot = wave_reduce_i(evals, [](int a, int c) { return a + c; });
+    if (lane == 0) atomicAdd(p.diag_fit, (unsigned long long)tot);
   }
   if (t < DK) {
     const uint32_t zr = p.ws_zr[(size_t)bh * DK + t];

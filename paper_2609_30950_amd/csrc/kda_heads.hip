@@ -188,10 +188,13 @@ __device__ __forceinline__ int fit_pack_cols(const float (&X)[ROW_BLOCK][CPL], c
   return evals;
 }
 
+constexpr int MAX_LEVELS = 6;   // b_max - b_min for head units (widths 2..8)
+
 template <int DK>
 struct HeadStepSmem {
   RowSmem<DK> rs;
   RecSmem<DK, DK> rsm;
+  int rank[MAX_LEVELS];
   int width;
 };
 
@@ -207,24 +210,38 @@ __global__ void __launch_bounds__(2 * DK) k_head_step(KParams p) {
   uint16_t* bscale = (uint16_t*)(rec + L.sc_off);
   __shared__ HeadStepSmem<DK> sm;
 
-  if (w == 0) {
-    // this head's width: slots (unit, l) of all heads of the sequence,
-    // granted to the `need` best keys (ties to the lower unit, then level)
-    const int nl = p.bmax - p.bmin;
-    bool granted = false;
-    if (lane < nl) {
-      const int l = p.bmin + 1 + lane;
-      const SlotKey mine = slot_key(p.ws_c[(size_t)b * p.H + h], l);
-      int rank = 0;
-      for (int u = 0; u < p.H; ++u) {
-        const double cu = p.ws_c[(size_t)b * p.H + u];
-        for (int l2 = p.bmin + 1; l2 <= p.bmax; ++l2)
-          rank += before(slot_key(cu, l2), u, l2, mine, h, l) ? 1 : 0;
-      }
-      granted = rank < p.need;
+  // this head's width: its slots (h, l) ranked against the slots (u, l2) of
+  // all heads of the sequence, the `need` best granted (ties to the lower
+  // unit, then level).  Every thread takes a share of the comparisons and
+  // counts, per slot l of this head, the slots ranked before it.
+  {
+    const int nl = p.bmax - p.bmin;   // at most MAX_LEVELS
+    if (t < MAX_LEVELS) sm.rank[t] = 0;
+    __syncthreads();
+    const double* cs = p.ws_c + (size_t)b * p.H;
+    const double cme = cs[h];
+    const int per_l = p.H * nl;
+    int cnt[MAX_LEVELS];
+#pragma unroll
+    for (int li = 0; li < MAX_LEVELS; ++li) cnt[li] = 0;
+    for (int q = t; q < nl * per_l; q += blockDim.x) {
+      const int li = q / per_l, rest = q % per_l;
+      const int u = rest / nl, l2 = p.bmin + 1 + rest % nl, l = p.bmin + 1 + li;
+      const bool bf = before(slot_key(cs[u], l2), u, l2, slot_key(cme, l), h, l);
+#pragma unroll
+      for (int k = 0; k < MAX_LEVELS; ++k) cnt[k] += (bf && k == li) ? 1 : 0;
     }
-    const int cnt = __builtin_popcountll(__ballot(granted));
-    if (lane == 0) sm.width = p.bmin + cnt;
+#pragma unroll
+    for (int k = 0; k < MAX_LEVELS; ++k) {
+      const int tot = wave_reduce_i(cnt[k], [](int x, int y) { return x + y; });
+      if (lane == 0 && tot != 0) atomicAdd(&sm.rank[k], tot);
+    }
+    __syncthreads();
+    if (t == 0) {
+      int g = 0;
+      for (int k = 0; k < nl; ++k) g += sm.rank[k] < p.need ? 1 : 0;
+      sm.width = p.bmin + g;
+    }
   }
 
   // the stored state of this lane's columns of the wave's block

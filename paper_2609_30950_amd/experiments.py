@@ -3,6 +3,7 @@
     python -m paper_2609_30950_amd.experiments erase [--heads 64] [--window 512]
     python -m paper_2609_30950_amd.experiments readout [--heads 64] [--tokens 2048]
     python -m paper_2609_30950_amd.experiments rounding [--heads 8] [--tokens 2048]
+    python -m paper_2609_30950_amd.experiments ablate [--heads 64] [--tokens 2048]
 
 ``erase``: the diagonal erase approximation against the exact Gramian
 (Sec. 2, Approximate erasure rate: with per-channel rates log-uniform in
@@ -33,6 +34,20 @@ inputs are stationary, so one set of weights per head serves every
 write-back).  Readout error = sum_t |o_t - o_ref,t|^2 / sum_t |o_ref,t|^2
 over all heads; the result is the EMA run's error over the exact run's, and
 a fourth run with uniform widths gives the ablation baseline.
+
+``ablate``: the allocation keys of the paper's ablation (Sec. 5, Table
+ablate, where only the key c_i varies and excess NLL is measured) with the
+readout error of a synthetic layer in place of NLL.  Inputs as ``readout``,
+with the values of each head scaled by exp(N(0, 1)) so that heads differ in
+range, and one layer budget over all heads (normalisation groups of one
+head).  Keys: the EMA weights (ours), range alone, raw range, relative
+range, DAMP's persistence w^(1), the write-back factor h^(C), erase rate 0,
+uniform widths (the library's weight modes), and shuffled decay: the
+stationary exact-Gramian weights of every head permuted across its rows,
+given as row weights, beside the same weights unpermuted.  Two errors: the
+absolute one over all heads, and the mean over heads of each head's error
+relative to its own output power (the paper's range normalisation assumes
+per-head output normalisation, which divides by that power).
 
 ``rounding``: correlated rounding errors at C = 1 (Sec. 2, Correlated rounding
 errors: with Kimi decays, rank-one writes and 2K tokens, lag-one error
@@ -156,6 +171,49 @@ def readout_error(heads=64, tokens=2048, C=16, mean_bits=3.0, dk=64, seed=0):
     return err(o_ema), err(o_ex), err(o_uni)
 
 
+def ablation(heads=64, tokens=2048, C=16, mean_bits=2.0, dk=64, seed=0):
+    """Readout errors (against the 32-bit mode) of every allocation key of the
+    ablation on one synthetic layer: {key: {"abs": e, "norm": e_head}}."""
+    qb, kb, vb, s, beta = readout_inputs(heads, tokens, dk, seed)
+    rng = np.random.default_rng([seed, 13])
+    scale = np.exp(rng.standard_normal(heads)).astype(np.float32)
+    vb = (vb.float() * torch.from_numpy(scale)[None, None, :, None]).to(torch.bfloat16)
+    q, k, v = qb.cuda(), kb.cuda(), vb.cuda()
+    sd, bd = torch.from_numpy(s).cuda(), torch.from_numpy(beta).cuda()
+    base = dict(B=1, H=heads, d_k=dk, d_v=dk, group_rows=dk, scope=0, mean_bits=mean_bits,
+                b_min=1, b_max=8)
+
+    def run(cfg, gamma=None):
+        recs = api.new_records(cfg)
+        o = torch.zeros(tokens * heads * dk, dtype=torch.float32, device="cuda")
+        ws = None if cfg.state32 else api.new_workspace(cfg)
+        api.kda_prefill(cfg, tokens, C, recs, q, k, v, sd, bd, o, ws, gamma=gamma)
+        return o
+
+    o_ref = run(api.Config(state32=1, **base))
+    ref2 = float(torch.sum(o_ref.double() ** 2))
+    ref_h = torch.sum(o_ref.double().view(tokens, heads, dk) ** 2, dim=(0, 2))
+
+    def err(o):
+        d2 = (o.double() - o_ref.double()) ** 2
+        # absolute readout error, and the mean over heads of each head's error
+        # relative to its own output power (what a per-head output norm sees)
+        return dict(abs=float(torch.sum(d2)) / ref2,
+                    norm=float(torch.mean(torch.sum(d2.view(tokens, heads, dk), dim=(0, 2)) / ref_h)))
+
+    out = {}
+    for mode in api.WEIGHT_MODES:
+        out[mode] = err(run(api.Config(weight_mode=api.WEIGHT_MODES.index(mode), **base)))
+    cfg = api.Config(**base)
+    gam = torch.zeros(heads * dk, dtype=torch.float64, device="cuda")
+    api.kda_weights_exact(cfg, tokens, C, qb.float().cuda(), sd, bd, kb.float().cuda(), gam)
+    out["exact"] = err(run(cfg, gamma=gam))
+    perm = np.argsort(rng.random((heads, dk)), axis=1) + np.arange(heads)[:, None] * dk
+    shuffled = gam[torch.from_numpy(perm.reshape(-1)).cuda()].contiguous()
+    out["shuffled_exact"] = err(run(cfg, gamma=shuffled))
+    return out
+
+
 def _host_step(S, q, k, v, s, beta):
     """eq. rule in float64 for a reference trajectory: S [H, dk, dv]; q, k, s
     [H, dk]; v [H, dv]; beta [H].  Returns (S, o)."""
@@ -236,7 +294,7 @@ def correlated_rounding(bits=4, heads=8, tokens=2048, dk=64, seed=0, keys="rando
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("experiment", choices=["erase", "readout", "rounding"])
+    ap.add_argument("experiment", choices=["erase", "readout", "rounding", "ablate"])
     ap.add_argument("--heads", type=int, default=64)
     ap.add_argument("--window", type=int, default=512)
     ap.add_argument("--tokens", type=int, default=2048)
@@ -247,6 +305,11 @@ def main():
             for bits in (3, 4, 5, 6):
                 out[f"{keys} keys, {bits} bits"] = correlated_rounding(
                     bits, args.heads if args.heads != 64 else 8, args.tokens, keys=keys)
+        print(json.dumps(out, indent=1))
+        return
+    if args.experiment == "ablate":
+        for C, mean in ((1, 4.0), (16, 2.0), (64, 2.0)):
+            out[f"C={C}, mean {mean:g} bits"] = ablation(args.heads, args.tokens, C, mean)
         print(json.dumps(out, indent=1))
         return
     if args.experiment == "readout":

@@ -5,6 +5,8 @@
   approximation's allocation stays within 3 % of the exact-Gramian
   allocation's distortion; with a persistent key it is clearly worse (errors
   orthogonal to a repeated key are never erased).
+* Allocation-key ablation (Sec. 5, Table ablate): shuffled weights and
+  uniform widths lose against weights matched to their rows.
 * Readout error (Sec. 3, State bit allocation; kda_prefill in 32-bit and
   quantised modes, kda_weights_exact): the EMA weights come within a few
   percent of exact-Gramian allocation, and both beat uniform widths."""
@@ -35,3 +37,22 @@ def test_readout_error_ema_vs_exact_and_uniform():
     assert 0 < e_ex and 0 < e_ema
     assert abs(e_ema / e_ex - 1) <= 0.05
     assert e_ema < 0.8 * e_uni and e_ex < 0.8 * e_uni
+
+
+def test_ablation_shuffled_decay_and_uniform_widths_lose():
+    """Sec. 5, Table ablate, on a synthetic layer: weights matched to their
+    rows beat the same weights shuffled across rows, decay-aware keys beat
+    uniform widths, and with per-head normalised errors the paper's key beats
+    relative range alone and decay with raw ranges."""
+    res = experiments.ablation(heads=16, tokens=512, C=16, mean_bits=2.0)
+    for kind in ("abs", "norm"):
+        r = {k: v[kind] for k, v in res.items()}
+        say(f"ablation readout errors ({kind}): " + ", ".join(f"{k} {v:.5f}" for k, v in r.items()))
+        assert all(v > 0 for v in r.values())
+        assert r["shuffled_exact"] > 1.05 * r["exact"]
+        assert r["ema"] < r["uniform"] and r["exact"] < r["uniform"]
+    # per-head normalised error (what the paper's range normalisation assumes):
+    # decay weighting beats relative range alone, and raw ranges overweight
+    # the heads with large values
+    r = {k: v["norm"] for k, v in res.items()}
+    assert r["ema"] < 0.9 * r["rel_range"] and r["ema"] < 0.9 * r["gamma_raw"]

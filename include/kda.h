@@ -78,8 +78,11 @@ typedef enum {
   KDA_WEIGHT_WRITEBACK = 5,     /* h R~^2, h = 1/(1 - exp(-2 C s^)) with C the
                                    write-back interval (1 for kda_step)        */
   KDA_WEIGHT_NO_ERASE_RATE = 6, /* Gamma^ with r = 0, times R~^2              */
-  KDA_WEIGHT_UNIFORM = 7        /* equal keys: uniform widths (the remainder
+  KDA_WEIGHT_UNIFORM = 7,       /* equal keys: uniform widths (the remainder
                                    of the budget to the lowest rows)          */
+  KDA_WEIGHT_DECAY = 8          /* Gamma^ alone, ranges ignored (decay-only
+                                   allocation, Sec. 5, Effect of range
+                                   normalization)                             */
 } kda_weight_mode;
 
 typedef struct {

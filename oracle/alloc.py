@@ -75,6 +75,8 @@ def mode_weights(gamma, R, Rt, mode="ema"):
     gamma = np.asarray(gamma, F64)
     if mode == "uniform":
         return np.ones_like(gamma)
+    if mode == "decay":
+        return gamma.copy()   # ranges ignored (R~ taken as 1)
     if mode in ("range", "gamma_raw"):
         Rr = np.asarray(R, np.float32).astype(F64)
         return gamma * (Rr * Rr)

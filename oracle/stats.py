@@ -97,12 +97,12 @@ def gamma_hat(s_hat, r):
 
 
 WEIGHT_MODES = ("ema", "range", "gamma_raw", "rel_range", "persist", "writeback",
-                "no_erase_rate", "uniform")
+                "no_erase_rate", "uniform", "decay")
 
 
 def mode_gamma(s_hat, r, mode="ema", C=1):
     s_hat = np.asarray(s_hat, F64)
-    if mode in ("ema", "gamma_raw"):
+    if mode in ("ema", "gamma_raw", "decay"):
         return gamma_hat(s_hat, r)
     if mode == "no_erase_rate":
         return gamma_hat(s_hat, np.zeros_like(s_hat))

@@ -180,7 +180,7 @@ def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None):
 
 # kda_weight_mode values, in the order of the oracle's stats.WEIGHT_MODES
 WEIGHT_MODES = ("ema", "range", "gamma_raw", "rel_range", "persist", "writeback",
-                "no_erase_rate", "uniform")
+                "no_erase_rate", "uniform", "decay")
 
 def kda_gate_quant(cfg, T, bits, s, s_out, mode="log"):
     """Per-token decay-gate quantisation; mode "log" or "linear"."""

@@ -53,7 +53,7 @@ int check_cfg(const kda_config* cfg, int* need) {
   if (cfg->chunked != 0 && cfg->chunked != 1) return KDA_ERR_ARG;
   if (cfg->chunked && (cfg->d_k > 128 || cfg->state32)) return KDA_ERR_UNSUPPORTED;
   if (cfg->head_units != 0 && cfg->head_units != 1) return KDA_ERR_ARG;
-  if (cfg->weight_mode < KDA_WEIGHT_EMA || cfg->weight_mode > KDA_WEIGHT_UNIFORM) return KDA_ERR_ARG;
+  if (cfg->weight_mode < KDA_WEIGHT_EMA || cfg->weight_mode > KDA_WEIGHT_DECAY) return KDA_ERR_ARG;
   // head widths come from the statistics alone (R~ = 1): no range variants
   if (cfg->head_units && (cfg->weight_mode == KDA_WEIGHT_RANGE ||
                           cfg->weight_mode == KDA_WEIGHT_GAMMA_RANGE ||

@@ -226,11 +226,12 @@ enum WeightMode {
   WM_WRITEBACK = 5,      // h^(C) R~^2, h^(C) = 1/(1 - exp(-2 C s^))
   WM_NO_ERASE_RATE = 6,  // Gamma^ with r = 0, times R~^2
   WM_UNIFORM = 7,        // equal keys: uniform widths
+  WM_DECAY = 8,          // Gamma^ alone (ranges ignored)
 };
 
 // Row factor of the key; rates clamped below at 1e-12 as in gamma_hat.
 __device__ __forceinline__ double mode_gamma(int mode, double s_hat, double r, int C) {
-  if (mode == WM_EMA || mode == WM_GAMMA_RAW) return gamma_hat(s_hat, r);
+  if (mode == WM_EMA || mode == WM_GAMMA_RAW || mode == WM_DECAY) return gamma_hat(s_hat, r);
   if (mode == WM_NO_ERASE_RATE) return gamma_hat(s_hat, 0.0);
   const double s = s_hat < 1e-12 ? 1e-12 : s_hat;
   if (mode == WM_PERSIST) return 1.0 / -expm1(-2.0 * s);
@@ -241,6 +242,7 @@ __device__ __forceinline__ double mode_gamma(int mode, double s_hat, double r, i
 // Key c of a row from its factor, row maximum and group RMS.
 __device__ __forceinline__ double mode_key(int mode, double gam, float R, double rms) {
   if (mode == WM_UNIFORM) return 1.0;
+  if (mode == WM_DECAY) return gam;
   if (mode == WM_RANGE || mode == WM_GAMMA_RAW) {
     const double Rr = (double)R;
     return gam * (Rr * Rr);

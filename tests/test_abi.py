@@ -94,11 +94,11 @@ def test_head_unit_configs():
     assert lib.kda_pack_state(ctypes.byref(cfg.c()), one, one, one, one, 0, one, None) == 3
     assert lib.kda_unpack_state(ctypes.byref(cfg.c()), one, one, None, None, None, None) == 3
     assert lib.kda_alloc_bits(ctypes.byref(cfg.c()), one, one, one, one, None) == 3
-    for mode, ok in ((1, False), (2, False), (3, False), (4, True), (7, True)):
+    for mode, ok in ((1, False), (2, False), (3, False), (4, True), (7, True), (8, True), (9, False)):
         c = K.Config(**base)
         c.weight_mode = mode
         assert (K.record_bytes(c) > 0) == ok, mode
-    bad = K.Config(B=1, H=2, d_k=64, d_v=64, weight_mode=8)
+    bad = K.Config(B=1, H=2, d_k=64, d_v=64, weight_mode=9)
     assert K.record_bytes(bad) == 0
 
 

@@ -56,3 +56,4 @@ def test_ablation_shuffled_decay_and_uniform_widths_lose():
     # the heads with large values
     r = {k: v["norm"] for k, v in res.items()}
     assert r["ema"] < 0.9 * r["rel_range"] and r["ema"] < 0.9 * r["gamma_raw"]
+    assert r["ema"] < r["decay"]   # decay alone (ranges ignored) loses too

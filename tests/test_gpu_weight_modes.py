@@ -103,7 +103,7 @@ def test_chunked_prefill_write_back_factor():
     _check(bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), exp, "chunked h^(48)")
 
 
-@pytest.mark.parametrize("mode", ["persist", "writeback", "no_erase_rate", "uniform"])
+@pytest.mark.parametrize("mode", ["persist", "writeback", "no_erase_rate", "uniform", "decay"])
 def test_head_units_modes(mode):
     w = W.sized(W.WORKLOADS["gdn2"], B=1, H=8, dk=64, dv=64, G=64, mean_bits=3.5, b_min=2)
     kc, oc = _cfgs(w, mode, head_units=1)

@@ -1,6 +1,7 @@
-"""Pins for the allocation-key variants the paper ablates (Sec. 5, Table ablate;
-Related work for DAMP's persistence w^(1) = 1/(1 - a^2); Choice of persistence
-factor for h^(C) = 1/(1 - exp(-2 C s)))."""
+"""Pins for the allocation-key variants the paper ablates (Sec. 5, Table ablate
+and Effect of range normalization for decay-only allocation; Related work for
+DAMP's persistence w^(1) = 1/(1 - a^2); Choice of persistence factor for
+h^(C) = 1/(1 - exp(-2 C s)))."""
 import numpy as np
 import pytest
 
@@ -77,3 +78,26 @@ def test_every_mode_meets_the_budget(mode):
     oc.weight = mode
     st, _ = step.write_back(S, m, e, nt, oc, C=16)
     assert int(st["widths"].sum()) == alloc.budget(3.5, 128)
+
+
+def test_decay_only_ignores_ranges_and_equals_ema_at_equal_ranges():
+    """Decay-only keys are Gamma^ itself: widths do not move when the state's
+    rows are rescaled, and they equal the paper's key when every row of a
+    group has the same range (R~ = 1)."""
+    oc, S, m, e, nt = _state()
+    oc.weight = "decay"
+    a, _ = step.write_back(S, m, e, nt, oc)
+    rng = np.random.default_rng(5)
+    S2 = (S * rng.uniform(0.1, 10.0, S.shape[:-1] + (1,))).astype(np.float32)
+    b, _ = step.write_back(S2, m, e, nt, oc)
+    assert np.array_equal(a["widths"], b["widths"])
+    # rows of equal range: scale every row to range 1, then R~ = 1 exactly
+    R = np.max(np.abs(S), axis=-1, keepdims=True)
+    S3 = (S / np.where(R > 0, R, 1)).astype(np.float32)
+    S3[..., 0] = np.where(np.max(np.abs(S3), axis=-1) < 1, 1.0, S3[..., 0])
+    assert np.all(np.max(np.abs(S3), axis=-1) == 1.0)
+    c, _ = step.write_back(S3, m, e, nt, oc)
+    oc.weight = "ema"
+    d, _ = step.write_back(S3, m, e, nt, oc)
+    assert np.array_equal(c["widths"], d["widths"])
+    assert not np.array_equal(a["widths"], step.write_back(S, m, e, nt, oc)[0]["widths"])

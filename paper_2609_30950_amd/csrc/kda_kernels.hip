@@ -787,8 +787,9 @@ constexpr int BUF_NT = 2;   // cache policy of a buffer access: nontemporal
 // Unquantised ("32-bit") state: load, the interval's tokens, store.  Columns
 // are independent in the recurrence, so a block takes one 64-column slice of a
 // head (blockIdx.x = head * slices + slice): 32 state values per lane keep the
-// register count low enough for eight waves per SIMD, and the grid holds
-// twice as many, half-sized blocks, which keeps more of the state streaming.
+// register count low (eight waves per SIMD for one token, ONE: the decode
+// step), and the grid holds more, smaller blocks, which keeps more of the
+// state streaming.
 template <int DK, int DV, bool BF16, bool ONE>
 __global__ void __launch_bounds__(2 * DK) k_step32(KParams p) {
   constexpr int NSL = DV / SLICE;

@@ -44,7 +44,10 @@ head).  Keys: the EMA weights (ours), range alone, raw range, relative
 range, DAMP's persistence w^(1), the write-back factor h^(C), erase rate 0,
 uniform widths (the library's weight modes), and shuffled decay: the
 stationary exact-Gramian weights of every head permuted across its rows,
-given as row weights, beside the same weights unpermuted.  Two errors: the
+given as row weights, beside the same weights unpermuted.  With C = 64 and
+two bits the run is repeated with natural and with equal row ranges (keys
+scaled so that the rows' steady-state magnitudes agree), our reading of the
+two settings of Fig. 1d.  Two errors: the
 absolute one over all heads, and the mean over heads of each head's error
 relative to its own output power (the paper's range normalisation assumes
 per-head output normalisation, which divides by that power).
@@ -171,10 +174,21 @@ def readout_error(heads=64, tokens=2048, C=16, mean_bits=3.0, dk=64, seed=0):
     return err(o_ema), err(o_ex), err(o_uni)
 
 
-def ablation(heads=64, tokens=2048, C=16, mean_bits=2.0, dk=64, seed=0):
+def ablation(heads=64, tokens=2048, C=16, mean_bits=2.0, dk=64, seed=0, ranges="natural"):
     """Readout errors (against the 32-bit mode) of every allocation key of the
-    ablation on one synthetic layer: {key: {"abs": e, "norm": e_head}}."""
+    ablation on one synthetic layer: {key: {"abs": e, "norm": e_head}}, plus
+    "range_spread": the standard deviation of log row ranges within a head
+    of the final unquantised state (median over heads).  ranges="equal"
+    scales key channel i by sqrt(1 - exp(-2 s_i)), which evens out the rows'
+    steady-state magnitudes 1/sqrt(1 - exp(-2 s_i)), so that decay is the
+    only thing that tells rows apart."""
     qb, kb, vb, s, beta = readout_inputs(heads, tokens, dk, seed)
+    if ranges == "equal":
+        g = np.sqrt(-np.expm1(-2.0 * s[:, :1].astype(np.float64)))
+        g = g / np.sqrt(np.mean(g * g, axis=-1, keepdims=True))
+        kb = (kb.float() * torch.from_numpy(g.astype(np.float32))).to(torch.bfloat16)
+    else:
+        assert ranges == "natural", ranges
     rng = np.random.default_rng([seed, 13])
     scale = np.exp(rng.standard_normal(heads)).astype(np.float32)
     vb = (vb.float() * torch.from_numpy(scale)[None, None, :, None]).to(torch.bfloat16)
@@ -183,14 +197,20 @@ def ablation(heads=64, tokens=2048, C=16, mean_bits=2.0, dk=64, seed=0):
     base = dict(B=1, H=heads, d_k=dk, d_v=dk, group_rows=dk, scope=0, mean_bits=mean_bits,
                 b_min=1, b_max=8)
 
+    state = {}
+
     def run(cfg, gamma=None):
         recs = api.new_records(cfg)
         o = torch.zeros(tokens * heads * dk, dtype=torch.float32, device="cuda")
         ws = None if cfg.state32 else api.new_workspace(cfg)
         api.kda_prefill(cfg, tokens, C, recs, q, k, v, sd, bd, o, ws, gamma=gamma)
+        if cfg.state32:
+            state["S"] = recs.view(torch.float32).view(heads, dk, dk).double()
         return o
 
     o_ref = run(api.Config(state32=1, **base))
+    R = torch.amax(torch.abs(state["S"]), dim=2)
+    spread = float(torch.median(torch.std(torch.log(R), dim=1)))
     ref2 = float(torch.sum(o_ref.double() ** 2))
     ref_h = torch.sum(o_ref.double().view(tokens, heads, dk) ** 2, dim=(0, 2))
 
@@ -211,6 +231,7 @@ def ablation(heads=64, tokens=2048, C=16, mean_bits=2.0, dk=64, seed=0):
     perm = np.argsort(rng.random((heads, dk)), axis=1) + np.arange(heads)[:, None] * dk
     shuffled = gam[torch.from_numpy(perm.reshape(-1)).cuda()].contiguous()
     out["shuffled_exact"] = err(run(cfg, gamma=shuffled))
+    out["range_spread"] = spread
     return out
 
 
@@ -310,6 +331,9 @@ def main():
     if args.experiment == "ablate":
         for C, mean in ((1, 4.0), (16, 2.0), (64, 2.0)):
             out[f"C={C}, mean {mean:g} bits"] = ablation(args.heads, args.tokens, C, mean)
+        for rg in ("natural", "equal"):   # the two settings of Fig. 1d: C = 64, two bits
+            out[f"C=64, mean 2 bits, {rg} row ranges"] = ablation(args.heads, args.tokens, 64, 2.0,
+                                                                  ranges=rg)
         print(json.dumps(out, indent=1))
         return
     if args.experiment == "readout":

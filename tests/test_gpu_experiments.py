@@ -45,6 +45,8 @@ def test_ablation_shuffled_decay_and_uniform_widths_lose():
     uniform widths, and with per-head normalised errors the paper's key beats
     relative range alone and decay with raw ranges."""
     res = experiments.ablation(heads=16, tokens=512, C=16, mean_bits=2.0)
+    spread = res.pop("range_spread")
+    assert spread > 0
     for kind in ("abs", "norm"):
         r = {k: v[kind] for k, v in res.items()}
         say(f"ablation readout errors ({kind}): " + ", ".join(f"{k} {v:.5f}" for k, v in r.items()))
@@ -57,3 +59,17 @@ def test_ablation_shuffled_decay_and_uniform_widths_lose():
     r = {k: v["norm"] for k, v in res.items()}
     assert r["ema"] < 0.9 * r["rel_range"] and r["ema"] < 0.9 * r["gamma_raw"]
     assert r["ema"] < r["decay"]   # decay alone (ranges ignored) loses too
+
+
+def test_equal_row_ranges_leave_decay_as_the_signal():
+    """Fig. 1d's two settings at C = 64, two bits: with row ranges evened out
+    the range-based key falls back to uniform widths, while decay-aware keys
+    keep their advantage."""
+    nat = experiments.ablation(heads=16, tokens=512, C=64, mean_bits=2.0, ranges="natural")
+    eq = experiments.ablation(heads=16, tokens=512, C=64, mean_bits=2.0, ranges="equal")
+    say(f"log-range spread natural {nat['range_spread']:.3f} equal {eq['range_spread']:.3f}; "
+        "equal ranges: " + ", ".join(f"{k} {v['norm']:.5f}" for k, v in eq.items()
+                                     if k != "range_spread"))
+    assert eq["range_spread"] < 0.7 * nat["range_spread"]
+    assert eq["ema"]["norm"] < 0.75 * eq["rel_range"]["norm"]
+    assert eq["ema"]["norm"] < 0.75 * eq["uniform"]["norm"]

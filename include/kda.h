@@ -260,8 +260,15 @@ int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode,
 /* Prefill of T tokens with a write-back after every C-th token and after the
  * last one (Sec. 2: once per prefill chunk).  With cfg->chunked, C must be
  * at most 64 (KDA_ERR_ARG otherwise) and the workspace (kda_workspace_bytes
- * of the same config) also holds the per-chunk records of up to 16 chunks
- * per head (about 93 KB per chunk and head at d_k = 128).
+ * of the same config) also holds the per-chunk records of two groups of up
+ * to 16 chunks per head (about 93 KB per chunk and head at d_k = 128).  The
+ * chunked form prepares the next group on a second stream of the library
+ * (one per device, created by the first chunked call made outside graph
+ * capture) beside the current group's intervals on `stream`, joined to
+ * `stream` with events before the call's last interval; captured into a
+ * graph, that work becomes branches of the graph.  Calls on one device take
+ * the same side stream in turn; a first call made while `stream` is being
+ * captured uses `stream` alone.
  * In:  q, k [B][T][H][d_k] bf16 (raw 16-bit patterns); v [B][T][H][d_v] bf16;
  *      s [B][T][H][d_k] f32 (or [B][T][H]); beta [B][T][H] f32; gamma as in
  *      kda_step.  In/out: records.  Out: o [B][T][H][d_v] f32. */

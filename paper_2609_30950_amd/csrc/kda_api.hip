@@ -33,10 +33,11 @@ WsLayout ws_layout(const kda_config* cfg) {
   // decode: the token's vectors w (d_v), a and g (d_k) per head
   w.hv_off = up256(w.gam_off + rows * sizeof(double));
   w.chunk_off = up256(w.hv_off + (size_t)cfg->B * cfg->H * (cfg->d_v + 2 * cfg->d_k) * sizeof(float));
-  // chunked prefill: the records of one group of chunks
+  // chunked prefill: the records of two groups of chunks (the next group is
+  // prepared while the current one is applied)
   const int nbh = cfg->B * cfg->H;
   const size_t chunk =
-      cfg->chunked ? (size_t)kda::chunk_group(nbh) * nbh * kda::chunk_record_bytes(cfg->d_k) : 0;
+      cfg->chunked ? (size_t)2 * kda::chunk_group(nbh) * nbh * kda::chunk_record_bytes(cfg->d_k) : 0;
   w.total = up256(w.chunk_off + chunk);
   return w;
 }

@@ -43,6 +43,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "kda_device.hpp"
 #include "kda_kernels.hpp"
 #include "kda_profile.hpp"
@@ -136,14 +138,16 @@ struct PrepSmem {
   float beta[CT];
 };
 
+// The state-independent parts of one chunk of one head (unit = chunk of the
+// group * B H + head); all threads of the block call it.
 template <int DK>
-__global__ void __launch_bounds__(NTP) k_chunk_prep(KParams p, int C, uint8_t* cws) {
+__device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws, int unit,
+                                          PrepSmem<DK>& sm) {
   using CW = ChunkWs<DK>;
   using SM = PrepSmem<DK>;
   constexpr int SEGS = SM::SEGS, SEGL = CT / SEGS;
-  __shared__ SM sm;
   const int nbh = p.B * p.H;
-  const int cg = blockIdx.x / nbh, bh = blockIdx.x % nbh;
+  const int cg = unit / nbh, bh = unit % nbh;
   const int b = bh / p.H, h = bh % p.H;
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
   const int tok0 = p.tok0 + cg * C;
@@ -461,6 +465,15 @@ __global__ void __launch_bounds__(NTP) k_chunk_prep(KParams p, int C, uint8_t* c
   }
 }
 
+// Units unit0 + blockIdx.x of a group.  Beside the per-interval kernels the
+// group is prepared by a series of launches of a few blocks each, which
+// leave compute units to the intervals running on the other stream.
+template <int DK>
+__global__ void __launch_bounds__(NTP) k_chunk_prep(KParams p, int C, uint8_t* cws, int unit0) {
+  __shared__ PrepSmem<DK> sm;
+  prep_unit<DK>(p, C, cws, unit0 + blockIdx.x, sm);
+}
+
 template <int DK>
 struct ApplySmem {
   static constexpr int SS = DK + 8;
@@ -667,26 +680,107 @@ int chunk_group(int nbh) {
   return g < 1 ? 1 : (g > 16 ? 16 : g);
 }
 
+// A second stream per device on which the preparation of the next group of
+// chunks runs while the current group's intervals run on the caller's
+// stream (the per-interval kernels fill only part of the chip).  Created on
+// first use, outside graph capture, and kept until the process ends; the
+// enqueue sequence of one call holds the device's lock, so calls from
+// several host threads do not interleave their event records.
+namespace {
+struct Side {
+  hipStream_t s = nullptr;
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};   // start/chain, prep x2, end
+  bool ok = false, tried = false;
+  std::mutex mu;
+};
+constexpr int MAX_DEV = 64;
+Side g_side[MAX_DEV];
+
+// The device's side stream, locked (nullptr: one-stream schedule).
+Side* side_for(hipStream_t st, std::unique_lock<std::mutex>& lk) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEV) return nullptr;
+  Side& sd = g_side[dev];
+  lk = std::unique_lock<std::mutex>(sd.mu);
+  if (!sd.tried) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+    sd.tried = true;
+    bool ok = hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking) == hipSuccess;
+    for (int i = 0; i < 4 && ok; ++i)
+      ok = hipEventCreateWithFlags(&sd.ev[i], hipEventDisableTiming) == hipSuccess;
+    sd.ok = ok;
+  }
+  return sd.ok ? &sd : nullptr;
+}
+}  // namespace
+
+// Blocks per preparation launch beside the intervals (one block fills a
+// compute unit: its LDS and registers).
+constexpr int PREP_SIDE_GRID = 128;
+
 template <int DK>
 static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
   const int nbh = p.B * p.H, nsl = p.dv / SLICE;
   const int nch = (p.T + C - 1) / C;
   const int gc = chunk_group(nbh);
+  const int ngr = (nch + gc - 1) / gc;
   const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
-  for (int g0 = 0; g0 < nch; g0 += gc) {
-    const int ng = nch - g0 < gc ? nch - g0 : gc;
-    p.tok0 = g0 * C;
-    hipError_t e = launch("prep", k_chunk_prep<DK>, nbh * ng, NTP, 0, st, p, C, p.ws_chunk);
-    if (e != hipSuccess) return e;
+  const size_t half = (size_t)gc * nbh * ChunkWs<DK>::bytes;   // one group's chunk records
+  std::unique_lock<std::mutex> lk;
+  Side* sd = ngr > 1 ? side_for(st, lk) : nullptr;
+  auto buf = [&](int g) { return p.ws_chunk + (sd ? (size_t)(g & 1) * half : 0); };
+  auto prep = [&](int g, hipStream_t s, bool side) {
+    KParams q = p;
+    q.tok0 = g * gc * C;
+    const int units = nbh * (nch - g * gc < gc ? nch - g * gc : gc);
+    const int step = side ? PREP_SIDE_GRID : units;
+    for (int u0 = 0; u0 < units; u0 += step) {
+      const hipError_t e = launch("prep", k_chunk_prep<DK>, units - u0 < step ? units - u0 : step,
+                                  NTP, 0, s, q, C, buf(g), u0);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  };
+  hipError_t e = prep(0, st, false);
+  if (e != hipSuccess) return e;
+  if (sd) {
+    // group 1 is prepared beside group 0's intervals
+    if ((e = hipEventRecord(sd->ev[0], st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(sd->s, sd->ev[0], 0)) != hipSuccess) return e;
+    if ((e = prep(1, sd->s, true)) != hipSuccess) return e;
+    if ((e = hipEventRecord(sd->ev[2], sd->s)) != hipSuccess) return e;
+  }
+  for (int g = 0; g < ngr; ++g) {
+    if (g > 0) {
+      if (sd) {
+        if ((e = hipStreamWaitEvent(st, sd->ev[1 + (g & 1)], 0)) != hipSuccess) return e;
+      } else if ((e = prep(g, st, false)) != hipSuccess) {
+        return e;
+      }
+    }
+    const int ng = nch - g * gc < gc ? nch - g * gc : gc;
     for (int c = 0; c < ng; ++c) {
-      p.tok0 = (g0 + c) * C;
+      p.tok0 = (g * gc + c) * C;
       p.ntk = (p.T - p.tok0) < C ? (p.T - p.tok0) : C;
       e = launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p,
-                 (const uint8_t*)(p.ws_chunk + (size_t)c * nbh * ChunkWs<DK>::bytes));
+                 (const uint8_t*)(buf(g) + (size_t)c * nbh * ChunkWs<DK>::bytes));
       if (e != hipSuccess) return e;
       e = launch_chunk_writeback(p, nsl, st);
       if (e != hipSuccess) return e;
     }
+    if (sd && g + 2 < ngr) {
+      // group g + 2 reuses this group's records once its intervals are done
+      if ((e = hipEventRecord(sd->ev[0], st)) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(sd->s, sd->ev[0], 0)) != hipSuccess) return e;
+      if ((e = prep(g + 2, sd->s, true)) != hipSuccess) return e;
+      if ((e = hipEventRecord(sd->ev[1 + (g & 1)], sd->s)) != hipSuccess) return e;
+    }
+  }
+  if (sd) {
+    // nothing of this call stays on the side stream after the caller's
+    if ((e = hipEventRecord(sd->ev[3], sd->s)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(st, sd->ev[3], 0)) != hipSuccess) return e;
   }
   return hipSuccess;
 }

@@ -165,12 +165,15 @@ def test_chunk_no_erase_d128():
     _one_interval(w, st0, W.tokens(w, 16, 16 + 64), oc, kc, "chunk no erasure")
 
 
-def test_multi_chunk_call_equals_single_interval_calls():
-    """T = 18 intervals of 64 plus a ragged 5 (two groups of 16 chunks at
-    B*H = 2): one call against 19 single-interval calls, bit for bit."""
+@pytest.mark.parametrize("n64", [18, 40])
+def test_multi_chunk_call_equals_single_interval_calls(n64):
+    """T = n64 intervals of 64 plus a ragged 5 (at B*H = 2 two groups of 16
+    chunks, or three: the third group's records reuse the first group's
+    space, prepared on the side stream once the first group's intervals are
+    done): one call against the single-interval calls, bit for bit."""
     w = W.sized(W.WORKLOADS["tiny"], bf16=True)
     kc, oc = _cfgs(w)
-    T = 18 * 64 + 5
+    T = n64 * 64 + 5
     xs = W.tokens(w, 0, T)
     st0 = step.zero_state(w.B, w.H, oc)
     recs, o, _ = _gpu_prefill(kc, w, st0, xs, 64)

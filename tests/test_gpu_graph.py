@@ -56,11 +56,13 @@ def test_captured_decode_step_replays_equal_eager_steps():
         assert same_r and same_o
 
 
-def test_captured_chunked_prefill_replays_equal_eager():
+@pytest.mark.parametrize("T", [150, 40 * 64 + 5])
+def test_captured_chunked_prefill_replays_equal_eager(T):
+    """T = 150: one group of chunks; T = 2565: three groups, the later ones
+    prepared on the library's side stream (branches of the captured graph)."""
     w = W.sized(W.WORKLOADS["tiny"], B=1, H=2, bf16=True)
     kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
                   b_min=w.b_min, b_max=w.b_max, chunked=1)
-    T = 150
     xs = W.tokens(w, 0, T)
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16).cuda()
     q, k, v = bf(xs["q"]), bf(xs["k"]), bf(xs["v"])

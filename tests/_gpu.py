@@ -57,3 +57,19 @@ def meaningful_equal(a, b, B, H, dk, dv, bmax):
         if ma.size != mb.size or not np.array_equal(ma, mb):
             bad.append(i)
     return bad
+
+
+def _up256(x):
+    return (x + 255) // 256 * 256
+
+
+def ws_state32(ws, w):
+    """float32 state after the last write-back interval, read from the
+    workspace (views in the order the library lays them out: EMA keys,
+    rate codes, widths, then the float32 state)."""
+    rows = w.B * w.H * w.dk
+    zr = _up256(rows * 8)
+    bits = _up256(zr + rows * 4)
+    s32 = _up256(bits + rows)
+    a = host(ws[s32:s32 + rows * w.dv * 4]).view(np.float32)
+    return a.reshape(w.B, w.H, w.dk, w.dv)

@@ -23,7 +23,7 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, stats, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes
+from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes, ws_state32
 
 pytestmark = pytest.mark.gpu
 
@@ -42,22 +42,6 @@ def _cfgs(w, scope=0, no_erase=False):
 
 def _bf16(a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16).cuda()
-
-
-def _up256(x):
-    return (x + 255) // 256 * 256
-
-
-def _ws_state32(ws, w):
-    """float32 state after the last write-back interval, read from the
-    workspace (views in the order the library lays them out: EMA keys,
-    rate codes, widths, then the float32 state)."""
-    rows = w.B * w.H * w.dk
-    zr = _up256(rows * 8)
-    bits = _up256(zr + rows * 4)
-    s32 = _up256(bits + rows)
-    a = host(ws)[s32:s32 + rows * w.dv * 4].view(np.float32)
-    return a.reshape(w.B, w.H, w.dk, w.dv)
 
 
 def _gpu_prefill(kc, w, st0, xs, C):
@@ -79,7 +63,7 @@ def _one_interval(w, st0, xs, oc, kc, label):
     """One write-back interval (T <= 64 tokens, C = 64)."""
     T = xs["q"].shape[1]
     recs, o, ws = _gpu_prefill(kc, w, st0, xs, 64)
-    Sg = _ws_state32(ws, w)
+    Sg = ws_state32(ws, w)
     og = host(o).reshape(w.B, T, w.H, w.dv)
     # float64 recurrence from the same dequantised start, on the bf16 inputs
     X = step.dequantize(st0).astype(np.float64)

@@ -5,7 +5,9 @@ budget) runs as one kda_step launch exactly as bench.py times it.  Sampled
 sequences start from oracle-made records (the others from the zero state:
 sequences are independent) and are compared one by one with the oracle.
 The long-context shape (Student-t values, 3-bit mean, window Gramian weights
-recomputed by kda_weights) is checked the same way at a reduced batch.
+recomputed by kda_weights) is checked the same way at a reduced batch.  The
+prefill workload (B=4, H=32, T=8192) runs as one kda_prefill call in both
+forms, with sampled write-back intervals checked against the oracle.
 """
 import numpy as np
 import pytest
@@ -13,8 +15,8 @@ import torch
 
 import paper_2609_30950_amd as K
 import workloads as W
-from oracle import record, stats, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes
+from oracle import recurrence, record, stats, step
+from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes, ws_state32
 
 pytestmark = pytest.mark.gpu
 
@@ -90,3 +92,67 @@ def test_long_context_window_weights_student_t():
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc,
                                               gamma=gam)
         _compare(bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), st, f"long t={t}")
+
+
+def _prefill_call(kc, w, xs, T):
+    """kda_prefill of tokens [0, T) from zero records, as bench.py calls it."""
+    recs = K.new_records(kc)
+    ws = K.new_workspace(kc)
+    o = torch.zeros(w.B * T * w.H * w.dv, dtype=torch.float32, device="cuda")
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a[:, :T])).to(torch.bfloat16).cuda()
+    K.kda_prefill(kc, T, w.C, recs, bf(xs["q"]), bf(xs["k"]), bf(xs["v"]),
+                  dev(np.ascontiguousarray(xs["s"][:, :T])), dev(np.ascontiguousarray(xs["beta"][:, :T])),
+                  o, ws)
+    return recs, o, ws
+
+
+@pytest.mark.parametrize("chunked", [1, 0])
+def test_prefill_full_size_sampled_intervals(chunked):
+    """The prefill workload (B=4, H=32, d=128, T=8192, write-back every 64
+    tokens, bf16 inputs, 4-bit mean) in the launch configuration bench.py
+    times: one call over all tokens from the empty state.  Calls that stop
+    at an interval boundary must produce the same outputs for the tokens they
+    share, bit for bit (the chunked form's groups of chunks change with T);
+    the interval after such a boundary (the 64th and the last) is then checked
+    against the oracle from the GPU's own record at the boundary: outputs and
+    state against the float64 recurrence (16 u_bf16 for the chunked form's
+    bf16 products, 1e-3 for the float32 token-sequential form), and the
+    write-back of the GPU's float32 state bit for bit against the oracle's
+    allocation and quantiser."""
+    w = W.WORKLOADS["prefill"]
+    kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                  b_min=w.b_min, b_max=w.b_max, chunked=chunked)
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
+    tol = 16 * 2.0 ** -9 if chunked else 1e-3
+    xs = W.tokens(w, 0, w.T)
+    say(f"prefill full size chunked={chunked}: inputs ready")
+    _, o_full, _ = _prefill_call(kc, w, xs, w.T)
+    o_full = host(o_full).reshape(w.B, w.T, w.H, w.dv)
+    for t_end in (64 * 64, w.T):
+        t0 = t_end - w.C
+        r0, o0, _ = _prefill_call(kc, w, xs, t0)
+        r1, o1, ws1 = _prefill_call(kc, w, xs, t_end)
+        o1 = host(o1).reshape(w.B, t_end, w.H, w.dv)
+        assert np.array_equal(o1.view(np.uint32), o_full[:, :t_end].view(np.uint32))
+        assert np.array_equal(host(o0).reshape(w.B, t0, w.H, w.dv).view(np.uint32),
+                              o_full[:, :t0].view(np.uint32))
+        st0 = bytes_to_state(host(r0), w.B, w.H, w.dk, w.dv, w.b_max)
+        X = step.dequantize(st0).astype(np.float64)
+        m, e = step.ema_start(st0)
+        ot = np.zeros((w.B, w.C, w.H, w.dv))
+        for j, t in enumerate(range(t0, t_end)):
+            x = {n: a[:, t] for n, a in xs.items()}
+            X, ot[:, j] = recurrence.truth_step_rowform(X, x["q"], x["k"], x["v"], x["s"], x["beta"])
+            m, e = stats.ema_update(m, e, x["s"], x["k"], np.asarray(x["beta"])[..., None], oc.span)
+        og = o1[:, t0:t_end]
+        Sg = ws_state32(ws1, w)
+        es = np.max(np.abs(Sg - X), axis=(2, 3)) / np.max(np.abs(X), axis=(2, 3))
+        eo = np.max(np.abs(og - ot), axis=(1, 3)) / np.max(np.abs(ot), axis=(1, 3))
+        say(f"interval [{t0}, {t_end}): state err {es.max():.2e}, output err {eo.max():.2e} "
+            f"(bound {tol:.1e})")
+        assert np.all(np.isfinite(Sg)) and es.max() <= tol and eo.max() <= tol
+        exp, _ = step.write_back(Sg, m, e, st0["ntok"] + w.C, oc)
+        got = bytes_to_state(host(r1), w.B, w.H, w.dk, w.dv, w.b_max)
+        for f in ("ntok", "widths", "z", "r16", "codes"):
+            assert np.array_equal(got[f], exp[f]), f
+        assert np.array_equal(got["scale"].view(np.uint16), exp["scale"].view(np.uint16))

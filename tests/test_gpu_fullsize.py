@@ -156,3 +156,66 @@ def test_prefill_full_size_sampled_intervals(chunked):
         for f in ("ntok", "widths", "z", "r16", "codes"):
             assert np.array_equal(got[f], exp[f]), f
         assert np.array_equal(got["scale"].view(np.uint16), exp["scale"].view(np.uint16))
+
+
+@pytest.mark.parametrize("name,heads", [("gdn2", 0), ("gdn6", 0), ("gdn2", 1), ("gdn6", 1)])
+def test_gdn_decode_full_batch_sampled_sequences(name, heads):
+    """The Gated-DeltaNet-shaped decode workloads (B=16, H=16, d=256, one
+    decay rate per head and token, mean 2 or 6 bits) as one kda_step launch,
+    with per-row widths or (heads = 1) one width per head and block scales:
+    sequences 0, 7 and 15 start from oracle-made records, the others from the
+    zero state, and the sampled ones are compared with the oracle."""
+    w = W.WORKLOADS[name]
+    if heads:
+        w = W.sized(w, b_min=2, G=w.dk)
+    kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                  b_min=w.b_min, b_max=w.b_max, decay_per_head=1, head_units=heads)
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                  unit="head" if heads else "row")
+    sel = [0, 7, 15]
+    warm = W.tokens(w, 0, 12)
+    xs = {n: a[sel] for n, a in warm.items()}
+    st0, _ = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
+    if heads:
+        slot = record.record_bytes_heads(w.dk, w.dv, w.b_max)
+        packed = np.concatenate([record.pack_heads(st0["ntok"][b, h], st0["width"][b, h],
+                                                   st0["bscale"][b, h], st0["z"][b, h],
+                                                   st0["r16"][b, h], st0["codes"][b, h], w.dk,
+                                                   w.dv, w.b_max)
+                                 for b in range(len(sel)) for h in range(w.H)])
+    else:
+        slot = record.record_bytes(w.dk, w.dv, w.b_max)
+        packed = state_to_bytes(st0, w.dk, w.dv, w.b_max)
+    recs = np.zeros((w.B, w.H * slot), np.uint8)
+    recs[sel] = packed.reshape(len(sel), -1)
+    recs_d = dev(recs.reshape(-1))
+    x = W.token(w, 12)
+    o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    K.kda_step(kc, recs_d, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"][..., 0]),
+               dev(x["beta"]), o, K.new_workspace(kc))
+    got = host(recs_d).reshape(w.B, w.H, slot)[sel]
+    og = host(o).reshape(w.B, w.H, w.dv)[sel]
+    xo = {n: a[sel] for n, a in x.items()}
+    X = step.dequantize(st0)
+    st1, o_or, _ = step.mirror_decode_step(st0, xo["q"], xo["k"], xo["v"], xo["s"], xo["beta"], oc)
+    label = f"{name} B=16 heads={heads} sampled"
+    if heads:
+        for b in range(len(sel)):
+            for h in range(w.H):
+                f = record.unpack_heads(got[b, h], w.dk, w.dv, w.b_max)
+                assert int(f["ntok"]) == int(st1["ntok"][b, h])
+                assert int(f["width"]) == int(st1["width"][b, h]), (b, h)
+                assert np.array_equal(np.asarray(f["bscale"]).view(np.uint16),
+                                      st1["bscale"][b, h].view(np.uint16)), (b, h)
+                assert np.array_equal(np.asarray(f["codes"]), st1["codes"][b, h]), (b, h)
+                assert np.array_equal(np.asarray(f["r16"]).view(np.uint16),
+                                      st1["r16"][b, h].view(np.uint16))
+                assert int(np.sum(np.asarray(f["z"]) != st1["z"][b, h])) <= 1
+        say(f"{label}: head widths {st1['width'].ravel().tolist()}")
+    else:
+        _compare(bytes_to_state(got.reshape(-1), len(sel), w.H, w.dk, w.dv, w.b_max), st1, label)
+    ot = step.truth_outputs(X, xo["q"], xo["k"], xo["v"], xo["s"], xo["beta"])
+    err = float(np.max(np.abs(og - ot)) / np.max(np.abs(ot)))
+    say(f"{label}: o normwise rel err vs float64 {err:.2e}")
+    assert err <= 1e-3
+    assert np.max(np.abs(og - o_or)) <= 1e-6 * np.max(np.abs(o_or))

@@ -219,3 +219,80 @@ def test_gdn_decode_full_batch_sampled_sequences(name, heads):
     say(f"{label}: o normwise rel err vs float64 {err:.2e}")
     assert err <= 1e-3
     assert np.max(np.abs(og - o_or)) <= 1e-6 * np.max(np.abs(o_or))
+
+
+def test_long_context_weights_full_size():
+    """Window weights of the long-context layer at full size (B=128, H=32,
+    d=128, a window of W=1024 tokens, C=1) as bench.py launches them: two
+    sequences' inputs tiled to 128 sequences.  The diagonal-erase estimate
+    (kda_weights) of every head against the oracle's float64 recursion, and
+    the exact Gramian recursion (kda_weights_exact) of sampled heads against
+    the oracle's matrix recursion."""
+    w = W.WORKLOADS["long"]
+    Wn = w.window
+    xs = W.tokens(W.sized(w, B=2), 0, Wn)
+    rep = w.B // 2
+    d = {n: dev(a).repeat((rep,) + (1,) * (a.ndim - 1)).contiguous() for n, a in xs.items()}
+    kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                  b_min=w.b_min, b_max=w.b_max)
+    g = torch.zeros(w.B * w.H * w.dk, dtype=torch.float64, device="cuda")
+    K.kda_weights(kc, Wn, 1, d["q"], d["s"], d["beta"], d["k"], g)
+    got = host(g).reshape(w.B, w.H, w.dk)
+    want = stats.window_gamma(np.moveaxis(xs["q"], 1, 0), np.moveaxis(xs["s"], 1, 0),
+                              np.moveaxis(xs["k"], 1, 0), np.moveaxis(xs["beta"], 1, 0), 1)
+    np.testing.assert_allclose(got, np.tile(want, (rep, 1, 1)), rtol=1e-12)
+    g.zero_()
+    K.kda_weights_exact(kc, Wn, 1, d["q"], d["s"], d["beta"], d["k"], g)
+    got = host(g).reshape(w.B, w.H, w.dk)
+    worst = 0.0
+    for b, h in ((0, 0), (1, 17), (127, 31)):
+        q = xs["q"][b % 2, :, h].astype(np.float64)
+        Fs = np.stack([stats.transition(xs["k"][b % 2, t, h], xs["s"][b % 2, t, h],
+                                        float(xs["beta"][b % 2, t, h])) for t in range(Wn)])
+        ref = stats.exact_window_gamma(q, Fs, 1)
+        worst = max(worst, float(np.max(np.abs(got[b, h] - ref) / np.abs(ref))))
+    say(f"long-context weights B=128 W=1024: exact Gramian max rel err {worst:.2e} (sampled heads)")
+    assert worst <= 1e-9
+
+
+def test_long_context_decode_full_batch_sampled_sequences():
+    """One decode step of the long-context workload at full batch (B=128,
+    H=32, d=128, mean 3 bits, widths [2, 8], Student-t values, weights given
+    by the caller): sequences 0, 64 and 127 start from oracle-made records
+    with window weights from their own inputs, the others from the zero
+    state with unit weights; the sampled ones are compared with the oracle."""
+    w = W.WORKLOADS["long"]
+    kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                  b_min=w.b_min, b_max=w.b_max)
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
+    sel = [0, 64, 127]
+    ws_ = W.sized(w, B=len(sel))
+    xs = W.tokens(ws_, 0, 32)
+    st0, _ = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
+    gam_sel = stats.window_gamma(np.moveaxis(xs["q"], 1, 0), np.moveaxis(xs["s"], 1, 0),
+                                 np.moveaxis(xs["k"], 1, 0), np.moveaxis(xs["beta"], 1, 0), 1)
+    gam = np.ones((w.B, w.H, w.dk))
+    gam[sel] = gam_sel
+    slot = record.record_bytes(w.dk, w.dv, w.b_max)
+    recs = np.zeros((w.B, w.H * slot), np.uint8)
+    recs[sel] = state_to_bytes(st0, w.dk, w.dv, w.b_max).reshape(len(sel), -1)
+    recs_d = dev(recs.reshape(-1))
+    x1 = W.token(ws_, 32)
+    x = {n: np.zeros((w.B,) + a.shape[1:], a.dtype) for n, a in x1.items()}
+    for n in x:
+        x[n][:] = x1[n][:1]          # unsampled sequences: any valid token
+        x[n][sel] = x1[n]
+    o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    K.kda_step(kc, recs_d, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
+               K.new_workspace(kc), gamma=dev(gam))
+    got = host(recs_d).reshape(w.B, w.H * slot)[sel].reshape(-1)
+    og = host(o).reshape(w.B, w.H, w.dv)[sel]
+    X = step.dequantize(st0)
+    st1, o_or, _ = step.mirror_decode_step(st0, x1["q"], x1["k"], x1["v"], x1["s"], x1["beta"], oc,
+                                           gamma=gam_sel)
+    _compare(bytes_to_state(got, len(sel), w.H, w.dk, w.dv, w.b_max), st1, "long B=128 sampled")
+    ot = step.truth_outputs(X, x1["q"], x1["k"], x1["v"], x1["s"], x1["beta"])
+    err = float(np.max(np.abs(og - ot)) / np.max(np.abs(ot)))
+    say(f"long B=128 sampled: o normwise rel err vs float64 {err:.2e}")
+    assert err <= 1e-3
+    assert np.max(np.abs(og - o_or)) <= 1e-6 * np.max(np.abs(o_or))

@@ -48,6 +48,11 @@ def budget(mean_bits, n_rows):
     return int(np.floor(F64(mean_bits) * F64(n_rows) + 0.5))
 
 
+# Rows per run of the group sum of squares (the paper fixes no summation
+# order; runs let a group of many rows be summed in parallel).
+RMS_RUN = 64
+
+
 def normalized_ranges(R, G):
     """R: [..., dk] float32 row maxima -> R~ float64 [..., dk]."""
     R = np.asarray(R, np.float32).astype(F64)
@@ -55,9 +60,14 @@ def normalized_ranges(R, G):
     assert dk % G == 0
     out = np.zeros_like(R)
     for g0 in range(0, dk, G):
+        # sum of squares in runs of RMS_RUN consecutive rows, each run summed
+        # in row order from zero and the run sums added in order
         acc = np.zeros(R.shape[:-1], F64)
-        for j in range(g0, g0 + G):
-            acc = acc + R[..., j] * R[..., j]
+        for c0 in range(g0, g0 + G, RMS_RUN):
+            part = np.zeros(R.shape[:-1], F64)
+            for j in range(c0, min(c0 + RMS_RUN, g0 + G)):
+                part = part + R[..., j] * R[..., j]
+            acc = acc + part
         rms = np.sqrt(acc / F64(G))
         with np.errstate(divide="ignore", invalid="ignore"):
             rt = R[..., g0:g0 + G] / rms[..., None]

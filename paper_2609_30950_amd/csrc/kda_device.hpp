@@ -16,6 +16,7 @@ constexpr int ROW_BLOCK = 32;   // rows per sequential fma chain (one wave)
 constexpr int SEG = 64;         // columns per sequential error chain
 constexpr int N_FIT = 16;       // clip factors f = (5 + m) / 20
 constexpr int MAX_B = 16;
+constexpr int RMS_RUN = 64;     // rows per run of a group's sum of squares (runs in order)
 
 // Record layout of one (sequence, head) slot; identical on host and device.
 struct Layout {

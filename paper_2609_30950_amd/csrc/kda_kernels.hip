@@ -485,30 +485,43 @@ __device__ __forceinline__ void row_rates(const KParams& p, int bh, StatSmem<DK>
   }
 }
 
-// Weights c = Gamma R~^2 from the row ranges st.R (group RMS in float64,
-// rows summed in order).  The caller has synchronised after writing st.R.
+// Sum of squares of the float32 values x[r0..r1) in float64, in order; with
+// 16-byte aligned bounds the reads are issued four values at a time ahead of
+// the sequential sum.
+__device__ __forceinline__ double run_sumsq(const float* x, int r0, int r1) {
+  double acc = 0.0;
+  int j = r0;
+  if (((r0 | r1) & 3) == 0) {
+    const float4* x4 = (const float4*)(x + r0);
+#pragma unroll 4
+    for (; j < r1; j += 4) {
+      const float4 v = x4[(j - r0) >> 2];
+      acc = acc + (double)v.x * (double)v.x;
+      acc = acc + (double)v.y * (double)v.y;
+      acc = acc + (double)v.z * (double)v.z;
+      acc = acc + (double)v.w * (double)v.w;
+    }
+  }
+  for (; j < r1; ++j) acc = acc + (double)x[j] * (double)x[j];
+  return acc;
+}
+
+// Weights c = Gamma R~^2 from the row ranges st.R (group RMS in float64: the
+// squares summed in runs of RMS_RUN rows, each run in row order, the run
+// sums in order).  The caller has synchronised after writing st.R.
 template <int DK>
 __device__ __forceinline__ void row_weights(const KParams& p, int bh, StatSmem<DK>& st, int t) {
-  if (t < DK && t % p.G == 0) {
+  const int G = p.G, runs = (G + RMS_RUN - 1) / RMS_RUN;
+  if (t < (DK / G) * runs) {
+    const int g = t / runs, r0 = g * G + (t % runs) * RMS_RUN;
+    st.c[t] = run_sumsq(st.R, r0, min(r0 + RMS_RUN, (g + 1) * G));   // run sums, in the
+    // space of the weights until those are formed
+  }
+  __syncthreads();
+  if (t < DK / G) {
     double acc = 0.0;
-    int j = 0;
-    if ((p.G & 3) == 0) {
-      // 16-byte reads issued ahead of the sequential sum (t is a multiple of 4)
-      const float4* R4 = (const float4*)(st.R + t);
-#pragma unroll 4
-      for (; j < p.G; j += 4) {
-        const float4 v = R4[j >> 2];
-        acc = acc + (double)v.x * (double)v.x;
-        acc = acc + (double)v.y * (double)v.y;
-        acc = acc + (double)v.z * (double)v.z;
-        acc = acc + (double)v.w * (double)v.w;
-      }
-    }
-    for (; j < p.G; ++j) {
-      const double R = (double)st.R[t + j];
-      acc = acc + R * R;
-    }
-    st.rms[t / p.G] = sqrt(acc / (double)p.G);
+    for (int k = 0; k < runs; ++k) acc = acc + st.c[t * runs + k];
+    st.rms[t] = sqrt(acc / (double)G);
   }
   __syncthreads();
   if (t < DK) {
@@ -1287,26 +1300,17 @@ __global__ void __launch_bounds__(1024) k_alloc_slices(KParams p, int N, int nsl
     R[n] = m;
   }
   __syncthreads();
-  const int G = p.G;
+  const int G = p.G, runs = (G + RMS_RUN - 1) / RMS_RUN;
+  // group RMS: squares summed in runs of RMS_RUN rows (each in row order),
+  // the run sums (held in c until the weights are formed) added in order
+  for (int u = tid; u < (N / G) * runs; u += nt) {
+    const int g = u / runs, r0 = g * G + (u % runs) * RMS_RUN;
+    c[u] = run_sumsq(R, r0, min(r0 + RMS_RUN, (g + 1) * G));
+  }
+  __syncthreads();
   for (int g = tid; g < N / G; g += nt) {
     double acc = 0.0;
-    const int r0 = g * G;
-    int j = 0;
-    if ((G & 3) == 0) {
-      const float4* R4 = (const float4*)(R + r0);
-#pragma unroll 4
-      for (; j < G; j += 4) {
-        const float4 v = R4[j >> 2];
-        acc = acc + (double)v.x * (double)v.x;
-        acc = acc + (double)v.y * (double)v.y;
-        acc = acc + (double)v.z * (double)v.z;
-        acc = acc + (double)v.w * (double)v.w;
-      }
-    }
-    for (; j < G; ++j) {
-      const double v = (double)R[r0 + j];
-      acc = acc + v * v;
-    }
+    for (int k = 0; k < runs; ++k) acc = acc + c[g * runs + k];
     rms[g] = sqrt(acc / (double)G);
   }
   __syncthreads();

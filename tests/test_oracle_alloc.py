@@ -87,3 +87,24 @@ def test_p12_groups_spanning_heads():
     for g in range(2):
         rms = np.sqrt(np.mean(Rt[:, 3 * dk * g:3 * dk * (g + 1)] ** 2, axis=1))
         np.testing.assert_allclose(rms, 1.0, rtol=1e-14)
+
+
+def test_group_rms_runs():
+    # the group sum of squares is formed in runs of 64 rows: for groups of at
+    # most 64 rows that is the plain row-order sum; for a group of 12 heads of
+    # 128 rows (1536) it stays within a few units of the exactly rounded sum
+    import math
+    rng = np.random.default_rng(15)
+    R = np.abs(rng.standard_normal((2, 1536)) * np.exp(rng.normal(0, 2, (2, 1536)))).astype(np.float32)
+    for G in (16, 64):
+        Rt = alloc.normalized_ranges(R, G)
+        for g0 in range(0, 1536, G):
+            acc = 0.0
+            for j in range(g0, g0 + G):
+                acc = acc + float(R[0, j]) * float(R[0, j])
+            assert np.array_equal(Rt[0, g0:g0 + G], R[0, g0:g0 + G].astype(np.float64) / np.sqrt(acc / G))
+    Rt = alloc.normalized_ranges(R, 1536)
+    for b in range(2):
+        exact = math.sqrt(math.fsum(float(r) * float(r) for r in R[b]) / 1536)
+        got = float(R[b, 0]) / Rt[b, 0]
+        assert abs(got - exact) <= 8 * np.spacing(exact)

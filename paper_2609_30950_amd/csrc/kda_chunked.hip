@@ -719,21 +719,53 @@ Side* side_for(hipStream_t st, std::unique_lock<std::mutex>& lk) {
 // compute unit: its LDS and registers).
 constexpr int PREP_SIDE_GRID = 128;
 
+// Chunks per group.  With a side stream the groups grow from one chunk
+// (1, 1, 2, 3, 5, 8, ... up to gc), so that the first interval starts after
+// one chunk's preparation and each later group's preparation (beside the
+// intervals) takes about as long as the previous group's intervals; without
+// one, groups of gc chunks.  Once a size reaches gc every later one is gc.
+static int group_size(int g, int gc, bool grow) {
+  if (!grow) return gc;
+  int a = 1, b = 1;
+  for (int j = 0; j < g && a < gc; ++j) {
+    const int n = a + b;
+    a = b;
+    b = n;
+  }
+  return a < gc ? a : gc;
+}
+static int group_first(int g, int gc, bool grow) {
+  int c0 = 0;
+  for (int i = 0; i < g; ++i) {
+    const int k = group_size(i, gc, grow);
+    c0 += k;
+    if (k == gc) return c0 + (g - 1 - i) * gc;
+  }
+  return c0;
+}
+
 template <int DK>
 static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
   const int nbh = p.B * p.H, nsl = p.dv / SLICE;
   const int nch = (p.T + C - 1) / C;
   const int gc = chunk_group(nbh);
-  const int ngr = (nch + gc - 1) / gc;
   const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
-  const size_t half = (size_t)gc * nbh * ChunkWs<DK>::bytes;   // one group's chunk records
+  const size_t half = (size_t)gc * nbh * ChunkWs<DK>::bytes;   // records of up to gc chunks
   std::unique_lock<std::mutex> lk;
-  Side* sd = ngr > 1 ? side_for(st, lk) : nullptr;
+  Side* sd = nch > 1 ? side_for(st, lk) : nullptr;
+  const bool grow = sd != nullptr;
+  auto first = [&](int g) { return group_first(g, gc, grow); };
+  auto count = [&](int g) {   // at most gc: one half of the records
+    const int k = group_size(g, gc, grow), left = nch - first(g);
+    return k < left ? k : left;
+  };
+  int ngr = 0;
+  while (first(ngr) < nch) ++ngr;
   auto buf = [&](int g) { return p.ws_chunk + (sd ? (size_t)(g & 1) * half : 0); };
   auto prep = [&](int g, hipStream_t s, bool side) {
     KParams q = p;
-    q.tok0 = g * gc * C;
-    const int units = nbh * (nch - g * gc < gc ? nch - g * gc : gc);
+    q.tok0 = first(g) * C;
+    const int units = nbh * count(g);
     const int step = side ? PREP_SIDE_GRID : units;
     for (int u0 = 0; u0 < units; u0 += step) {
       const hipError_t e = launch("prep", k_chunk_prep<DK>, units - u0 < step ? units - u0 : step,
@@ -759,9 +791,9 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
         return e;
       }
     }
-    const int ng = nch - g * gc < gc ? nch - g * gc : gc;
+    const int g0 = first(g), ng = count(g);
     for (int c = 0; c < ng; ++c) {
-      p.tok0 = (g * gc + c) * C;
+      p.tok0 = (g0 + c) * C;
       p.ntk = (p.T - p.tok0) < C ? (p.T - p.tok0) : C;
       e = launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p,
                  (const uint8_t*)(buf(g) + (size_t)c * nbh * ChunkWs<DK>::bytes));

@@ -1,12 +1,32 @@
-"""GPU parity of kda_alloc_bits and kda_weights against the oracle."""
+"""GPU parity of kda_alloc_bits and kda_weights against the oracle; widths
+also against the plain optimality condition of the allocation
+(oracle/plain.py)."""
 import numpy as np
 import pytest
 import torch
 
 import paper_2609_30950_amd as K
 import workloads as W
-from oracle import alloc, stats
+from oracle import alloc, plain, stats
 from tests._gpu import dev, host, say
+
+
+def _plain_widths(gamma, R, G, scope, mean, bmin, bmax, got, label):
+    """The GPU's widths minimise sum c 4^-b over each scope unit, with keys
+    from plain group sums of squares."""
+    B, H, d = gamma.shape
+    if G <= d:
+        c = plain.keys(gamma, R, G)
+    else:
+        c = plain.keys(gamma.reshape(B, H * d), R.reshape(B, H * d), G).reshape(B, H, d)
+    units = [(b, slice(None)) for b in range(B)] if scope == 0 else \
+        [(b, h) for b in range(B) for h in range(H)]
+    ex = 0
+    for b, h in units:
+        res = plain.check_widths(c[b, h], got[b, h], mean, bmin, bmax)
+        assert res["ok"], f"{label}: unit {(b, h)} {res}"
+        ex += res["exempt"]
+    say(f"plain widths {label}: exempt rows {ex}")
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +70,7 @@ def test_alloc_bits_bit_exact(case):
     got = host(bits).reshape(B, H, d).astype(np.int64)
     want = _oracle_bits(gamma, R, G, scope, mean, bmin, bmax)
     assert np.array_equal(got, want), f"{np.sum(got != want)} widths differ"
+    _plain_widths(gamma, R, G, scope, mean, bmin, bmax, got, str(case))
 
 
 def test_alloc_all_zero_weights_fill_in_row_order():
@@ -138,3 +159,4 @@ def test_alloc_ties_and_ranges(kind, mean):
     got = host(bits).reshape(B, H, d).astype(np.int64)
     want = _oracle_bits(gamma, R, 64, 0, mean, 2, 8)
     assert np.array_equal(got, want), f"{kind}: {np.sum(got != want)} widths differ"
+    _plain_widths(gamma, R, 64, 0, mean, 2, 8, got, f"{kind} {mean}")

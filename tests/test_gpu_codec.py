@@ -1,11 +1,13 @@
-"""GPU parity of kda_pack_state / kda_unpack_state against the oracle (bit exact)."""
+"""GPU parity of kda_pack_state / kda_unpack_state against the oracle (bit
+exact), and the packed scales and codes against the plain definitions of the
+fit (oracle/plain.py)."""
 import numpy as np
 import pytest
 import torch
 
 import paper_2609_30950_amd as K
 from oracle import quant, record, stats
-from tests._gpu import dev, host, meaningful_equal, say
+from tests._gpu import bytes_to_state, dev, host, meaningful_equal, plain_check, say
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +64,8 @@ def test_pack_matches_oracle_bit_exact(case):
     want = _oracle_pack(S, bits, s_hat, r, 5, d, d, bmax)
     bad = meaningful_equal(got, want, B, H, d, d, bmax)
     assert not bad, f"records differ for slots {bad}"
+    plain_check(S, None, bytes_to_state(got, B, H, d, d, bmax), G=d, scope=0,
+                mean_bits=cfg.mean_bits, b_min=bmin, b_max=bmax, label=f"pack {case}")
 
 
 @pytest.mark.parametrize("case", CASES)

@@ -15,7 +15,9 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import quant, record, recurrence, stats, step
-from tests._gpu import bytes_to_state, dev, host, meaningful_equal, say, state_to_bytes
+from tests._gpu import (bytes_to_state, decode_gamma, decode_state_gpu, dev, host,
+                        meaningful_equal, plain_check, prefill_gamma, say, state_to_bytes,
+                        ws_state32)
 
 pytestmark = pytest.mark.gpu
 
@@ -112,11 +114,15 @@ def test_forced_decode_steps_d256(name, scope):
     for t in range(6, 8):
         x = W.token(w, t, base=base)
         recs = dev(state_to_bytes(st, D, D, w.b_max))
+        before = recs.clone()
         K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(_s_arg(x["s"], w)),
                    dev(x["beta"]), o, ws)
+        stg = bytes_to_state(host(recs), w.B, w.H, D, D, w.b_max)
+        plain_check(decode_state_gpu(kc, before, ws), decode_gamma(st, x, oc.span), stg, G=w.G,
+                    scope=scope, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                    label=f"{name} scope={scope} t={t}")
         X = step.dequantize(st)
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
-        stg = bytes_to_state(host(recs), w.B, w.H, D, D, w.b_max)
         dc = _codes_off(stg, st)
         ds = int(np.sum(stg["scale"].view(np.uint16) != st["scale"].view(np.uint16)))
         say(f"{name} scope={scope} t={t}: widths {int(np.sum(stg['widths'] != st['widths']))} "
@@ -146,10 +152,13 @@ def test_prefill_d256_ragged():
     T = 20
     o = torch.zeros(w.B * T * w.H * D, dtype=torch.float32, device="cuda")
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16).cuda()
+    ws = K.new_workspace(kc)
     K.kda_prefill(kc, T, 8, recs, bf(xs["q"]), bf(xs["k"]), bf(xs["v"]), dev(_s_arg(xs["s"], w)),
-                  dev(xs["beta"]), o, K.new_workspace(kc))
+                  dev(xs["beta"]), o, ws)
     st, o_or, _ = step.mirror_prefill(st0, xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], 8, oc)
     stg = bytes_to_state(host(recs), w.B, w.H, D, D, w.b_max)
+    plain_check(ws_state32(ws, w), prefill_gamma(st0, xs, 8, oc.span), stg, G=w.G, scope=1,
+                mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max, label="prefill d=256")
     dc = _codes_off(stg, st)
     say(f"prefill d=256 C=8 T=20: codes {dc} of {stg['codes'].size}")
     assert np.array_equal(stg["ntok"], st["ntok"])

@@ -7,8 +7,15 @@ sequences are independent) and are compared one by one with the oracle.
 The long-context shape (Student-t values, 3-bit mean, window Gramian weights
 recomputed by kda_weights) is checked the same way at a reduced batch.  The
 prefill workload (B=4, H=32, T=8192) runs as one kda_prefill call in both
-forms, with sampled write-back intervals checked against the oracle.
+forms, with sampled write-back intervals checked against the oracle.  The
+decode step is also run from the benchmark's own prior records (512 decode
+tokens from the zero state on the GPU, as bench.py builds them).  Every
+write-back checked here is also checked against the plain definitions of
+widths, clip factors, scales and codes (oracle/plain.py) on the GPU's own
+float32 state.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -16,7 +23,8 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, record, stats, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes, ws_state32
+from tests._gpu import (bytes_to_state, decode_gamma, decode_state_gpu, dev, host, plain_check,
+                        plain_check_heads, say, state32_step_gpu, state_to_bytes, ws_state32)
 
 pytestmark = pytest.mark.gpu
 
@@ -52,14 +60,20 @@ def test_decode_full_batch_sampled_sequences():
     recs_d = dev(recs.reshape(-1))
     x = W.token(w, 24, base=base)
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    ws = K.new_workspace(kc)
+    before = recs_d.clone()
     K.kda_step(kc, recs_d, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
-               K.new_workspace(kc))
+               ws)
     got = host(recs_d).reshape(w.B, w.H * slot)[sel].reshape(-1)
     og = host(o).reshape(w.B, w.H, w.dv)[sel]
     xo = {n: a[sel] for n, a in x.items()}
     X = step.dequantize(st0)
     st1, o_or, _ = step.mirror_decode_step(st0, xo["q"], xo["k"], xo["v"], xo["s"], xo["beta"], oc)
-    _compare(bytes_to_state(got, len(sel), w.H, w.dk, w.dv, w.b_max), st1, "decode B=64 sampled")
+    stg = bytes_to_state(got, len(sel), w.H, w.dk, w.dv, w.b_max)
+    plain_check(decode_state_gpu(kc, before, ws, sel), decode_gamma(st0, xo, oc.span), stg,
+                G=w.G, scope=0, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                label="decode B=64 sampled")
+    _compare(stg, st1, "decode B=64 sampled")
     ot = step.truth_outputs(X, xo["q"], xo["k"], xo["v"], xo["s"], xo["beta"])
     err = float(np.max(np.abs(og - ot)) / np.max(np.abs(ot)))
     say(f"decode B=64 sampled: o normwise rel err vs float64 {err:.2e}")
@@ -87,11 +101,15 @@ def test_long_context_window_weights_student_t():
     base = W.base_rates(w)
     for t in range(w.window, w.window + 6):
         x = W.token(w, t, base=base)
+        before = recs.clone()
         K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
                    ws, gamma=dev(gam))
+        stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
+        plain_check(decode_state_gpu(kc, before, ws), gam, stg, G=w.G, scope=0,
+                    mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max, label=f"long t={t}")
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc,
                                               gamma=gam)
-        _compare(bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), st, f"long t={t}")
+        _compare(stg, st, f"long t={t}")
 
 
 def _prefill_call(kc, w, xs, T):
@@ -153,6 +171,9 @@ def test_prefill_full_size_sampled_intervals(chunked):
         assert np.all(np.isfinite(Sg)) and es.max() <= tol and eo.max() <= tol
         exp, _ = step.write_back(Sg, m, e, st0["ntok"] + w.C, oc)
         got = bytes_to_state(host(r1), w.B, w.H, w.dk, w.dv, w.b_max)
+        s_hat, r = stats.ema_rates(m, e)
+        plain_check(Sg, stats.mode_gamma(s_hat, r), got, G=w.G, scope=0, mean_bits=w.mean_bits,
+                    b_min=w.b_min, b_max=w.b_max, label=f"prefill interval [{t0}, {t_end})")
         for f in ("ntok", "widths", "z", "r16", "codes"):
             assert np.array_equal(got[f], exp[f]), f
         assert np.array_equal(got["scale"].view(np.uint16), exp["scale"].view(np.uint16))
@@ -191,14 +212,30 @@ def test_gdn_decode_full_batch_sampled_sequences(name, heads):
     recs_d = dev(recs.reshape(-1))
     x = W.token(w, 12)
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    ws = K.new_workspace(kc)
+    before = recs_d.clone()
     K.kda_step(kc, recs_d, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"][..., 0]),
-               dev(x["beta"]), o, K.new_workspace(kc))
+               dev(x["beta"]), o, ws)
     got = host(recs_d).reshape(w.B, w.H, slot)[sel]
     og = host(o).reshape(w.B, w.H, w.dv)[sel]
     xo = {n: a[sel] for n, a in x.items()}
     X = step.dequantize(st0)
     st1, o_or, _ = step.mirror_decode_step(st0, xo["q"], xo["k"], xo["v"], xo["s"], xo["beta"], oc)
     label = f"{name} B=16 heads={heads} sampled"
+    g_sel = decode_gamma(st0, xo, oc.span)
+    if heads:
+        stg = {k_: np.stack([np.stack([np.asarray(record.unpack_heads(got[b, h], w.dk, w.dv,
+                                                                      w.b_max)[k_])
+                                       for h in range(w.H)]) for b in range(len(sel))])
+               for k_ in ("width", "bscale", "codes")}
+        S_sel = state32_step_gpu(dataclasses.replace(kc, B=len(sel)), X, xo)
+        plain_check_heads(S_sel, g_sel, stg, mean_bits=w.mean_bits, b_min=w.b_min,
+                          b_max=w.b_max, label=label)
+    else:
+        plain_check(decode_state_gpu(kc, before, ws, sel), g_sel,
+                    bytes_to_state(got.reshape(-1), len(sel), w.H, w.dk, w.dv, w.b_max),
+                    G=w.G, scope=0, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                    label=label)
     if heads:
         for b in range(len(sel)):
             for h in range(w.H):
@@ -283,16 +320,85 @@ def test_long_context_decode_full_batch_sampled_sequences():
         x[n][:] = x1[n][:1]          # unsampled sequences: any valid token
         x[n][sel] = x1[n]
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    ws = K.new_workspace(kc)
+    before = recs_d.clone()
     K.kda_step(kc, recs_d, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
-               K.new_workspace(kc), gamma=dev(gam))
+               ws, gamma=dev(gam))
     got = host(recs_d).reshape(w.B, w.H * slot)[sel].reshape(-1)
     og = host(o).reshape(w.B, w.H, w.dv)[sel]
     X = step.dequantize(st0)
     st1, o_or, _ = step.mirror_decode_step(st0, x1["q"], x1["k"], x1["v"], x1["s"], x1["beta"], oc,
                                            gamma=gam_sel)
-    _compare(bytes_to_state(got, len(sel), w.H, w.dk, w.dv, w.b_max), st1, "long B=128 sampled")
+    stg = bytes_to_state(got, len(sel), w.H, w.dk, w.dv, w.b_max)
+    plain_check(decode_state_gpu(kc, before, ws, sel), gam_sel, stg, G=w.G, scope=0,
+                mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max, label="long B=128 sampled")
+    _compare(stg, st1, "long B=128 sampled")
     ot = step.truth_outputs(X, x1["q"], x1["k"], x1["v"], x1["s"], x1["beta"])
     err = float(np.max(np.abs(og - ot)) / np.max(np.abs(ot)))
     say(f"long B=128 sampled: o normwise rel err vs float64 {err:.2e}")
     assert err <= 1e-3
     assert np.max(np.abs(og - o_or)) <= 1e-6 * np.max(np.abs(o_or))
+
+
+def test_decode_from_bench_prior_records():
+    """The decode workload from the records the benchmark times: 512 decode
+    tokens from the zero state run by the library (as bench.py builds its
+    prior state), then three more steps; for sampled sequences each step is
+    compared with the oracle started from the GPU's own records of that step
+    (widths, scales and codes bit for bit, rate codes counted in the
+    mismatch rate, outputs against float64), and checked against the plain
+    definitions."""
+    w = W.WORKLOADS["decode"]
+    kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
+                  b_min=w.b_min, b_max=w.b_max)
+    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
+    base = W.base_rates(w)
+    recs = K.new_records(kc)
+    ws = K.new_workspace(kc)
+    o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
+    warm = 512
+    for t in range(warm):
+        x = {n: torch.from_numpy(a).cuda() for n, a in W.token(w, t, base=base).items()}
+        K.kda_step(kc, recs, x["q"], x["k"], x["v"], x["s"], x["beta"], o, ws)
+    torch.cuda.synchronize()
+    say(f"bench prior: {warm} warm-up decode tokens done")
+    sel = [0, 21, 42, 63]
+    slot = record.record_bytes(w.dk, w.dv, w.b_max)
+    bad = tot = 0
+    for t in range(warm, warm + 3):
+        x = W.token(w, t, base=base)
+        xo = {n: a[sel] for n, a in x.items()}
+        st0 = bytes_to_state(host(recs).reshape(w.B, w.H * slot)[sel].reshape(-1), len(sel), w.H,
+                             w.dk, w.dv, w.b_max)
+        before = recs.clone()
+        K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
+                   ws)
+        stg = bytes_to_state(host(recs).reshape(w.B, w.H * slot)[sel].reshape(-1), len(sel), w.H,
+                             w.dk, w.dv, w.b_max)
+        plain_check(decode_state_gpu(kc, before, ws, sel), decode_gamma(st0, xo, oc.span), stg,
+                    G=w.G, scope=0, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                    label=f"bench prior t={t}")
+        X = step.dequantize(st0)
+        st1, o_or, _ = step.mirror_decode_step(st0, xo["q"], xo["k"], xo["v"], xo["s"],
+                                               xo["beta"], oc)
+        for j, b in enumerate(sel):
+            one = {f: a[j:j + 1] for f, a in stg.items()}
+            ref = {f: a[j:j + 1] for f, a in st1.items()}
+            assert np.array_equal(one["ntok"], ref["ntok"])
+            assert np.array_equal(one["widths"], ref["widths"]), (t, b)
+            assert np.array_equal(one["scale"].view(np.uint16), ref["scale"].view(np.uint16)), (t, b)
+            assert np.array_equal(one["r16"].view(np.uint16), ref["r16"].view(np.uint16)), (t, b)
+            dc = int(np.sum(one["codes"] != ref["codes"]))
+            dz = int(np.sum(one["z"] != ref["z"]))
+            bad += dc + dz
+            tot += one["codes"].size + one["z"].size
+        hist = np.bincount(stg["widths"].ravel(), minlength=w.b_max + 1)[w.b_min:]
+        og = host(o).reshape(w.B, w.H, w.dv)[sel]
+        ot = step.truth_outputs(X, xo["q"], xo["k"], xo["v"], xo["s"], xo["beta"])
+        err = float(np.max(np.abs(og - ot)) / np.max(np.abs(ot)))
+        say(f"bench prior t={t}: widths {w.b_min}..{w.b_max}: {hist.tolist()}, "
+            f"o rel err vs float64 {err:.2e}")
+        assert err <= 1e-3
+        assert np.max(np.abs(og - o_or)) <= 1e-6 * np.max(np.abs(o_or))
+    say(f"bench prior: code and rate-code mismatch rate {bad / tot:.2e} ({bad} of {tot})")
+    assert bad / tot <= 1e-5

@@ -10,7 +10,7 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import record, step
-from tests._gpu import dev, host, say
+from tests._gpu import decode_gamma, dev, host, plain_check_heads, say, state32_step_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -76,8 +76,12 @@ def test_forced_decode_steps_heads(name, dk, H, mean):
         K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(_s_arg(x["s"], w)),
                    dev(x["beta"]), o, ws)
         X = step.dequantize(st)
+        stg = _from_bytes(host(recs), w)
+        plain_check_heads(state32_step_gpu(kc, X, x), decode_gamma(st, x, oc.span), stg,
+                          mean_bits=w.mean_bits, b_min=2, b_max=w.b_max,
+                          label=f"heads {name} d={dk} mean={mean} t={t}")
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
-        _check(_from_bytes(host(recs), w), st, f"heads {name} d={dk} mean={mean} t={t}")
+        _check(stg, st, f"heads {name} d={dk} mean={mean} t={t}")
         og = host(o).reshape(o_or.shape)
         ot = step.truth_outputs(X, x["q"], x["k"], x["v"], x["s"], x["beta"])
         assert float(np.max(np.abs(og - ot)) / np.max(np.abs(ot))) <= 1e-3
@@ -133,9 +137,12 @@ def test_given_row_weights():
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
     K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(_s_arg(x["s"], w)),
                dev(x["beta"]), o, K.new_workspace(kc), gamma=dev(gamma))
+    stg = _from_bytes(host(recs), w)
+    plain_check_heads(state32_step_gpu(kc, step.dequantize(st), x), gamma, stg,
+                      mean_bits=w.mean_bits, b_min=2, b_max=w.b_max, label="given weights")
     st, _, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc,
                                        gamma=gamma)
-    _check(_from_bytes(host(recs), w), st, "given weights")
+    _check(stg, st, "given weights")
     assert len(set(st["width"].ravel().tolist())) > 1
 
 

@@ -13,7 +13,8 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, stats, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes
+from tests._gpu import (bytes_to_state, decode_gamma, decode_state_gpu, dev, host, plain_check,
+                        prefill_gamma, say, state_to_bytes, ws_state32)
 
 pytestmark = pytest.mark.gpu
 
@@ -52,8 +53,13 @@ def test_forced_decode_no_erasure_groups_across_heads(H, G):
     for t in range(16, 19):
         x = W.token(w, t)
         recs = dev(state_to_bytes(st, w.dk, w.dv, w.b_max))
+        before = recs.clone()
         K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"][..., 0]),
                    dev(x["beta"]), o, ws)
+        plain_check(decode_state_gpu(kc, before, ws), decode_gamma(st, x, oc.span, erase=False),
+                    bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), G=w.G, scope=0,
+                    mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                    label=f"mamba2 H={H} G={G} t={t}")
         X = step.dequantize(st)
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
         stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
@@ -79,8 +85,12 @@ def test_prefill_no_erasure_ragged():
                   dev(xs["v"], torch.bfloat16), dev(xs["s"][..., 0]), dev(xs["beta"]), o, ws)
     st, o_or, _ = step.mirror_prefill(step.zero_state(w.B, w.H, oc), xs["q"], xs["k"], xs["v"],
                                       xs["s"], xs["beta"], C, oc)
-    dc, n = _compare(bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), st,
-                     "mamba2 prefill")
+    stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
+    st0 = step.zero_state(w.B, w.H, oc)
+    plain_check(ws_state32(ws, w), prefill_gamma(st0, xs, C, oc.span, erase=False), stg, G=w.G,
+                scope=0, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                label="mamba2 prefill")
+    dc, n = _compare(stg, st, "mamba2 prefill")
     assert dc / n <= 1e-5
     og = host(o).reshape(o_or.shape)
     assert np.max(np.abs(og - o_or)) <= 1e-5 * np.max(np.abs(o_or))

@@ -1,5 +1,8 @@
 """GPU parity of kda_prefill (write-back every C tokens and after the last)
-against the oracle, from oracle-made starting records."""
+against the oracle, from oracle-made starting records.  The last write-back
+of every call is also checked against the plain definitions of widths,
+clip factors, scales and codes (oracle/plain.py) on the GPU's own float32
+state before it."""
 import numpy as np
 import pytest
 import torch
@@ -7,7 +10,8 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes
+from tests._gpu import (bytes_to_state, dev, host, plain_check, prefill_gamma, say,
+                        state_to_bytes, ws_state32)
 
 pytestmark = pytest.mark.gpu
 
@@ -31,11 +35,15 @@ def _run(w, st0, xs, C, scope=0):
     recs = dev(state_to_bytes(st0, w.dk, w.dv, w.b_max))
     o = torch.zeros(w.B * T * w.H * w.dv, dtype=torch.float32, device="cuda")
     s_arg = xs["s"] if w.decay != "head" else xs["s"][..., 0]
+    ws = K.new_workspace(kc)
     K.kda_prefill(kc, T, C, recs, _bf16(xs["q"]), _bf16(xs["k"]), _bf16(xs["v"]), dev(s_arg),
-                  dev(xs["beta"]), o, K.new_workspace(kc))
+                  dev(xs["beta"]), o, ws)
     st, o_or, diags = step.mirror_prefill(st0, xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], C, oc)
     stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
     og = host(o).reshape(o_or.shape)
+    plain_check(ws_state32(ws, w), prefill_gamma(st0, xs, C, oc.span), stg, G=w.G, scope=scope,
+                mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                label=f"prefill B={w.B} H={w.H} d={w.dk} T={T} C={C}")
     return stg, st, og, o_or
 
 

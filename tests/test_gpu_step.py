@@ -1,11 +1,15 @@
 """GPU parity of kda_step against the oracle.
 
 * 32-bit mode: float32 contract of the recurrence, free-running.
-* quantised decode, free-running from the zero state (tiny workload): both
-  sides run their own trajectories from identical inputs.
+* quantised decode, free-running from the zero state (tiny workload, all
+  256 tokens): both sides run their own trajectories from identical inputs.
 * oracle-forced single steps on the decode workload's shape (layer budget
   over 32 heads x 128 rows): the GPU starts from records the oracle produced
   and its output is compared with the oracle's next record.
+
+Every quantised step is also checked against the plain definitions of the
+widths, clip factors, scales and codes (oracle/plain.py) on the GPU's own
+float32 state, independently of the float32 contract's evaluation order.
 """
 import numpy as np
 import pytest
@@ -14,7 +18,8 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, step
-from tests._gpu import bytes_to_state, dev, host, meaningful_equal, say, state_to_bytes
+from tests._gpu import (bytes_to_state, decode_gamma, decode_state_gpu, dev, host,
+                        meaningful_equal, plain_check, say, state_to_bytes)
 
 pytestmark = pytest.mark.gpu
 
@@ -33,7 +38,8 @@ def _s_arg(x, w):
 
 
 def _compare(st_gpu, st_or, label):
-    """Field-wise comparison; returns (code mismatches, codes compared)."""
+    """Field-wise comparison; returns (code and rate-code mismatches, codes
+    and rate codes compared)."""
     assert np.array_equal(st_gpu["ntok"], st_or["ntok"]), label
     dw = int(np.sum(st_gpu["widths"] != st_or["widths"]))
     ds = int(np.sum(st_gpu["scale"].view(np.uint16) != st_or["scale"].view(np.uint16)))
@@ -45,7 +51,21 @@ def _compare(st_gpu, st_or, label):
     say(f"{label}: widths {dw} scales {ds} zcodes {dz} r16 {dr} codes {dc}")
     assert dw == 0 and ds == 0 and dr == 0, label
     assert dz <= max(1, st_gpu["z"].size // 100000), label
-    return dc, st_gpu["codes"].size
+    return dc + dz, st_gpu["codes"].size + st_gpu["z"].size
+
+
+def _step_plain(kc, oc, recs, x, o, ws, st_old, label, gamma=None):
+    """kda_step on device records, then the plain check of the new records
+    on the GPU's own float32 state; returns the decoded new records."""
+    before = recs.clone()
+    K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
+               ws, gamma=None if gamma is None else dev(gamma))
+    stg = bytes_to_state(host(recs), kc.B, kc.H, kc.d_k, kc.d_v, kc.b_max)
+    S = decode_state_gpu(kc, before, ws)
+    g = gamma if gamma is not None else decode_gamma(st_old, x, oc.span)
+    plain_check(S, g, stg, G=kc.group_rows, scope=kc.scope, mean_bits=kc.mean_bits,
+                b_min=kc.b_min, b_max=kc.b_max, label=label)
+    return stg
 
 
 @pytest.mark.parametrize("d", [64, 128])
@@ -75,9 +95,11 @@ def test_state32_step_matches_contract(d):
 
 
 def test_quantized_decode_free_running_tiny():
+    """The tiny workload's whole run (T = 256 decode tokens from the zero
+    state); the code-mismatch rate counts codes and rate codes."""
     w = W.WORKLOADS["tiny"]
     kc, oc = _cfgs(w)
-    T = 48
+    T = w.T
     recs = K.new_records(kc)
     ws = K.new_workspace(kc)
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
@@ -87,10 +109,9 @@ def test_quantized_decode_free_running_tiny():
     worst_o = 0.0
     for t in range(T):
         x = W.token(w, t, base=base)
-        K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o, ws)
+        stg = _step_plain(kc, oc, recs, x, o, ws, st, f"tiny t={t}")
         X = step.dequantize(st)
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
-        stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
         dc, n = _compare(stg, st, f"tiny t={t}")
         bad += dc
         tot += n
@@ -99,7 +120,8 @@ def test_quantized_decode_free_running_tiny():
         worst_o = max(worst_o, float(np.max(np.abs(og - ot)) / np.max(np.abs(ot))))
         if dc:
             st = stg      # continue each side from identical states only if needed
-    say(f"free-running tiny: code mismatch rate {bad / tot:.2e}, worst o rel err {worst_o:.2e}")
+    say(f"free-running tiny, {T} tokens: code mismatch rate {bad / tot:.2e} ({bad} of {tot}), "
+        f"worst o rel err {worst_o:.2e}")
     assert bad / tot <= 1e-5
     assert worst_o <= 1e-3
 
@@ -117,10 +139,9 @@ def test_oracle_forced_steps_decode_shape(scope):
     for t in range(24, 27):
         x = W.token(w, t, base=base)
         recs = dev(state_to_bytes(st, w.dk, w.dv, w.b_max))
-        K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o, ws)
+        stg = _step_plain(kc, oc, recs, x, o, ws, st, f"decode-shape scope={scope} t={t}")
         X = step.dequantize(st)
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
-        stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
         dc, n = _compare(stg, st, f"decode-shape scope={scope} t={t}")
         bad += dc
         tot += n
@@ -149,9 +170,8 @@ def test_forced_steps_narrow_widths(d, scope):
     for t in range(16, 19):
         x = W.token(w, t, base=base)
         recs = dev(state_to_bytes(st, w.dk, w.dv, w.b_max))
-        K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o, ws)
+        stg = _step_plain(kc, oc, recs, x, o, ws, st, f"narrow d={d} scope={scope} t={t}")
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
-        stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
         dc, n = _compare(stg, st, f"narrow d={d} scope={scope} t={t}")
         bad += dc
         tot += n
@@ -170,10 +190,8 @@ def test_window_gamma_input_and_span1():
     x = W.token(w, 8)
     recs = dev(state_to_bytes(st, w.dk, w.dv, w.b_max))
     o = torch.zeros(w.B * w.H * w.dv, dtype=torch.float32, device="cuda")
-    K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]), o,
-               K.new_workspace(kc), gamma=dev(gamma))
+    stg = _step_plain(kc, oc, recs, x, o, K.new_workspace(kc), st, "gamma input", gamma=gamma)
     st2, _, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc, gamma=gamma)
-    stg = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
     dc, n = _compare(stg, st2, "gamma input")
     assert dc == 0
 

@@ -10,7 +10,8 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import record, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes
+from tests._gpu import (bytes_to_state, decode_gamma, decode_state_gpu, dev, host, plain_check,
+                        prefill_gamma, say, state_to_bytes, ws_state32)
 
 pytestmark = pytest.mark.gpu
 
@@ -50,8 +51,13 @@ def test_decode_steps_every_mode(mode):
     for t in range(12, 14):
         x = W.token(w, t, base=base)
         recs = dev(state_to_bytes(st, w.dk, w.dv, w.b_max))
+        before = recs.clone()
         K.kda_step(kc, recs, dev(x["q"]), dev(x["k"]), dev(x["v"]), dev(x["s"]), dev(x["beta"]),
                    o, ws)
+        plain_check(decode_state_gpu(kc, before, ws), decode_gamma(st, x, oc.span, mode=mode),
+                    bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), G=w.G, scope=0,
+                    mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max, mode=mode,
+                    label=f"{mode} t={t}")
         st, o_or, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
         _check(bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), st, f"{mode} t={t}")
     if mode == "uniform":
@@ -69,9 +75,14 @@ def test_prefill_write_back_factor():
     st0 = step.zero_state(w.B, w.H, oc)
     recs = dev(state_to_bytes(st0, w.dk, w.dv, w.b_max))
     o = torch.zeros(w.B * 40 * w.H * w.dv, dtype=torch.float32, device="cuda")
+    ws = K.new_workspace(kc)
     K.kda_prefill(kc, 40, 16, recs, _bf(xs["q"]), _bf(xs["k"]), _bf(xs["v"]), dev(xs["s"]),
-                  dev(xs["beta"]), o, K.new_workspace(kc))
+                  dev(xs["beta"]), o, ws)
     st, _, _ = step.mirror_prefill(st0, xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], 16, oc)
+    plain_check(ws_state32(ws, w), prefill_gamma(st0, xs, 16, oc.span, mode="writeback"),
+                bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), G=w.G, scope=0,
+                mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max, mode="writeback",
+                label="prefill h^(16)")
     _check(bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max), st, "prefill h^(16)")
 
 

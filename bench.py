@@ -141,20 +141,24 @@ def run_state32_reference(w, args, K, torch):
 # Chunked prefill: one chunk record per chunk and head (bytes at d_k = d_v =
 # 128: Wk, Qhat, Ktil^T bf16 [64][128], A bf16 [64][64], Uv f32 [64][128],
 # gamma f32 [128], EMA sums f64 [4][128]).
-CHUNK_RECORD_BYTES = 3 * 64 * 128 * 2 + 64 * 64 * 2 + 64 * 128 * 4 + 128 * 4 + 4 * 128 * 8
+# per chunk and head at d = 128: Wk, Qhat, Ktil^T and A as bf16 hi and lo
+# planes, Uv float32, gamma_end float32, EMA sums float64
+CHUNK_RECORD_BYTES = 2 * (3 * 64 * 128 * 2 + 64 * 64 * 2) + 64 * 128 * 4 + 128 * 4 + 4 * 128 * 8
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def chunk_mfma_flops(dk):
     """bf16 MFMA flops issued per chunk and head (16x16x32 tiles, 16384 flops
-    each): prep forms L and A on the ten tiles of the lower 16-token blocks
-    (d_k / 32 steps each) and T diag(beta) [V | Khat] on six tile rows x
-    2 d_k / 16 columns; apply forms Wk S0 and Qhat S0 (4 x d_v/16 tiles,
-    d_k / 32 steps), A U (six tile rows) and Ktil^T U (d_k/16 x d_v/16 tiles,
-    two steps)."""
+    each; operands split into hi and lo parts take three products, or two
+    against an exact bf16 operand): prep forms L and A on the ten tiles of the
+    lower 16-token blocks (d_k / 32 steps each, three products), T diag(beta)
+    V (two) and T diag(beta) Khat (three) on six tile rows x d_k / 16
+    columns; apply forms Wk S0 and Qhat S0 (4 x d_v/16 tiles, d_k / 32
+    steps), A U (six tile rows) and Ktil^T U (d_k/16 x d_v/16 tiles, two
+    steps), three products each."""
     t = 16 * 16 * 32 * 2
-    prep = 10 * 2 * (dk // 32) * t + 6 * (2 * dk // 16) * t
-    apply_ = (2 * 4 * (dk // 16) * (dk // 32) + 6 * (dk // 16) + (dk // 16) * (dk // 16) * 2) * t
+    prep = 3 * 10 * 2 * (dk // 32) * t + (2 + 3) * 6 * (dk // 16) * t
+    apply_ = 3 * (2 * 4 * (dk // 16) * (dk // 32) + 6 * (dk // 16) + (dk // 16) * (dk // 16) * 2) * t
     return prep, apply_
 
 
@@ -175,10 +179,13 @@ def run_prefill(args, K, torch):
     recs = K.new_records(cfg)
     ws = K.new_workspace(cfg)
     o = torch.zeros(w.B * w.T * w.H * w.dv, dtype=torch.float32, device="cuda")
+    # the chunked form prepares later chunks on a second stream of ours
+    aux = torch.cuda.Stream() if args.chunked else None
 
     def run():
         recs.zero_()
-        K.kda_prefill(cfg, w.T, w.C, recs, dev["q"], dev["k"], dev["v"], dev["s"], dev["beta"], o, ws)
+        K.kda_prefill(cfg, w.T, w.C, recs, dev["q"], dev["k"], dev["v"], dev["s"], dev["beta"], o, ws,
+                      aux_stream=aux)
 
     run()
     torch.cuda.synchronize()

@@ -112,10 +112,12 @@ typedef struct {
                              recurrence (bit-reproducible contract); 1: each
                              write-back interval in the chunked (WY/UT) form
                              of eq. rule on bf16 MFMA with float32
-                             accumulation: the same state and outputs up to
-                             bf16 operand rounding, with C <= 64 and
-                             d_k <= 128.  The write-back quantiser is the
-                             same in both modes.                              */
+                             accumulation, every operand that is not exact
+                             in bf16 split into hi and lo bf16 parts (three
+                             products), so state and outputs agree with the
+                             recurrence to float32-level accuracy (not bit
+                             for bit), with C <= 64 and d_k <= 128.  The
+                             write-back quantiser is the same in both modes. */
   int32_t head_units;     /* 1: allocation units are heads (Sec. 3, Allocation
                              units, Gated DeltaNet): one width per head from
                              the layer budget over the H heads of a sequence
@@ -207,13 +209,23 @@ int kda_pack_state(const kda_config* cfg, const float* S, const uint8_t* bits,
                    const double* s_hat, const double* r, uint32_t tokens_seen,
                    void* records, void* stream);
 
-/* Decode records.  Out (each may be NULL): S [B][H][d_k][d_v] f32
+/* Decode records (Sec. 3, Levels and storage: x^ = code * Delta per row,
+ * one-bit rows +-mean|x|; rows addressed by prefix sums of the widths; rates
+ * from their log-uniform codes, Sec. 3, Decay-gate quantization).
+ * Out (each may be NULL): S [B][H][d_k][d_v] f32
  * dequantised state; bits [B][H][d_k] u8; s_hat [B][H][d_k] f64 decoded
- * rates; r [B][H][d_k] f64 decoded erase rates.  In 32-bit mode only S. */
+ * rates; r [B][H][d_k] f64 decoded erase rates.  In 32-bit mode only S.
+ * Records are only read; a zero slot decodes to the zero state. */
 int kda_unpack_state(const kda_config* cfg, const void* records, float* S,
                      uint8_t* bits, double* s_hat, double* r, void* stream);
 
-/* One decode token for B x H heads with a write-back (C = 1).
+/* One decode token for B x H heads with a write-back (C = 1): the gated
+ * delta rule of Sec. 2, eq. rule (KDA erase and write vectors, or none with
+ * no_erase), the output o = S^T q read before quantisation (Sec. 2,
+ * Accumulated readout error), then the write-back of Sec. 3: EMA rate
+ * statistics and weights (eq. weight), range normalisation, widths in the
+ * layer budget (eq. alloc), the fitted row quantiser (Levels and storage)
+ * and the record rewritten in place.
  * In:  q, k [B][H][d_k] f32 (k unit norm); v [B][H][d_v] f32;
  *      s [B][H][d_k] f32 (or [B][H] with decay_per_head), s > 0;
  *      beta [B][H] f32; gamma: NULL to weight rows by the EMA estimate of
@@ -224,8 +236,10 @@ int kda_step(const kda_config* cfg, void* records, const float* q,
              const double* gamma, float* o, void* ws, void* stream);
 
 /* kda_step in two phases, for callers that overlap a layer's write-back with
- * later work (the outputs precede the quantisation, Sec. 2, so the next
- * layer needs only the first phase).
+ * later work (the outputs precede the quantisation, Sec. 2, Accumulated
+ * readout error, so the next layer needs only the first phase).  The first
+ * phase is Sec. 2, eq. rule and the rate statistics, weights and widths of
+ * Sec. 3 (eq. weight, eq. alloc); the second is Sec. 3, Levels and storage.
  * kda_step_outputs: the token's recurrence, outputs o, rate statistics,
  *   weights and widths; what the write-back needs of the state after the
  *   token is left in ws (the token's vectors for d_k <= 128, else the float32
@@ -258,17 +272,14 @@ int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode,
                    float* s_out, void* stream);
 
 /* Prefill of T tokens with a write-back after every C-th token and after the
- * last one (Sec. 2: once per prefill chunk).  With cfg->chunked, C must be
- * at most 64 (KDA_ERR_ARG otherwise) and the workspace (kda_workspace_bytes
- * of the same config) also holds the per-chunk records of two groups of up
- * to 16 chunks per head (about 93 KB per chunk and head at d_k = 128).  The
- * chunked form prepares the next group on a second stream of the library
- * (one per device, created by the first chunked call made outside graph
- * capture) beside the current group's intervals on `stream`, joined to
- * `stream` with events before the call's last interval; captured into a
- * graph, that work becomes branches of the graph.  Calls on one device take
- * the same side stream in turn; a first call made while `stream` is being
- * captured uses `stream` alone.
+ * last one (Sec. 2: the state is written back once per prefill chunk; the
+ * recurrence is eq. rule and each write-back the quantiser of Sec. 3, as in
+ * kda_step).  With cfg->chunked, each write-back interval is evaluated in the
+ * chunked (WY/UT) form of eq. rule; C must then be at most 64 (KDA_ERR_ARG
+ * otherwise) and the workspace (kda_workspace_bytes of the same config) also
+ * holds the per-chunk records of two groups of up to 16 chunks per head
+ * (152 064 bytes per chunk and head at d_k = 128).  All work is enqueued on
+ * `stream`.
  * In:  q, k [B][T][H][d_k] bf16 (raw 16-bit patterns); v [B][T][H][d_v] bf16;
  *      s [B][T][H][d_k] f32 (or [B][T][H]); beta [B][T][H] f32; gamma as in
  *      kda_step.  In/out: records.  Out: o [B][T][H][d_v] f32. */
@@ -276,6 +287,23 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records,
                 const uint16_t* q, const uint16_t* k, const uint16_t* v,
                 const float* s, const float* beta, const double* gamma,
                 float* o, void* ws, void* stream);
+
+/* kda_prefill with a second stream of the caller's (Sec. 2, chunked
+ * prefill as above).  With cfg->chunked and more than one chunk, the
+ * chunk preparation of later groups of chunks runs on aux_stream beside the
+ * current group's write-back intervals on `stream`: the call orders the two
+ * streams with events it creates and destroys itself, and before returning
+ * (on every path, errors included) makes `stream` wait for all of its work on
+ * aux_stream, so the call's work is complete in `stream` order and, under
+ * graph capture on `stream`, every branch on aux_stream is joined back.  The
+ * caller owns aux_stream and must not enqueue other work on it during the
+ * call.  aux_stream NULL or equal to `stream`: the single-stream schedule of
+ * kda_prefill.  Without cfg->chunked aux_stream is not used.  The library
+ * keeps no streams, events or locks between calls. */
+int kda_prefill_aux(const kda_config* cfg, int32_t T, int32_t C, void* records,
+                    const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                    const float* s, const float* beta, const double* gamma,
+                    float* o, void* ws, void* stream, void* aux_stream);
 
 /* Diagnostics: per-kernel timing and work counts.  With KDA_PROFILE_EVENTS,
  * every kernel a call enqueues is bracketed by two hipEvents recorded on the

@@ -38,6 +38,8 @@ SIGNATURES = {
     "kda_step_outputs": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "kda_step_writeback": (ctypes.c_int, [_CFG, _P, _P, _P]),
     "kda_prefill": (ctypes.c_int, [_CFG, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kda_prefill_aux": (ctypes.c_int, [_CFG, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                       _P]),
     "kda_gate_quant": (ctypes.c_int, [_CFG, _I32, _I32, _I32, _P, _P, _P]),
     "kda_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "kda_profile_counters": (ctypes.c_int, [ctypes.POINTER(ctypes.c_ulonglong)]),

@@ -164,18 +164,23 @@ def kda_step_writeback(cfg, records, ws):
 _BF16 = (torch.bfloat16, torch.int16)   # bf16 values or their raw bit patterns
 
 
-def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None):
+def kda_prefill(cfg, T, C, records, q, k, v, s, beta, o, ws, gamma=None, aux_stream=None):
+    """aux_stream: a torch.cuda.Stream for the chunked form's preparation of
+    later chunks (kda_prefill_aux), or None for one stream."""
     n_s = cfg.B * T * cfg.H * (1 if cfg.decay_per_head else cfg.d_k)
     n_qk = cfg.B * T * cfg.H * cfg.d_k
-    _check(load().kda_prefill(
-        ctypes.byref(cfg.c()), int(T), int(C),
-        _ptr(records, torch.uint8, cfg.B * cfg.H * record_bytes(cfg), "records"),
-        _ptr(q, _BF16, n_qk, "q"), _ptr(k, _BF16, n_qk, "k"),
-        _ptr(v, _BF16, cfg.B * T * cfg.H * cfg.d_v, "v"), _ptr(s, torch.float32, n_s, "s"),
-        _ptr(beta, torch.float32, cfg.B * T * cfg.H, "beta"),
-        _ptr(gamma, torch.float64, _rows(cfg), "gamma"),
-        _ptr(o, torch.float32, cfg.B * T * cfg.H * cfg.d_v, "o"), _ptr(ws, torch.uint8, None, "ws"),
-        _stream()))
+    args = [ctypes.byref(cfg.c()), int(T), int(C),
+            _ptr(records, torch.uint8, cfg.B * cfg.H * record_bytes(cfg), "records"),
+            _ptr(q, _BF16, n_qk, "q"), _ptr(k, _BF16, n_qk, "k"),
+            _ptr(v, _BF16, cfg.B * T * cfg.H * cfg.d_v, "v"), _ptr(s, torch.float32, n_s, "s"),
+            _ptr(beta, torch.float32, cfg.B * T * cfg.H, "beta"),
+            _ptr(gamma, torch.float64, _rows(cfg), "gamma"),
+            _ptr(o, torch.float32, cfg.B * T * cfg.H * cfg.d_v, "o"),
+            _ptr(ws, torch.uint8, None, "ws"), _stream()]
+    if aux_stream is None:
+        _check(load().kda_prefill(*args))
+    else:
+        _check(load().kda_prefill_aux(*args, ctypes.c_void_p(aux_stream.cuda_stream)))
 
 
 # kda_weight_mode values, in the order of the oracle's stats.WEIGHT_MODES

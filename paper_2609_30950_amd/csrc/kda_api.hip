@@ -315,9 +315,9 @@ int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode,
                                            (hipStream_t)stream));
 }
 
-int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, const uint16_t* q,
-                const uint16_t* k, const uint16_t* v, const float* s, const float* beta,
-                const double* gamma, float* o, void* ws, void* stream) {
+int kda_prefill_aux(const kda_config* cfg, int32_t T, int32_t C, void* records, const uint16_t* q,
+                    const uint16_t* k, const uint16_t* v, const float* s, const float* beta,
+                    const double* gamma, float* o, void* ws, void* stream, void* aux_stream) {
   int need = 0;
   int st = check_cfg(cfg, &need);
   if (st != KDA_OK) return st;
@@ -340,10 +340,16 @@ int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, cons
   if (!cfg->state32) set_ws(p, cfg, ws);
   if (cfg->chunked) {
     if (C > 64) return KDA_ERR_ARG;
-    return hip_status(kda::launch_prefill_chunked(p, C, (hipStream_t)stream));
+    return hip_status(kda::launch_prefill_chunked(p, C, (hipStream_t)stream, (hipStream_t)aux_stream));
   }
   if (cfg->head_units) return hip_status(kda::launch_prefill_heads(p, C, (hipStream_t)stream));
   return hip_status(kda::launch_prefill(p, C, (hipStream_t)stream));
+}
+
+int kda_prefill(const kda_config* cfg, int32_t T, int32_t C, void* records, const uint16_t* q,
+                const uint16_t* k, const uint16_t* v, const float* s, const float* beta,
+                const double* gamma, float* o, void* ws, void* stream) {
+  return kda_prefill_aux(cfg, T, C, records, q, k, v, s, beta, gamma, o, ws, stream, nullptr);
 }
 
 }  // extern "C"

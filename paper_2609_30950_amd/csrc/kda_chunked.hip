@@ -43,8 +43,6 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include <mutex>
-
 #include "kda_device.hpp"
 #include "kda_kernels.hpp"
 #include "kda_profile.hpp"
@@ -77,6 +75,17 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
   return (uint32_t)bf16_rne(a) | ((uint32_t)bf16_rne(b) << 16);
 }
 
+// x = hi + lo with hi = bf16(x) and lo = bf16(x - hi) (x - hi is exact in
+// float32): the pair holds x to a relative 2^-18.
+__device__ __forceinline__ uint16_t bf16_lo(float x, uint16_t hi) { return bf16_rne(x - bf16_f32(hi)); }
+
+// Two values as packed hi and lo pairs.
+__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  const uint16_t ah = bf16_rne(a), bh = bf16_rne(b);
+  hi = (uint32_t)ah | ((uint32_t)bh << 16);
+  lo = (uint32_t)bf16_lo(a, ah) | ((uint32_t)bf16_lo(b, bh) << 16);
+}
+
 // D += A B for 16x16 tiles, K = 32: lane l supplies row l % 16 of A and
 // column l % 16 of B, each at k = 8 (l / 16) .. 8 (l / 16) + 7 (eight bf16
 // in one 16-byte register quad); it receives D rows 4 (l / 16) + r, r < 4,
@@ -84,6 +93,20 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 __device__ __forceinline__ f32x4 mma(uint4 a, uint4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// D += (Ah + Al)(Bh + Bl) to a relative 2^-17: the three products of the
+// split pairs (Al Bl, below 2^-18 of the product, is dropped).
+__device__ __forceinline__ f32x4 mma3(uint4 ah, uint4 al, uint4 bh, uint4 bl, f32x4 c) {
+  c = mma(al, bh, c);
+  c = mma(ah, bl, c);
+  return mma(ah, bh, c);
+}
+
+// D += (Ah + Al) B for an operand B exact in bf16.
+__device__ __forceinline__ f32x4 mma2(uint4 ah, uint4 al, uint4 b, f32x4 c) {
+  c = mma(al, b, c);
+  return mma(ah, b, c);
 }
 
 __device__ __forceinline__ float max16(float m) {
@@ -96,14 +119,17 @@ __device__ __forceinline__ float max16(float m) {
 }  // namespace
 
 // Byte layout of one chunk's record (per chunk and head), 256-byte aligned
-// fields; DV == DK.
+// fields; DV == DK.  Matrices that enter MFMA products as the A operand are
+// stored as bf16 hi and lo planes (hi = bf16(x), lo = bf16(x - hi)), so the
+// products keep float32-level accuracy (three bf16 MFMAs each).
 template <int DK>
 struct ChunkWs {
-  static constexpr size_t wk = 0;                         // bf16 [CT][DK]: T diag(beta) Khat
-  static constexpr size_t qh = wk + (size_t)CT * DK * 2;  // bf16 [CT][DK]: Qhat
-  static constexpr size_t ktt = qh + (size_t)CT * DK * 2; // bf16 [DK][CT]: Ktil^T
-  static constexpr size_t am = ktt + (size_t)DK * CT * 2; // bf16 [CT][CT]: A (lower, with diagonal)
-  static constexpr size_t uv = am + (size_t)CT * CT * 2;  // f32 [CT][DK]: T diag(beta) V
+  static constexpr size_t PL = (size_t)CT * DK * 2;       // one bf16 [CT][DK] plane
+  static constexpr size_t wk = 0;                         // bf16 [2][CT][DK]: T diag(beta) Khat
+  static constexpr size_t qh = wk + 2 * PL;               // bf16 [2][CT][DK]: Qhat
+  static constexpr size_t ktt = qh + 2 * PL;              // bf16 [2][DK][CT]: Ktil^T
+  static constexpr size_t am = ktt + 2 * PL;              // bf16 [2][CT][CT]: A (lower, with diagonal)
+  static constexpr size_t uv = am + (size_t)2 * CT * CT * 2;  // f32 [CT][DK]: T diag(beta) V
   static constexpr size_t gend = uv + (size_t)CT * DK * 4;// f32 [DK]: gamma_{n-1}
   static constexpr size_t ema = gend + (size_t)DK * 4;    // f64 [4][DK]: Q_m, Q_e, first samples
   static constexpr size_t bytes = (ema + (size_t)4 * DK * 8 + 255) / 256 * 256;
@@ -121,11 +147,12 @@ struct PrepSmem {
     struct {
       float T[CT][LS];                // (I + diag(beta) L)^-1
       float X[4][16][20];             // per-wave 16x16 products
+      uint16_t tbl[CT][TS];           // lo plane of T diag(beta)
     } t;
   } u0;
   uint16_t k[CT][KS], q[CT][KS];      // keys and queries
   uint16_t vt[DK][TS];                // V^T
-  uint16_t kht[DK][TS];               // Khat^T
+  uint16_t kht[2][DK][TS];            // Khat^T, hi and lo planes
   union {
     float L[CT][LS];                  // strictly lower L
     struct {
@@ -134,7 +161,7 @@ struct PrepSmem {
       double first[2][DK];            // first samples of the chunk
     } seg;
   } u1;
-  uint16_t tb[CT][TS];                // T diag(beta), bf16
+  uint16_t tb[CT][TS];                // T diag(beta), bf16 hi plane
   float beta[CT];
 };
 
@@ -242,7 +269,8 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
   }
   __syncthreads();
 
-  // Qhat (row-major), Khat^T (LDS), Ktil^T and gamma_{n-1}
+  // Qhat (row-major), Khat^T (LDS), Ktil^T and gamma_{n-1}, hi and lo
+  // planes; decay factors with the correctly rounded float32 exponential
   {
     uint16_t* qh = (uint16_t*)(out + CW::qh);
     for (int e = t; e < CT * V8; e += NTP) {
@@ -251,20 +279,25 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
       const float4 c0 = *(const float4*)&sm.u0.c[j][i0], c1 = *(const float4*)&sm.u0.c[j][i0 + 4];
       const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
       const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
-      uint32_t o[4];
+      uint32_t oh[4], ol[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        o[u] = pack2(bf16_f32((uint16_t)(qw[u] & 0xFFFFu)) * __expf(-cc[2 * u]),
-                     bf16_f32((uint16_t)(qw[u] >> 16)) * __expf(-cc[2 * u + 1]));
-      *(uint4*)&qh[j * DK + i0] = make_uint4(o[0], o[1], o[2], o[3]);
+        split2(bf16_f32((uint16_t)(qw[u] & 0xFFFFu)) * expf(-cc[2 * u]),
+               bf16_f32((uint16_t)(qw[u] >> 16)) * expf(-cc[2 * u + 1]), oh[u], ol[u]);
+      *(uint4*)&qh[j * DK + i0] = make_uint4(oh[0], oh[1], oh[2], oh[3]);
+      *(uint4*)&qh[CT * DK + j * DK + i0] = make_uint4(ol[0], ol[1], ol[2], ol[3]);
     }
     uint16_t* ktt = (uint16_t*)(out + CW::ktt);
     for (int e = t; e < CT * DK; e += NTP) {
       const int i = e / CT, j = e % CT;
       const float c = sm.u0.c[j][i], ce = sm.u0.c[CT - 1][i];
       const float kk = bf16_f32(sm.k[j][i]);
-      sm.kht[i][j] = bf16_rne(kk * __expf(-c));
-      ktt[e] = bf16_rne(kk * __expf(c - ce));
+      const float kh = kk * expf(-c), kt = kk * expf(c - ce);
+      const uint16_t hh = bf16_rne(kh), th = bf16_rne(kt);
+      sm.kht[0][i][j] = hh;
+      sm.kht[1][i][j] = bf16_lo(kh, hh);
+      ktt[e] = th;
+      ktt[CT * DK + e] = bf16_lo(kt, th);
     }
     if (t < DK) ((float*)(out + CW::gend))[t] = (float)exp(-(double)sm.u0.c[CT - 1][t]);
   }
@@ -304,15 +337,19 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
       const float cj[8] = {j0.x, j0.y, j0.z, j0.w, j1.x, j1.y, j1.z, j1.w};
       const uint4 kv = *(const uint4*)&sm.k[jr][i0], qv = *(const uint4*)&sm.q[jr][i0];
       const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w}, qw[4] = {qv.x, qv.y, qv.z, qv.w};
-      uint32_t ak[4], aq[4];
+      uint32_t akh[4], akl[4], aqh[4], aql[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float f0 = __expf(cr[2 * e] - cj[2 * e]), f1 = __expf(cr[2 * e + 1] - cj[2 * e + 1]);
-        ak[e] = pack2(bf16_f32((uint16_t)(kw[e] & 0xFFFFu)) * f0, bf16_f32((uint16_t)(kw[e] >> 16)) * f1);
-        aq[e] = pack2(bf16_f32((uint16_t)(qw[e] & 0xFFFFu)) * f0, bf16_f32((uint16_t)(qw[e] >> 16)) * f1);
+        const float f0 = expf(cr[2 * e] - cj[2 * e]), f1 = expf(cr[2 * e + 1] - cj[2 * e + 1]);
+        split2(bf16_f32((uint16_t)(kw[e] & 0xFFFFu)) * f0, bf16_f32((uint16_t)(kw[e] >> 16)) * f1,
+               akh[e], akl[e]);
+        split2(bf16_f32((uint16_t)(qw[e] & 0xFFFFu)) * f0, bf16_f32((uint16_t)(qw[e] >> 16)) * f1,
+               aqh[e], aql[e]);
       }
-      const uint4 AK = make_uint4(ak[0], ak[1], ak[2], ak[3]);
-      const uint4 AQ = make_uint4(aq[0], aq[1], aq[2], aq[3]);
+      const uint4 AKh = make_uint4(akh[0], akh[1], akh[2], akh[3]);
+      const uint4 AKl = make_uint4(akl[0], akl[1], akl[2], akl[3]);
+      const uint4 AQh = make_uint4(aqh[0], aqh[1], aqh[2], aqh[3]);
+      const uint4 AQl = make_uint4(aql[0], aql[1], aql[2], aql[3]);
 #pragma unroll
       for (int T = 0; T < 4; ++T) {
         if ((T & 1) != par || T > J || (T == J && diag_valu)) continue;
@@ -321,14 +358,16 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
         const float ct[8] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
         const uint4 tv = *(const uint4*)&sm.k[jt][i0];
         const uint32_t tw[4] = {tv.x, tv.y, tv.z, tv.w};
-        uint32_t bk[4];
+        uint32_t bkh[4], bkl[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          bk[e] = pack2(bf16_f32((uint16_t)(tw[e] & 0xFFFFu)) * __expf(ct[2 * e] - cr[2 * e]),
-                        bf16_f32((uint16_t)(tw[e] >> 16)) * __expf(ct[2 * e + 1] - cr[2 * e + 1]));
-        const uint4 BK = make_uint4(bk[0], bk[1], bk[2], bk[3]);
-        if (erase) accL[T] = mma(AK, BK, accL[T]);
-        accA[T] = mma(AQ, BK, accA[T]);
+          split2(bf16_f32((uint16_t)(tw[e] & 0xFFFFu)) * expf(ct[2 * e] - cr[2 * e]),
+                 bf16_f32((uint16_t)(tw[e] >> 16)) * expf(ct[2 * e + 1] - cr[2 * e + 1]), bkh[e],
+                 bkl[e]);
+        const uint4 BKh = make_uint4(bkh[0], bkh[1], bkh[2], bkh[3]);
+        const uint4 BKl = make_uint4(bkl[0], bkl[1], bkl[2], bkl[3]);
+        if (erase) accL[T] = mma3(AKh, AKl, BKh, BKl, accL[T]);
+        accA[T] = mma3(AQh, AQl, BKh, BKl, accA[T]);
       }
     }
 #pragma unroll
@@ -340,9 +379,13 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
         if (T > J) {
           sm.u1.L[j][tau] = 0.f;
           am[j * CT + tau] = 0;
+          am[CT * CT + j * CT + tau] = 0;
         } else if (T < J || !diag_valu) {
           sm.u1.L[j][tau] = tau < j ? accL[T][r] : 0.f;
-          am[j * CT + tau] = tau <= j ? bf16_rne(accA[T][r]) : (uint16_t)0;
+          const float a = tau <= j ? accA[T][r] : 0.f;
+          const uint16_t ah = bf16_rne(a);
+          am[j * CT + tau] = ah;
+          am[CT * CT + j * CT + tau] = bf16_lo(a, ah);
         }
       }
     }
@@ -353,13 +396,16 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
         float l = 0.f, a = 0.f;
         if (tau <= j) {
           for (int i = 0; i < DK; ++i) {
-            const float kt = bf16_f32(sm.k[tau][i]) * __expf(sm.u0.c[tau][i] - sm.u0.c[j][i]);
+            const float kt = bf16_f32(sm.k[tau][i]) * expf(sm.u0.c[tau][i] - sm.u0.c[j][i]);
             l = fmaf(bf16_f32(sm.k[j][i]), kt, l);
             a = fmaf(bf16_f32(sm.q[j][i]), kt, a);
           }
         }
         sm.u1.L[j][tau] = (tau < j && erase) ? l : 0.f;
-        am[j * CT + tau] = tau <= j ? bf16_rne(a) : (uint16_t)0;
+        const float av = tau <= j ? a : 0.f;
+        const uint16_t ah = bf16_rne(av);
+        am[j * CT + tau] = ah;
+        am[CT * CT + j * CT + tau] = bf16_lo(av, ah);
       }
     }
   }
@@ -421,7 +467,10 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
   __syncthreads();
   for (int e = t; e < CT * CT; e += NTP) {
     const int j = e / CT, m = e % CT;
-    sm.tb[j][m] = m <= j ? bf16_rne(sm.u0.t.T[j][m] * sm.beta[m]) : (uint16_t)0;
+    const float x = m <= j ? sm.u0.t.T[j][m] * sm.beta[m] : 0.f;
+    const uint16_t xh = bf16_rne(x);
+    sm.tb[j][m] = xh;
+    sm.u0.t.tbl[j][m] = bf16_lo(x, xh);
   }
   __syncthreads();
 
@@ -440,14 +489,16 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
 #pragma unroll
     for (int ks = 0; ks < CT / 32; ++ks) {
       if (32 * ks > 16 * J + 15) break;   // T is lower triangular
-      const uint4 a = *(const uint4*)&sm.tb[16 * J + (lane & 15)][32 * ks + k8];
+      const uint4 ah = *(const uint4*)&sm.tb[16 * J + (lane & 15)][32 * ks + k8];
+      const uint4 al = *(const uint4*)&sm.u0.t.tbl[16 * J + (lane & 15)][32 * ks + k8];
 #pragma unroll
       for (int ct = 0; ct < NC; ++ct) {
         const uint4 bv = *(const uint4*)&sm.vt[16 * (c0 + ct) + (lane & 15)][32 * ks + k8];
-        au[ct] = mma(a, bv, au[ct]);
+        au[ct] = mma2(ah, al, bv, au[ct]);
         if (erase) {
-          const uint4 bk = *(const uint4*)&sm.kht[16 * (c0 + ct) + (lane & 15)][32 * ks + k8];
-          aw[ct] = mma(a, bk, aw[ct]);
+          const uint4 bh = *(const uint4*)&sm.kht[0][16 * (c0 + ct) + (lane & 15)][32 * ks + k8];
+          const uint4 bl = *(const uint4*)&sm.kht[1][16 * (c0 + ct) + (lane & 15)][32 * ks + k8];
+          aw[ct] = mma3(ah, al, bh, bl, aw[ct]);
         }
       }
     }
@@ -459,7 +510,9 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
       for (int r = 0; r < 4; ++r) {
         const int j = 16 * J + 4 * (lane >> 4) + r, i = 16 * (c0 + ct) + (lane & 15);
         uv[j * DK + i] = au[ct][r];
-        wk[j * DK + i] = bf16_rne(aw[ct][r]);
+        const uint16_t wh = bf16_rne(aw[ct][r]);
+        wk[j * DK + i] = wh;
+        wk[CT * DK + j * DK + i] = bf16_lo(aw[ct][r], wh);
       }
     }
   }
@@ -478,21 +531,40 @@ template <int DK>
 struct ApplySmem {
   static constexpr int SS = DK + 8;
   static constexpr int US = CT + 8;
-  uint16_t s0t[SLICE][SS];   // S0 of the slice, transposed, bf16
-  uint16_t ut[SLICE][US];    // U of the slice, transposed, bf16
+  uint16_t s0t[2][SLICE][SS];   // S0 of the slice, transposed, bf16 hi and lo planes
+  uint16_t ut[2][SLICE][US];    // U of the slice, transposed, bf16 hi and lo planes
 };
+
+// Block of a write-back interval: (head, 64-column slice).  Workgroups are
+// dealt to the eight XCDs in turn, so the slices of one head are placed 8
+// block indices apart: they run on one XCD and the second read of the head's
+// chunk record hits that XCD's L2.  Heads past the last multiple of 8 map in
+// order.
+__device__ __forceinline__ void apply_block(int nbh, int nsl, int& bh, int& sl) {
+  constexpr int XCD = 8;
+  const int id = blockIdx.x, full = (nbh / XCD) * XCD * nsl;
+  if (id < full) {
+    sl = (id / XCD) % nsl;
+    bh = id % XCD + XCD * (id / (XCD * nsl));
+  } else {
+    bh = (nbh / XCD) * XCD + (id - full) / nsl;
+    sl = (id - full) % nsl;
+  }
+}
 
 // One write-back interval of one 64-column slice of one head: tokens
 // [p.tok0, p.tok0 + p.ntk) from the record's state; writes the outputs, the
 // float32 state, its per-slice row maxima and (slice 0) Gamma and the rate
-// codes, as the token-sequential stats kernel does.
+// codes, as the token-sequential stats kernel does.  Every product takes its
+// operands as hi and lo bf16 planes (mma3), float32 accumulation.
 template <int DK>
 __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw) {
   using CW = ChunkWs<DK>;
   constexpr int RT = DK / 64;            // 16-row state tiles per wave
   constexpr int KS = DK / 32;            // k-steps over the state's rows
   const int nsl = p.dv / SLICE;
-  const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
+  int bh, sl;
+  apply_block(p.B * p.H, nsl, bh, sl);
   const int b = bh / p.H, h = bh % p.H;
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
   const int n = p.ntk;
@@ -506,8 +578,8 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
 
-  // the chunk record's operands of this lane, loaded before the state's
-  // record so that both round trips overlap
+  // the chunk record's operands of this lane (hi and lo planes), loaded
+  // before the state's record so that both round trips overlap
   const uint16_t* wk = (const uint16_t*)(in + CW::wk);
   const uint16_t* qh = (const uint16_t*)(in + CW::qh);
   const uint16_t* am = (const uint16_t*)(in + CW::am);
@@ -515,25 +587,31 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   const float* uv = (const float*)(in + CW::uv);
   const float* gend = (const float*)(in + CW::gend);
   const bool erase = !p.no_erase;
-  uint4 fw[KS], fq[KS], fa[CT / 32], fk[RT][CT / 32];
+  constexpr int PL = CT * DK;            // elements of one plane
+  uint4 fw[2][KS], fq[2][KS], fa[2][CT / 32], fk[2][RT][CT / 32];
   float fu[4][4], fg[RT][4];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    fw[ks] = erase ? *(const uint4*)&wk[jrow * DK + 32 * ks + k8] : make_uint4(0u, 0u, 0u, 0u);
-    fq[ks] = *(const uint4*)&qh[jrow * DK + 32 * ks + k8];
-  }
+  for (int hl = 0; hl < 2; ++hl) {
 #pragma unroll
-  for (int ks = 0; ks < CT / 32; ++ks)
-    fa[ks] = 32 * ks <= 16 * w + 15 ? *(const uint4*)&am[jrow * CT + 32 * ks + k8]
-                                    : make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
+    for (int ks = 0; ks < KS; ++ks) {
+      fw[hl][ks] = erase ? *(const uint4*)&wk[hl * PL + jrow * DK + 32 * ks + k8]
+                         : make_uint4(0u, 0u, 0u, 0u);
+      fq[hl][ks] = *(const uint4*)&qh[hl * PL + jrow * DK + 32 * ks + k8];
+    }
 #pragma unroll
     for (int ks = 0; ks < CT / 32; ++ks)
-      fk[rt][ks] = *(const uint4*)&ktt[(16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
+      fa[hl][ks] = 32 * ks <= 16 * w + 15 ? *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8]
+                                          : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < CT / 32; ++ks)
+        fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
+  }
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
-  }
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
@@ -549,7 +627,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
 
   // S0 at this lane's state-tile positions: float32 gamma_{n-1} * S0 as the
-  // accumulator of S_n, bf16 S0^T in LDS for the products with S0
+  // accumulator of S_n, S0^T in LDS as hi and lo planes for the products
   f32x4 acc[RT][4];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -566,7 +644,9 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
         const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
         const float x = ((float)code + add) * mul;
         acc[rt][ct][r] = fg[rt][r] * x;
-        sm.s0t[c][i] = bf16_rne(x);
+        const uint16_t xh = bf16_rne(x);
+        sm.s0t[0][c][i] = xh;
+        sm.s0t[1][c][i] = bf16_lo(x, xh);
       }
     }
   }
@@ -583,18 +663,22 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
-      const uint4 bs = *(const uint4*)&sm.s0t[16 * ct + l16][32 * ks + k8];
-      if (erase) aw[ct] = mma(fw[ks], bs, aw[ct]);
-      ao[ct] = mma(fq[ks], bs, ao[ct]);
+      const uint4 bh_ = *(const uint4*)&sm.s0t[0][16 * ct + l16][32 * ks + k8];
+      const uint4 bl_ = *(const uint4*)&sm.s0t[1][16 * ct + l16][32 * ks + k8];
+      if (erase) aw[ct] = mma3(fw[0][ks], fw[1][ks], bh_, bl_, aw[ct]);
+      ao[ct] = mma3(fq[0][ks], fq[1][ks], bh_, bl_, ao[ct]);
     }
   }
-  // U = Uv - W, transposed into LDS as bf16
+  // U = Uv - W, transposed into LDS as hi and lo planes
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int j = 16 * w + 4 * (lane >> 4) + r, c = 16 * ct + l16;
-      sm.ut[c][j] = bf16_rne(fu[ct][r] - aw[ct][r]);
+      const float u = fu[ct][r] - aw[ct][r];
+      const uint16_t uh = bf16_rne(u);
+      sm.ut[0][c][j] = uh;
+      sm.ut[1][c][j] = bf16_lo(u, uh);
     }
   }
   __syncthreads();
@@ -605,8 +689,9 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     if (32 * ks > 16 * w + 15) break;
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
-      const uint4 bu = *(const uint4*)&sm.ut[16 * ct + l16][32 * ks + k8];
-      ao[ct] = mma(fa[ks], bu, ao[ct]);
+      const uint4 uh = *(const uint4*)&sm.ut[0][16 * ct + l16][32 * ks + k8];
+      const uint4 ul = *(const uint4*)&sm.ut[1][16 * ct + l16][32 * ks + k8];
+      ao[ct] = mma3(fa[0][ks], fa[1][ks], uh, ul, ao[ct]);
     }
   }
 #pragma unroll
@@ -626,8 +711,9 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     for (int ks = 0; ks < CT / 32; ++ks) {
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
-        const uint4 bu = *(const uint4*)&sm.ut[16 * ct + l16][32 * ks + k8];
-        acc[rt][ct] = mma(fk[rt][ks], bu, acc[rt][ct]);
+        const uint4 uh = *(const uint4*)&sm.ut[0][16 * ct + l16][32 * ks + k8];
+        const uint4 ul = *(const uint4*)&sm.ut[1][16 * ct + l16][32 * ks + k8];
+        acc[rt][ct] = mma3(fk[0][rt][ks], fk[1][rt][ks], uh, ul, acc[rt][ct]);
       }
     }
   }
@@ -680,39 +766,40 @@ int chunk_group(int nbh) {
   return g < 1 ? 1 : (g > 16 ? 16 : g);
 }
 
-// A second stream per device on which the preparation of the next group of
-// chunks runs while the current group's intervals run on the caller's
-// stream (the per-interval kernels fill only part of the chip).  Created on
-// first use, outside graph capture, and kept until the process ends; the
-// enqueue sequence of one call holds the device's lock, so calls from
-// several host threads do not interleave their event records.
+// Fork and join of the caller's auxiliary stream.  The preparation of the
+// next group of chunks runs on `aux` while the current group's intervals run
+// on `st` (the per-interval kernels fill only part of the chip).  The events
+// that order the two streams are created by the call and destroyed when it
+// returns; the library keeps no streams, events or locks of its own.  Once
+// `aux` has been forked from `st`, every return path (errors included)
+// records the end of the call's work on `aux` and makes `st` wait for it, so
+// nothing of the call is left on `aux` after `st` -- in particular no branch
+// of a graph being captured on `st` stays unjoined when the capture ends.
 namespace {
-struct Side {
-  hipStream_t s = nullptr;
-  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};   // start/chain, prep x2, end
-  bool ok = false, tried = false;
-  std::mutex mu;
-};
-constexpr int MAX_DEV = 64;
-Side g_side[MAX_DEV];
+struct AuxFork {
+  hipStream_t st = nullptr, aux = nullptr;
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};   // fork, prep x2, join
+  bool ok = false, forked = false;
 
-// The device's side stream, locked (nullptr: one-stream schedule).
-Side* side_for(hipStream_t st, std::unique_lock<std::mutex>& lk) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEV) return nullptr;
-  Side& sd = g_side[dev];
-  lk = std::unique_lock<std::mutex>(sd.mu);
-  if (!sd.tried) {
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
-    sd.tried = true;
-    bool ok = hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking) == hipSuccess;
+  AuxFork(hipStream_t s, hipStream_t a) : st(s), aux(a) {
+    if (aux == nullptr || aux == st) return;
+    ok = true;
     for (int i = 0; i < 4 && ok; ++i)
-      ok = hipEventCreateWithFlags(&sd.ev[i], hipEventDisableTiming) == hipSuccess;
-    sd.ok = ok;
+      ok = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming) == hipSuccess;
   }
-  return sd.ok ? &sd : nullptr;
-}
+  // aux waits for everything enqueued on st so far
+  hipError_t fork() {
+    hipError_t e = hipEventRecord(ev[0], st);
+    if (e == hipSuccess) e = hipStreamWaitEvent(aux, ev[0], 0);
+    if (e == hipSuccess) forked = true;
+    return e;
+  }
+  ~AuxFork() {
+    if (forked && hipEventRecord(ev[3], aux) == hipSuccess) (void)hipStreamWaitEvent(st, ev[3], 0);
+    for (int i = 0; i < 4; ++i)
+      if (ev[i] != nullptr) (void)hipEventDestroy(ev[i]);
+  }
+};
 }  // namespace
 
 // Blocks per preparation launch beside the intervals (one block fills a
@@ -745,15 +832,15 @@ static int group_first(int g, int gc, bool grow) {
 }
 
 template <int DK>
-static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
+static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_stream) {
   const int nbh = p.B * p.H, nsl = p.dv / SLICE;
   const int nch = (p.T + C - 1) / C;
   const int gc = chunk_group(nbh);
   const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
   const size_t half = (size_t)gc * nbh * ChunkWs<DK>::bytes;   // records of up to gc chunks
-  std::unique_lock<std::mutex> lk;
-  Side* sd = nch > 1 ? side_for(st, lk) : nullptr;
-  const bool grow = sd != nullptr;
+  AuxFork fk(st, nch > 1 ? aux_stream : nullptr);
+  const bool two = fk.ok;
+  const bool grow = two;
   auto first = [&](int g) { return group_first(g, gc, grow); };
   auto count = [&](int g) {   // at most gc: one half of the records
     const int k = group_size(g, gc, grow), left = nch - first(g);
@@ -761,7 +848,7 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
   };
   int ngr = 0;
   while (first(ngr) < nch) ++ngr;
-  auto buf = [&](int g) { return p.ws_chunk + (sd ? (size_t)(g & 1) * half : 0); };
+  auto buf = [&](int g) { return p.ws_chunk + (two ? (size_t)(g & 1) * half : 0); };
   auto prep = [&](int g, hipStream_t s, bool side) {
     KParams q = p;
     q.tok0 = first(g) * C;
@@ -776,17 +863,16 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
   };
   hipError_t e = prep(0, st, false);
   if (e != hipSuccess) return e;
-  if (sd) {
+  if (two && ngr > 1) {
     // group 1 is prepared beside group 0's intervals
-    if ((e = hipEventRecord(sd->ev[0], st)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(sd->s, sd->ev[0], 0)) != hipSuccess) return e;
-    if ((e = prep(1, sd->s, true)) != hipSuccess) return e;
-    if ((e = hipEventRecord(sd->ev[2], sd->s)) != hipSuccess) return e;
+    if ((e = fk.fork()) != hipSuccess) return e;
+    if ((e = prep(1, fk.aux, true)) != hipSuccess) return e;
+    if ((e = hipEventRecord(fk.ev[2], fk.aux)) != hipSuccess) return e;
   }
   for (int g = 0; g < ngr; ++g) {
     if (g > 0) {
-      if (sd) {
-        if ((e = hipStreamWaitEvent(st, sd->ev[1 + (g & 1)], 0)) != hipSuccess) return e;
+      if (two) {
+        if ((e = hipStreamWaitEvent(st, fk.ev[1 + (g & 1)], 0)) != hipSuccess) return e;
       } else if ((e = prep(g, st, false)) != hipSuccess) {
         return e;
       }
@@ -801,25 +887,19 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st) {
       e = launch_chunk_writeback(p, nsl, st);
       if (e != hipSuccess) return e;
     }
-    if (sd && g + 2 < ngr) {
+    if (two && g + 2 < ngr) {
       // group g + 2 reuses this group's records once its intervals are done
-      if ((e = hipEventRecord(sd->ev[0], st)) != hipSuccess) return e;
-      if ((e = hipStreamWaitEvent(sd->s, sd->ev[0], 0)) != hipSuccess) return e;
-      if ((e = prep(g + 2, sd->s, true)) != hipSuccess) return e;
-      if ((e = hipEventRecord(sd->ev[1 + (g & 1)], sd->s)) != hipSuccess) return e;
+      if ((e = fk.fork()) != hipSuccess) return e;
+      if ((e = prep(g + 2, fk.aux, true)) != hipSuccess) return e;
+      if ((e = hipEventRecord(fk.ev[1 + (g & 1)], fk.aux)) != hipSuccess) return e;
     }
   }
-  if (sd) {
-    // nothing of this call stays on the side stream after the caller's
-    if ((e = hipEventRecord(sd->ev[3], sd->s)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(st, sd->ev[3], 0)) != hipSuccess) return e;
-  }
-  return hipSuccess;
+  return hipSuccess;   // fk joins aux into st
 }
 
-hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st) {
-  if (p.dk == 64) return run_chunked<64>(p, C, st);
-  return run_chunked<128>(p, C, st);
+hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st, hipStream_t aux) {
+  if (p.dk == 64) return run_chunked<64>(p, C, st, aux);
+  return run_chunked<128>(p, C, st, aux);
 }
 
 }  // namespace kda

@@ -49,7 +49,7 @@ hipError_t launch_prefill(KParams p, int C, hipStream_t st);
 // workspace.
 hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st);
 // Chunked prefill (WY/UT form on MFMA), d_k = d_v in {64, 128}, C <= 64.
-hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st);
+hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st, hipStream_t aux);
 // Bytes of one chunk record (per chunk and head) and chunks per group for
 // B*H heads.
 size_t chunk_record_bytes(int dk);

@@ -1,20 +1,16 @@
 """GPU parity of the chunked (WY/UT, bf16 MFMA) prefill.
 
-The chunked form evaluates the same recurrence (eq. rule) with bf16 operands
-and float32 accumulation, so its state and outputs are compared with the
-float64 recurrence from the same starting record within a tolerance, and its
-write-back is compared bit for bit with the oracle's quantiser applied to the
-GPU's own float32 state (EMA statistics from the oracle's token-order
-recursion).  A multi-chunk call must equal the same chunks run one call at a
-time, bit for bit.
-
-Tolerance: every product in the chunk form has bf16-rounded operands (unit
-roundoff u = 2^-9); the longest chain is T (rounded) -> Wk, Uv (rounded) ->
-U = Uv - Wk S0 (rounded) -> Ktil^T U, about six roundings of relative size u
-on terms of the state's magnitude, with cancellation between Uv and Wk S0
-when the state already predicts v.  The bound used is 16 u = 3.1e-2 of the
-head's largest |S| (state) or largest |o| (outputs); observed errors are
-printed.
+The chunked form evaluates the same recurrence (eq. rule) in another order:
+products on bf16 MFMA with float32 accumulation, each operand that is not
+exact in bf16 split into hi and lo bf16 parts (relative 2^-18) and multiplied
+as three products.  Its state and outputs are compared with the float64
+recurrence from the same starting record within the benchmark spec's 1e-3 of the
+head's largest |S| (state) or largest |o| (outputs), normwise; observed
+errors are printed.  Its write-back is compared bit for bit with the oracle's
+quantiser applied to the GPU's own float32 state (EMA statistics from the
+oracle's token-order recursion), and checked against the plain definitions.
+A multi-chunk call must equal the same chunks run one call at a time, bit for
+bit.
 """
 import numpy as np
 import pytest
@@ -23,12 +19,11 @@ import torch
 import paper_2609_30950_amd as K
 import workloads as W
 from oracle import recurrence, stats, step
-from tests._gpu import bytes_to_state, dev, host, say, state_to_bytes, ws_state32
+from tests._gpu import bytes_to_state, dev, host, plain_check, say, state_to_bytes, ws_state32
 
 pytestmark = pytest.mark.gpu
 
-U_BF16 = 2.0 ** -9
-TOL = 16 * U_BF16
+TOL = 1e-3
 
 
 def _cfgs(w, scope=0, no_erase=False):
@@ -44,6 +39,16 @@ def _bf16(a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16).cuda()
 
 
+_AUX = []
+
+
+def _aux():
+    """The caller's second stream for the preparation of later chunks."""
+    if not _AUX:
+        _AUX.append(torch.cuda.Stream())
+    return _AUX[0]
+
+
 def _gpu_prefill(kc, w, st0, xs, C):
     T = xs["q"].shape[1]
     recs = dev(state_to_bytes(st0, w.dk, w.dv, w.b_max))
@@ -51,7 +56,7 @@ def _gpu_prefill(kc, w, st0, xs, C):
     ws = K.new_workspace(kc)
     s_arg = xs["s"] if w.decay != "head" else xs["s"][..., 0]
     K.kda_prefill(kc, T, C, recs, _bf16(xs["q"]), _bf16(xs["k"]), _bf16(xs["v"]), dev(s_arg),
-                  dev(xs["beta"]), o, ws)
+                  dev(xs["beta"]), o, ws, aux_stream=_aux())
     return recs, o, ws
 
 
@@ -90,6 +95,9 @@ def _one_interval(w, st0, xs, oc, kc, label):
     # the write-back of the GPU's own state, bit for bit
     exp, _ = step.write_back(Sg, m, e, st0["ntok"] + T, oc)
     got = bytes_to_state(host(recs), w.B, w.H, w.dk, w.dv, w.b_max)
+    s_hat, r = stats.ema_rates(m, e)
+    plain_check(Sg, stats.mode_gamma(s_hat, r), got, G=w.G, scope=kc.scope,
+                mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max, label=label)
     for f in ("ntok", "widths", "z", "r16", "codes"):
         assert np.array_equal(got[f], exp[f]), f
     assert np.array_equal(got["scale"].view(np.uint16), exp["scale"].view(np.uint16))
@@ -151,10 +159,11 @@ def test_chunk_no_erase_d128():
 
 @pytest.mark.parametrize("n64", [18, 40])
 def test_multi_chunk_call_equals_single_interval_calls(n64):
-    """T = n64 intervals of 64 plus a ragged 5 (at B*H = 2 two groups of 16
-    chunks, or three: the third group's records reuse the first group's
-    space, prepared on the side stream once the first group's intervals are
-    done): one call against the single-interval calls, bit for bit."""
+    """T = n64 intervals of 64 plus a ragged 5, in groups of chunks growing
+    from one to 16 (later groups' records reuse earlier groups' space,
+    prepared on the caller's second stream once those groups' intervals are
+    done): one call against the single-interval calls, bit for bit; and the
+    same call on one stream."""
     w = W.sized(W.WORKLOADS["tiny"], bf16=True)
     kc, oc = _cfgs(w)
     T = n64 * 64 + 5
@@ -176,6 +185,12 @@ def test_multi_chunk_call_equals_single_interval_calls(n64):
     say(f"multi-chunk: {len(parts)} intervals")
     assert np.array_equal(host(r), whole)
     assert np.array_equal(np.concatenate(parts, axis=1).view(np.uint32), o_whole.view(np.uint32))
+    r1 = dev(state_to_bytes(st0, w.dk, w.dv, w.b_max))
+    o1 = torch.zeros(w.B * T * w.H * w.dv, dtype=torch.float32, device="cuda")
+    K.kda_prefill(kc, T, 64, r1, _bf16(xs["q"]), _bf16(xs["k"]), _bf16(xs["v"]), dev(xs["s"]),
+                  dev(xs["beta"]), o1, K.new_workspace(kc))
+    assert np.array_equal(host(r1), whole)
+    assert torch.equal(o1.view(torch.int32), o.view(torch.int32))
 
 
 def test_chunked_rejects_long_interval_and_wide_heads():

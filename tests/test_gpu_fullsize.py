@@ -133,15 +133,14 @@ def test_prefill_full_size_sampled_intervals(chunked):
     share, bit for bit (the chunked form's groups of chunks change with T);
     the interval after such a boundary (the 64th and the last) is then checked
     against the oracle from the GPU's own record at the boundary: outputs and
-    state against the float64 recurrence (16 u_bf16 for the chunked form's
-    bf16 products, 1e-3 for the float32 token-sequential form), and the
+    state against the float64 recurrence within 1e-3 (normwise, both forms), and the
     write-back of the GPU's float32 state bit for bit against the oracle's
     allocation and quantiser."""
     w = W.WORKLOADS["prefill"]
     kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
                   b_min=w.b_min, b_max=w.b_max, chunked=chunked)
     oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max)
-    tol = 16 * 2.0 ** -9 if chunked else 1e-3
+    tol = 1e-3
     xs = W.tokens(w, 0, w.T)
     say(f"prefill full size chunked={chunked}: inputs ready")
     _, o_full, _ = _prefill_call(kc, w, xs, w.T)

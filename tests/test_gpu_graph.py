@@ -58,8 +58,9 @@ def test_captured_decode_step_replays_equal_eager_steps():
 
 @pytest.mark.parametrize("T", [150, 40 * 64 + 5])
 def test_captured_chunked_prefill_replays_equal_eager(T):
-    """T = 150: one group of chunks; T = 2565: three groups, the later ones
-    prepared on the library's side stream (branches of the captured graph)."""
+    """T = 150 and T = 2565 (groups of chunks growing from one to 16): the
+    preparation of later groups runs on the caller's second stream, forked
+    from and joined back into the captured stream (branches of the graph)."""
     w = W.sized(W.WORKLOADS["tiny"], B=1, H=2, bf16=True)
     kc = K.Config(B=w.B, H=w.H, d_k=w.dk, d_v=w.dv, group_rows=w.G, mean_bits=w.mean_bits,
                   b_min=w.b_min, b_max=w.b_max, chunked=1)
@@ -72,16 +73,17 @@ def test_captured_chunked_prefill_replays_equal_eager(T):
     ws_e, ws_g = K.new_workspace(kc), K.new_workspace(kc)
     o_e = torch.zeros(w.B * T * w.H * w.dv, dtype=torch.float32, device="cuda")
     o_g = torch.zeros_like(o_e)
-    K.kda_prefill(kc, T, 64, rec_e, q, k, v, s, beta, o_e, ws_e)
+    aux = torch.cuda.Stream()
+    K.kda_prefill(kc, T, 64, rec_e, q, k, v, s, beta, o_e, ws_e, aux_stream=aux)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        K.kda_prefill(kc, T, 64, zero.clone(), q, k, v, s, beta, o_g, ws_g)
+        K.kda_prefill(kc, T, 64, zero.clone(), q, k, v, s, beta, o_g, ws_g, aux_stream=aux)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        K.kda_prefill(kc, T, 64, rec_g, q, k, v, s, beta, o_g, ws_g)
+        K.kda_prefill(kc, T, 64, rec_g, q, k, v, s, beta, o_g, ws_g, aux_stream=aux)
     for rep in range(3):
         rec_g.copy_(zero)                                  # eager reset between replays
         o_g.zero_()

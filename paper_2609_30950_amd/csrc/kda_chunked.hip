@@ -535,23 +535,6 @@ struct ApplySmem {
   uint16_t ut[2][SLICE][US];    // U of the slice, transposed, bf16 hi and lo planes
 };
 
-// Block of a write-back interval: (head, 64-column slice).  Workgroups are
-// dealt to the eight XCDs in turn, so the slices of one head are placed 8
-// block indices apart: they run on one XCD and the second read of the head's
-// chunk record hits that XCD's L2.  Heads past the last multiple of 8 map in
-// order.
-__device__ __forceinline__ void apply_block(int nbh, int nsl, int& bh, int& sl) {
-  constexpr int XCD = 8;
-  const int id = blockIdx.x, full = (nbh / XCD) * XCD * nsl;
-  if (id < full) {
-    sl = (id / XCD) % nsl;
-    bh = id % XCD + XCD * (id / (XCD * nsl));
-  } else {
-    bh = (nbh / XCD) * XCD + (id - full) / nsl;
-    sl = (id - full) % nsl;
-  }
-}
-
 // One write-back interval of one 64-column slice of one head: tokens
 // [p.tok0, p.tok0 + p.ntk) from the record's state; writes the outputs, the
 // float32 state, its per-slice row maxima and (slice 0) Gamma and the rate
@@ -564,7 +547,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   constexpr int KS = DK / 32;            // k-steps over the state's rows
   const int nsl = p.dv / SLICE;
   int bh, sl;
-  apply_block(p.B * p.H, nsl, bh, sl);
+  slice_block(p.B * p.H, nsl, bh, sl);
   const int b = bh / p.H, h = bh % p.H;
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
   const int n = p.ntk;

@@ -72,7 +72,8 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
       const uint32_t hi = wr[DV + col];   // staged; masked off unless straddling
       const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
       const int code = __builtin_amdgcn_sbfe((int)f, 0, b);
-      X[r][c] = ((float)code + add) * mul;
+      // the row's width is wave-uniform: widths >= 2 (add = 0) skip the add
+      X[r][c] = b > 1 ? (float)code * mul : ((float)code + add) * mul;
     }
     // finish row r before the reads of later rows are issued: the compiler
     // would otherwise keep every row's descriptor and words live at once
@@ -229,6 +230,38 @@ __device__ __forceinline__ float seg_combine_p(float v) {
   }
 }
 
+// Ternary rows (width 2: levels -Delta, 0, Delta).  The general evaluation
+// codes x as c = clamp(rint(fl32(x inv)), -1, 1), so |c| = 1 exactly when
+// fl32(|x| inv) > 1/2, i.e. when |x| > th, th the largest float with
+// fl32(th inv) <= 1/2 (fl32(a inv) is monotone in a; th lies within three
+// ulps of Delta / 2, which is exact).  With K = 2^(23 - E), E the exponent of
+// th, K (|x| - th) is at least 1 for every float |x| > th and at most 0
+// otherwise, so clamping fma(|x|, K, -K th) to [0, 1] gives |c| in one
+// operation; fma(-|c|, Delta, |x|) is then +-fma(-c, Delta, x), so the error
+// sum is the same float32 value.  Delta = 0 (inv = 0): no |x| passes.
+__device__ __forceinline__ void ternary_threshold(float d, float inv, float& K, float& nKth) {
+  if (!(d > 0.f)) {
+    K = 1.f;
+    nKth = -__builtin_inff();
+    return;
+  }
+  const int a0 = __builtin_bit_cast(int, 0.5f * d);
+  float th = __builtin_bit_cast(float, a0 - 3);
+#pragma unroll
+  for (int k = -2; k <= 3; ++k) {
+    const float c = __builtin_bit_cast(float, a0 + k);
+    if (c * inv <= 0.5f) th = c;
+  }
+  const int E = ((__builtin_bit_cast(int, th) >> 23) & 255) - 127;
+  K = __builtin_bit_cast(float, (127 + 23 - E) << 23);
+  nKth = -(K * th);
+}
+
+// |c| of a ternary row: fma(|x|, K, -K th) clamped to [0, 1].
+__device__ __forceinline__ float ternary_code(float x, float K, float nKth) {
+  return __builtin_amdgcn_fmed3f(__builtin_fmaf(fabsf(x), K, nKth), 0.f, 1.f);
+}
+
 // Quantise the rows of a row-major float32 state S[DK][DV] (device memory)
 // with widths bits[] (method: see the top of this file and include/kda.h).
 // Thread t handles the 64-column segment t % (DV/64) of row
@@ -304,6 +337,9 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
     float best = __builtin_inff();
     int mb = N_FIT - 1;
     if constexpr (PAIRS == 1) {
+      // waves whose rows all have width 2 take the three-operation form of
+      // the same evaluation (ternary_threshold)
+      const bool ternary = __all(b == 2);
       float ph = phi[b][N_FIT - 1];
       for (int m = N_FIT - 1; m >= 0; --m) {
         const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
@@ -313,11 +349,21 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
         ++evals;
         const float inv = d > 0.f ? 1.0f / d : 0.f;
         float err = 0.f;
+        if (ternary) {
+          float K, nKth;
+          ternary_threshold(d, inv, K, nKth);
 #pragma unroll
-        for (int j = 0; j < SEG; ++j) {
-          const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-          const float e = __builtin_fmaf(-c, d, x[j]);
-          err = __builtin_fmaf(e, e, err);
+          for (int j = 0; j < SEG; ++j) {
+            const float e = __builtin_fmaf(-ternary_code(x[j], K, nKth), d, fabsf(x[j]));
+            err = __builtin_fmaf(e, e, err);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < SEG; ++j) {
+            const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
+            const float e = __builtin_fmaf(-c, d, x[j]);
+            err = __builtin_fmaf(e, e, err);
+          }
         }
         err = seg_combine<SEGS>(err);
         if (err <= best) { best = err; mb = m; }
@@ -567,11 +613,23 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
   const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
   MetaSmem<DK>& meta = sm.meta;
   StatSmem<DK>& st = sm.st;
-  // the first token's row scalars and the whole code-word capacity of the
-  // record are requested together with the metadata (one memory round trip)
+  // the first token's row scalars are requested with the metadata; the
+  // record's meaningful code words (ceil(sum b / 32) per column) follow once
+  // the widths are known
   RowIn in = load_rows<DK, BF16>(sm.rs, p, bh, p.tok0);
-  stage_words<DV, false>(rec, L, L.wc * 32, words);   // the barrier in load_meta covers it
   load_meta<DK, DV>(rec, L, p.bmax, meta);
+  // up to four 16-byte loads per thread are issued now and written to LDS
+  // after the row threads' float64 work below, the rest (means above 8 bits
+  // at d = 128) then
+  constexpr int NPT = 4;
+  const int n4 = ((meta.P[DK] + 31) >> 5) * (DV / 4);
+  const uint4* wsrc = (const uint4*)(rec + L.codes_off);
+  uint4 wv[NPT];
+#pragma unroll
+  for (int u = 0; u < NPT; ++u) {
+    const int e = t + u * (int)blockDim.x;
+    wv[u] = e < n4 ? wsrc[e] : make_uint4(0u, 0u, 0u, 0u);
+  }
   // EMA states of row t (threads t < DK): from the record, or fresh; token
   // samples are folded in as soon as the token's inputs are loaded (float64
   // work of the row threads that overlaps the other waves' decoding)
@@ -595,6 +653,13 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
     fresh = false;
   };
   ema(in);
+#pragma unroll
+  for (int u = 0; u < NPT; ++u) {
+    const int e = t + u * (int)blockDim.x;
+    if (e < n4) ((uint4*)words)[e] = wv[u];
+  }
+  for (int e = t + NPT * (int)blockDim.x; e < n4; e += blockDim.x) ((uint4*)words)[e] = wsrc[e];
+  __syncthreads();
   float X[ROW_BLOCK][DV / WAVE];
   unpack_cols<DK, DV>(words, meta, X);
   // COMPACT (one token): the requantisation rebuilds the state from the

@@ -13,6 +13,23 @@ namespace kda {
 // Columns of one prefill column slice (one block per slice and head).
 constexpr int SLICE = 64;
 
+// Block of a per-slice kernel: (head, 64-column slice).  Workgroups are
+// dealt to the eight XCDs in turn, so the slices of one head are placed 8
+// block indices apart: they run on one XCD, and what they both read (the
+// head's metadata, token inputs, chunk records) comes from that XCD's L2
+// after the first read.  Heads past the last multiple of 8 map in order.
+__device__ __forceinline__ void slice_block(int nbh, int nsl, int& bh, int& sl) {
+  constexpr int XCD = 8;
+  const int id = blockIdx.x, full = (nbh / XCD) * XCD * nsl;
+  if (id < full) {
+    sl = (id / XCD) % nsl;
+    bh = id % XCD + XCD * (id / (XCD * nsl));
+  } else {
+    bh = (nbh / XCD) * XCD + (id - full) / nsl;
+    sl = (id - full) % nsl;
+  }
+}
+
 __device__ __forceinline__ const uint8_t* slot_ptr(const void* recs, long long slot, int bh) {
   return (const uint8_t*)recs + slot * (long long)bh;
 }

@@ -235,6 +235,26 @@ int kda_step(const kda_config* cfg, void* records, const float* q,
              const float* k, const float* v, const float* s, const float* beta,
              const double* gamma, float* o, void* ws, void* stream);
 
+/* kda_step without a workspace argument and without any device allocation,
+ * for callers that cannot allocate: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  The scratch kda_step takes
+ * from `ws` comes from a file-scope device array of the library instead (one
+ * per GPU, 16 MiB, kda_step_noalloc_max_bytes(), held until the process
+ * ends; its address is looked up once per device).  Same arguments, results
+ * and errors as kda_step, except: d_k <= 128 with per-row units (head_units
+ * or d_k = 256 give KDA_ERR_UNSUPPORTED; 32-bit mode needs no scratch and is
+ * forwarded to kda_step), and a configuration whose scratch exceeds 16 MiB
+ * (the decode layer B=64, H=32, d_k=128 needs about 10.3 MiB) gives
+ * KDA_ERR_WORKSPACE before anything is launched.  Every call on one GPU
+ * shares that GPU's array, which keeps the previous call's contents (any
+ * contents are valid on entry): calls that overlap on one GPU (concurrent
+ * streams, or host threads without ordering) race and must not be made. */
+int kda_step_noalloc(const kda_config* cfg, void* records, const float* q,
+                     const float* k, const float* v, const float* s,
+                     const float* beta, const double* gamma, float* o,
+                     void* stream);
+size_t kda_step_noalloc_max_bytes(void);
+
 /* kda_step in two phases, for callers that overlap a layer's write-back with
  * later work (the outputs precede the quantisation, Sec. 2, Accumulated
  * readout error, so the next layer needs only the first phase).  The first

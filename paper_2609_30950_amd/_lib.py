@@ -35,6 +35,8 @@ SIGNATURES = {
     "kda_pack_state": (ctypes.c_int, [_CFG, _P, _P, _P, _P, ctypes.c_uint32, _P, _P]),
     "kda_unpack_state": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P, _P]),
     "kda_step": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kda_step_noalloc": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kda_step_noalloc_max_bytes": (ctypes.c_size_t, []),
     "kda_step_outputs": (ctypes.c_int, [_CFG, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "kda_step_writeback": (ctypes.c_int, [_CFG, _P, _P, _P]),
     "kda_prefill": (ctypes.c_int, [_CFG, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),

@@ -143,6 +143,19 @@ def kda_step(cfg, records, q, k, v, s, beta, o, ws, gamma=None):
         _stream()))
 
 
+def kda_step_noalloc(cfg, records, q, k, v, s, beta, o, gamma=None):
+    """kda_step on the library's own device scratch (no workspace argument,
+    no device allocation)."""
+    n_s = cfg.B * cfg.H * (1 if cfg.decay_per_head else cfg.d_k)
+    _check(load().kda_step_noalloc(
+        ctypes.byref(cfg.c()), _ptr(records, torch.uint8, cfg.B * cfg.H * record_bytes(cfg), "records"),
+        _ptr(q, torch.float32, _rows(cfg), "q"), _ptr(k, torch.float32, _rows(cfg), "k"),
+        _ptr(v, torch.float32, cfg.B * cfg.H * cfg.d_v, "v"), _ptr(s, torch.float32, n_s, "s"),
+        _ptr(beta, torch.float32, cfg.B * cfg.H, "beta"),
+        _ptr(gamma, torch.float64, _rows(cfg), "gamma"),
+        _ptr(o, torch.float32, cfg.B * cfg.H * cfg.d_v, "o"), _stream()))
+
+
 def kda_step_outputs(cfg, records, q, k, v, s, beta, o, ws, gamma=None):
     n_s = cfg.B * cfg.H * (1 if cfg.decay_per_head else cfg.d_k)
     _check(load().kda_step_outputs(

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstring>
 
@@ -144,6 +145,47 @@ void set_ws(KParams& p, const kda_config* cfg, void* ws) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KDA_OK : KDA_ERR_HIP; }
 
+// ------------------------------------------------ allocation-free step ---
+// Scratch of kda_step_noalloc: a file-scope device array (one copy per GPU
+// the library runs on, held until the process ends).  Host code never uses
+// the array's name as a device address; it uses the address that
+// hipGetSymbolAddress returns for the current device, kept per device.
+constexpr size_t KDA_SCRATCH_BYTES = (size_t)16 << 20;
+__device__ __align__(256) unsigned char scratch[KDA_SCRATCH_BYTES];
+constexpr int SCRATCH_MAX_DEV = 64;
+std::atomic<void*> g_scratch_addr[SCRATCH_MAX_DEV];
+
+// Device address of this device's scratch (nullptr on a HIP error).  Calls
+// that race here compute the same address.
+void* scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_MAX_DEV) return nullptr;
+  void* ptr = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_addr[dev].store(ptr, std::memory_order_release);
+  }
+  return ptr;
+}
+
+// Views of the decode step (d_k <= 128, per-row units) inside the scratch:
+// keys, rate codes, widths, per-slice row maxima, Gamma and the token's
+// vectors; no float32 state (the requantisation rebuilds it).
+WsLayout scratch_layout(const kda_config* cfg) {
+  const size_t rows = (size_t)cfg->B * cfg->H * cfg->d_k;
+  WsLayout w;
+  w.c_off = 0;
+  w.zr_off = up256(w.c_off + rows * sizeof(double));
+  w.bits_off = up256(w.zr_off + rows * sizeof(uint32_t));
+  w.s32_off = up256(w.bits_off + rows);
+  w.rpart_off = w.s32_off;
+  w.gam_off = up256(w.rpart_off + rows * (size_t)(cfg->d_v / 64) * sizeof(float));
+  w.hv_off = up256(w.gam_off + rows * sizeof(double));
+  w.chunk_off = up256(w.hv_off + (size_t)cfg->B * cfg->H * (cfg->d_v + 2 * cfg->d_k) * sizeof(float));
+  w.total = w.chunk_off;
+  return w;
+}
+
 // Kernels use 16-byte vector accesses on records, workspace and states.
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
@@ -277,6 +319,36 @@ int kda_step(const kda_config* cfg, void* records, const float* q, const float* 
   if (cfg->head_units) return hip_status(kda::launch_step_heads(p, (hipStream_t)stream));
   return hip_status(kda::launch_step(p, (hipStream_t)stream));
 }
+
+int kda_step_noalloc(const kda_config* cfg, void* records, const float* q, const float* k,
+                     const float* v, const float* s, const float* beta, const double* gamma,
+                     float* o, void* stream) {
+  int need = 0;
+  const int st = check_cfg(cfg, &need);
+  if (st != KDA_OK) return st;
+  if (cfg->state32)   // the unquantised step needs no scratch
+    return kda_step(cfg, records, q, k, v, s, beta, gamma, o, nullptr, stream);
+  if (cfg->head_units || cfg->d_k > 128) return KDA_ERR_UNSUPPORTED;
+  if (scratch_layout(cfg).total > KDA_SCRATCH_BYTES) return KDA_ERR_WORKSPACE;
+  void* ws = scratch_address();
+  if (ws == nullptr) return KDA_ERR_HIP;
+  KParams p;
+  const int ps = step_params(cfg, records, q, k, v, s, beta, gamma, o, ws, 3, &p);
+  if (ps != KDA_OK) return ps;
+  const WsLayout w = scratch_layout(cfg);
+  uint8_t* base = (uint8_t*)ws;
+  p.ws_c = (double*)(base + w.c_off);
+  p.ws_zr = (uint32_t*)(base + w.zr_off);
+  p.ws_bits = base + w.bits_off;
+  p.ws_s32 = nullptr;
+  p.ws_rpart = (float*)(base + w.rpart_off);
+  p.ws_gam = (double*)(base + w.gam_off);
+  p.ws_hv = (float*)(base + w.hv_off);
+  p.ws_chunk = nullptr;
+  return hip_status(kda::launch_step(p, (hipStream_t)stream));
+}
+
+size_t kda_step_noalloc_max_bytes(void) { return KDA_SCRATCH_BYTES; }
 
 int kda_step_outputs(const kda_config* cfg, void* records, const float* q, const float* k,
                      const float* v, const float* s, const float* beta, const double* gamma,

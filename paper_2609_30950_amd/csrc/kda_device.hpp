@@ -71,6 +71,25 @@ __device__ __forceinline__ uint16_t f32_to_f16_sat(float x) {
   return u;
 }
 
+// FP16 bits of a non-negative float (scales R phi of the fit), round to
+// nearest even, saturating at 65504: the same value as f32_to_f16_sat for
+// x >= 0 with the saturation as one minimum before the conversion (values
+// from 65504 up round to 65504 either way; NaN is not an input).
+__device__ __forceinline__ uint16_t f32_to_f16_sat_nonneg(float x) {
+  asm volatile("" : "+v"(x));
+  return __builtin_bit_cast(uint16_t, (_Float16)fminf(x, 65504.0f));
+}
+
+// fl32(1 / d) for d an FP16 value (positive, or 0 -> 0): the hardware
+// reciprocal refined by one Newton step, fma(r0, fma(-d, r0, 1), r0), which
+// equals the correctly rounded quotient for every positive finite FP16 value
+// (checked exhaustively on gfx950 against the IEEE division).
+__device__ __forceinline__ float recip_f16_value(float d) {
+  const float r0 = __builtin_amdgcn_rcpf(d);
+  const float r1 = __builtin_fmaf(r0, __builtin_fmaf(-d, r0, 1.0f), r0);
+  return d > 0.f ? r1 : 0.f;
+}
+
 __device__ __forceinline__ float f16_to_f32(uint16_t u) {
   return (float)__builtin_bit_cast(_Float16, u);
 }

@@ -136,12 +136,12 @@ __device__ __forceinline__ int fit_pack_block(const float (&X)[ROW_BLOCK][CPL], 
   float best = __builtin_inff();
   int mb = N_FIT - 1, evals = 0;
   for (int m = N_FIT - 1; m >= 0; --m) {
-    const float d = f16_to_f32(f32_to_f16_sat(mx * phi[m]));
+    const float d = f16_to_f32(f32_to_f16_sat_nonneg(mx * phi[m]));
     // the row maximum's clip error bounds this and every smaller factor
     const float emax = __builtin_fmaf(-nf, d, mx);
     if (emax >= 0.f && emax * emax > best) break;
     ++evals;
-    const float inv = d > 0.f ? 1.0f / d : 0.f;
+    const float inv = recip_f16_value(d);
     float err = 0.f;
 #pragma unroll
     for (int r = 0; r < ROW_BLOCK; ++r) {
@@ -154,9 +154,9 @@ __device__ __forceinline__ int fit_pack_block(const float (&X)[ROW_BLOCK][CPL], 
       mb = m;
     }
   }
-  const uint16_t dh = f32_to_f16_sat(mx * phi[mb]);
+  const uint16_t dh = f32_to_f16_sat_nonneg(mx * phi[mb]);
   const float d = f16_to_f32(dh);
-  const float inv = d > 0.f ? 1.0f / d : 0.f;
+  const float inv = recip_f16_value(d);
   uint32_t wd[B + 1];
 #pragma unroll
   for (int k = 0; k <= B; ++k) wd[k] = 0u;

@@ -342,12 +342,12 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
       const bool ternary = __all(b == 2);
       float ph = phi[b][N_FIT - 1];
       for (int m = N_FIT - 1; m >= 0; --m) {
-        const float d = f16_to_f32(f32_to_f16_sat(mx * ph));
+        const float d = f16_to_f32(f32_to_f16_sat_nonneg(mx * ph));
         ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
         const float emax = __builtin_fmaf(-nf, d, mx);
         if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
         ++evals;
-        const float inv = d > 0.f ? 1.0f / d : 0.f;
+        const float inv = recip_f16_value(d);
         float err = 0.f;
         if (ternary) {
           float K, nKth;
@@ -371,14 +371,14 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
     } else {
       for (int m0 = N_FIT - 1; m0 >= 1; m0 -= 2) {
         const int m1 = m0 - 1;
-        const float d0 = f16_to_f32(f32_to_f16_sat(mx * phi[b][m0]));
-        const float d1 = f16_to_f32(f32_to_f16_sat(mx * phi[b][m1]));
+        const float d0 = f16_to_f32(f32_to_f16_sat_nonneg(mx * phi[b][m0]));
+        const float d1 = f16_to_f32(f32_to_f16_sat_nonneg(mx * phi[b][m1]));
         const float e0 = __builtin_fmaf(-nf, d0, mx), e1 = __builtin_fmaf(-nf, d1, mx);
         if (e0 >= 0.f && e0 * e0 > best) break;           // row-uniform decisions
         const bool stop1 = e1 >= 0.f && e1 * e1 > best;
         const float d = half ? d1 : d0;
         if (!half || !stop1) ++evals;
-        const float inv = d > 0.f ? 1.0f / d : 0.f;
+        const float inv = recip_f16_value(d);
         float err = 0.f;
 #pragma unroll
         for (int j = 0; j < SEG; ++j) {
@@ -394,9 +394,9 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
         if (stop1) break;
       }
     }
-    const uint16_t dh = f32_to_f16_sat(mx * phi[b][mb]);
+    const uint16_t dh = f32_to_f16_sat_nonneg(mx * phi[b][mb]);
     const float d = f16_to_f32(dh);
-    const float inv = d > 0.f ? 1.0f / d : 0.f;
+    const float inv = recip_f16_value(d);
     if (writer) {
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {

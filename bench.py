@@ -62,36 +62,90 @@ def committed_traffic(kernel, workload):
     return e["hbm_bytes_per_launch"]
 
 
-def cpu_baseline(name, budget_s=12.0, warm_tokens=32, head_units=False):
-    """CPU oracle decode steps on one sequence (all its heads) for about
-    budget_s seconds, after a short oracle warm-up of its own."""
+def _oracle_cfg(w, head_units):
+    from oracle import step
+    return step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
+                    erase=w.erase, unit="head" if head_units else "row")
+
+
+def _oracle_worker(job):
+    """One host process: decode steps of sequence `seq` of the workload for
+    about budget_s seconds after its own oracle warm-up; path "mirror" is the
+    float32-contract step with its write-back (recurrence, statistics,
+    allocation, fitted quantiser), "truth" the float64 recurrence and outputs
+    of the same steps.  Returns (state-tokens, seconds)."""
+    name, seq, path, budget_s, warm_tokens, head_units = job
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1):   # one thread per process: BLAS pools off
+        return _oracle_steps(name, seq, path, budget_s, warm_tokens, head_units)
+
+
+def _oracle_steps(name, seq, path, budget_s, warm_tokens, head_units):
     from oracle import step
     w = W.WORKLOADS[name]
     if head_units:
         w = W.sized(w, b_min=2, G=w.dk)
-    oc = step.Cfg(dk=w.dk, dv=w.dv, G=w.G, mean_bits=w.mean_bits, b_min=w.b_min, b_max=w.b_max,
-                  erase=w.erase, unit="head" if head_units else "row")
+    oc = _oracle_cfg(w, head_units)
     base = W.base_rates(w)
     xs = {n: [] for n in ("q", "k", "v", "s", "beta")}
     for t in range(warm_tokens):
         x = W.token(w, t, base=base)
         for n in xs:
-            xs[n].append(x[n][:1])
+            xs[n].append(x[n][seq:seq + 1])
     xs = {n: np.stack(a, axis=1) for n, a in xs.items()}
-    st, _ = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
+    st, S = step.warm_state(xs["q"], xs["k"], xs["v"], xs["s"], xs["beta"], oc)
     n = 0
     t0 = time.perf_counter()
     while True:
         x = W.token(w, warm_tokens + n, base=base)
-        x = {k: v[:1] for k, v in x.items()}
-        st, _, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
+        x = {k: v[seq:seq + 1] for k, v in x.items()}
+        if path == "mirror":
+            st, _, _ = step.mirror_decode_step(st, x["q"], x["k"], x["v"], x["s"], x["beta"], oc)
+        else:
+            from oracle import recurrence
+            S, _ = recurrence.truth_step_rowform(S, x["q"], x["k"], x["v"], x["s"], x["beta"],
+                                                 oc.erase)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return dict(value=w.H * n / el, unit="state-tokens/s", cores=1, kind="oracle",
-                sample=f"{n} decode steps of 1 of {w.B} sequences ({w.H} heads, "
-                       f"{w.dk}x{w.dv} states), float32-contract oracle, one thread")
+    return w.H * n, el
+
+
+def cpu_baseline(name, budget_s=6.0, warm_tokens=32, head_units=False):
+    """The CPU oracle on the host's cores (a reported baseline, not a
+    target): both oracle paths, on one thread and on all cores with one
+    process per sequence (sequences are independent; the layer budget couples
+    the heads of one), each timed on decode steps after its own warm-up."""
+    import multiprocessing as mp
+    import platform
+    import subprocess
+    ncpu = os.cpu_count() or 1
+    nproc = max(1, min(ncpu, 16))
+    try:
+        model = [l.split(":", 1)[1].strip() for l in
+                 subprocess.run(["lscpu"], capture_output=True, text=True).stdout.splitlines()
+                 if l.startswith("Model name")][0]
+    except Exception:   # lscpu missing or unparsable
+        model = platform.processor() or "unknown"
+    ctx = mp.get_context("spawn")   # fresh interpreters: nothing of this process's GPU state
+    paths = {}
+    for path in ("mirror", "truth"):
+        tok, sec = _oracle_worker((name, 0, path, budget_s, warm_tokens, head_units))
+        one = tok / sec
+        with ctx.Pool(nproc) as pool:
+            res = pool.map(_oracle_worker, [(name, s, path, budget_s, warm_tokens, head_units)
+                                            for s in range(nproc)])
+        allc = sum(t / s for t, s in res)
+        paths[path] = {"one_thread": one, "all_cores": allc, "processes": nproc}
+    w = W.WORKLOADS[name]
+    return dict(value=paths["mirror"]["all_cores"], unit="state-tokens/s", cores=nproc,
+                kind="oracle",
+                sample=f"decode steps of 1 sequence per process ({w.H} heads, {w.dk}x{w.dv} "
+                       f"states, {budget_s:g} s each after a {warm_tokens}-token oracle warm-up), "
+                       f"float32-contract oracle with its write-back (value), {nproc} processes; "
+                       f"also one thread, and the float64 recurrence alone",
+                paths=paths, os_cpu_count=ncpu, cpu_model=model)
 
 
 def run_state32_reference(w, args, K, torch):
@@ -361,6 +415,13 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    # the CPU oracle first, in host processes started before this process
+    # touches the GPU (decode workloads)
+    cpu = None
+    if not args.no_cpu_baseline and args.workload not in ("prefill", "weights"):
+        cpu = cpu_baseline(args.workload, head_units=args.head_units)
+        print(f"# cpu baseline: {cpu['paths']}", file=sys.stderr, flush=True)
+
     import torch
     import paper_2609_30950_amd as K
 
@@ -538,8 +599,8 @@ def main():
     if not args.no_ref32 and w.name == "decode":
         del layers
         out["state32_reference"] = run_state32_reference(w, args, K, torch)
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload, head_units=args.head_units)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 

@@ -66,6 +66,8 @@ __device__ __forceinline__ int block_excl_scan(int v, int* scratch, int* total) 
 
 // 52 fraction bits of the frexp mantissa of c > 0 (c = (1 + F 2^-52) 2^(E-1)).
 __device__ __forceinline__ unsigned long long frac_bits(double c) {
+  const unsigned long long u = (unsigned long long)__double_as_longlong(c);
+  if ((u >> 52) != 0ull) return u & ((1ull << 52) - 1ull);   // normal: the stored fraction
   int e;
   const double m = frexp(c, &e);
   return (unsigned long long)ldexp(m, 53) - (1ull << 52);
@@ -83,6 +85,12 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   static_assert(RPT <= 32, "candidate mask");
   int E[RPT];
   double Cv[RPT];
+  // weights first: their load latency overlaps the clearing of the histograms
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int n = tid + k * nt;
+    Cv[k] = n < N ? c_at(n) : 0.0;
+  }
   for (int e = tid; e < EBINS; e += nt) sm.hist_e[e] = 0;
   for (int e = tid; e < 2 * 256; e += nt) sm.hist_d[e >> 8][e & 255] = 0;
   for (int n = tid; n < N; n += nt) sm.extra[n] = 0;
@@ -95,12 +103,9 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   int npos = 0, emin = 0x7fffffff, emax = -0x7fffffff;
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
-    const int n = tid + k * nt;
     E[k] = E_ZERO;
-    Cv[k] = 0.0;
-    if (n < N) {
-      const double cv = c_at(n);
-      Cv[k] = cv;
+    {
+      const double cv = Cv[k];
       if (cv > 0.0) {
         int ei;
         frexp(cv, &ei);
@@ -112,8 +117,9 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     }
   }
   __syncthreads();
-  // histogram of exponents (few distinct values: LDS atomics conflict little);
-  // count and exponent range reduced per wave, one LDS atomic each
+  // histogram of exponents (one LDS atomic per row: the exponents of a
+  // wave's rows are too varied for per-value aggregation to pay); count and
+  // exponent range reduced per wave, one LDS atomic each
 #pragma unroll
   for (int k = 0; k < RPT; ++k)
     if (E[k] != E_ZERO) atomicAdd(&sm.hist_e[E[k] + EOFF], 1);
@@ -291,18 +297,21 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   }
   __syncthreads();
   if (tid < WAVE) {
+    // keys held one per lane, the others read across lanes (no LDS round
+    // trip per comparison)
     const int nc = sm.cand_n;
-    if (lane < nc) {
-      const unsigned long long my = sm.cand_key[lane];
-      const int myr = sm.cand_row[lane];
-      int rank = 0;
-      for (int j = 0; j < nc; ++j) {
-        const unsigned long long o = sm.cand_key[j];
-        const int orow = sm.cand_row[j];
-        rank += (o > my) || (o == my && orow < myr);
-      }
-      if (rank < rem) sm.extra[myr] = 1;
+    const unsigned long long my = lane < nc ? sm.cand_key[lane] : 0ull;
+    const int myr = lane < nc ? sm.cand_row[lane] : 0;
+    const unsigned mlo = (unsigned)my, mhi = (unsigned)(my >> 32);
+    int rank = 0;
+    for (int j = 0; j < nc; ++j) {
+      const unsigned long long o =
+          ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)mhi, j) << 32) |
+          (unsigned)__builtin_amdgcn_readlane((int)mlo, j);
+      const int orow = __builtin_amdgcn_readlane(myr, j);
+      rank += (o > my) || (o == my && orow < myr);
     }
+    if (lane < nc && rank < rem) sm.extra[myr] = 1;
   }
   __syncthreads();
 #pragma unroll

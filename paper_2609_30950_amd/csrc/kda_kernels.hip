@@ -182,28 +182,32 @@ struct OrderSmem {
   int P[DK + 1];
 };
 
+// perm[0 .. hi - lo) lists the rows lo .. hi - 1 by width, widest first
+// (ties in row order); os.P holds the bit offsets of all DK rows.
 template <int DK>
-__device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, OrderSmem<DK>& os) {
+__device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, OrderSmem<DK>& os,
+                                            int lo = 0, int hi = DK) {
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
-  int b = 0, below = 0;
+  int b = 0, bp = 0, below = 0;
   if (t < DK) {
     b = bits[t];
+    bp = t >= lo && t < hi ? b : 0;   // widths are at least 1: 0 marks rows outside the range
     const unsigned long long lt = (1ull << lane) - 1ull;
     for (int v = 1; v <= MAX_B; ++v) {
-      const unsigned long long m = __ballot(b == v);
+      const unsigned long long m = __ballot(bp == v);
       if (lane == 0) os.cnt[w][v] = __popcll(m);
-      if (b == v) below = __popcll(m & lt);
+      if (bp == v) below = __popcll(m & lt);
     }
     // prefix sums of widths in row order
     const int incl = wave_incl_scan(b);
     os.P[t + 1] = incl;          // per-wave inclusive; fixed up below
   }
   __syncthreads();
-  if (t < DK) {
+  if (bp > 0) {
     int pos = below;
-    for (int v = b + 1; v <= MAX_B; ++v)
+    for (int v = bp + 1; v <= MAX_B; ++v)
       for (int q = 0; q < DK / WAVE; ++q) pos += os.cnt[q][v];
-    for (int q = 0; q < w; ++q) pos += os.cnt[q][b];
+    for (int q = 0; q < w; ++q) pos += os.cnt[q][bp];
     perm[pos] = (uint8_t)t;
   }
   // wave totals of widths -> global prefix
@@ -224,10 +228,19 @@ __device__ __forceinline__ float seg_combine_p(float v) {
   if constexpr (PAIRS == 1) {
     return seg_combine<SEGS>(v);
   } else {
-    static_assert(SEGS <= 2, "candidate pairs with at most two segments per row");
-    if constexpr (SEGS == 2) v = v + dpp_f<0x4E>(v);   // lanes differing in bit 1
+    static_assert(SEGS <= 2, "candidate lanes with at most two segments per row");
+    if constexpr (SEGS == 2) {
+      if constexpr (PAIRS == 2) v = v + dpp_f<0x4E>(v);   // lanes differing in bit 1
+      else v = v + __shfl_xor(v, PAIRS);                  // lanes differing in bit log2(PAIRS)
+    }
     return v;
   }
+}
+
+// Lane q of each group of four (quad_perm [q, q, q, q]).
+template <int Q>
+__device__ __forceinline__ float quad_lane(float v) {
+  return dpp_f<Q * 0x55>(v);
 }
 
 // Ternary rows (width 2: levels -Delta, 0, Delta).  The general evaluation
@@ -276,29 +289,31 @@ __device__ __forceinline__ float ternary_code(float x, float K, float nKth) {
 // reach the minimum, so the scan stops; the result equals the exhaustive
 // first strict minimum over all 16 candidates.
 //
-// PAIRS = 2 (blocks of 4 d_k threads, for grids with few heads): two adjacent
-// lanes hold the same segment and evaluate the candidates m and m - 1 of one
-// step together.  The second one's bound is tested against the best error
-// before the first one's result, so it may be evaluated where the sequential
-// scan would have stopped; its error then exceeds the best (the bound is a
-// lower bound) and the scan ends at the next step: the same choice, at most
-// one evaluation more.
-template <int DK, int DV, bool SYNC_AFTER_LOAD = false, int PAIRS = 1, typename LoadRow,
-          typename CT>
+// PAIRS = 2 or 4 (blocks of 2 PAIRS d_k threads, for grids with few heads):
+// PAIRS adjacent lanes hold the same segment and evaluate the candidates
+// m, m - 1, .., m - PAIRS + 1 of one step together.  Every bound of a step is
+// tested against the best error before the step, so a candidate may be
+// evaluated where the sequential scan would have stopped; its error then
+// exceeds the best (the bound is a lower bound), the merge in candidate order
+// passes over it and the scan ends after the step: the same choice, at most
+// PAIRS - 1 evaluations more per row.
+// ROWS: the rows perm[0 .. ROWS) (a block may take part of a head's rows).
+template <int DK, int DV, bool SYNC_AFTER_LOAD = false, int PAIRS = 1, int ROWS = DK,
+          typename LoadRow, typename CT>
 __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, const uint8_t* perm,
                          const float (*phi)[N_FIT], CT* Ct, uint16_t* scale_out,
                          unsigned long long* diag) {
   constexpr int LD = ct_ld<DK, CT>();
   constexpr int SEGS = DV / SEG;
-  constexpr int ITEMS = DK * SEGS * PAIRS;
-  static_assert(PAIRS == 1 || PAIRS == 2, "candidates per step");
+  constexpr int ITEMS = ROWS * SEGS * PAIRS;
+  static_assert(PAIRS == 1 || PAIRS == 2 || PAIRS == 4, "candidates per step");
   static_assert(N_FIT % PAIRS == 0, "whole candidate pairs");
   const int tid = threadIdx.x, nt = blockDim.x;
   const int iters = (ITEMS + nt - 1) / nt;   // same count for every thread
   for (int rep = 0; rep < iters; ++rep) {
   const int unit = rep * nt + tid;
   const bool valid = unit < ITEMS;
-  const int half = PAIRS == 2 ? (unit & 1) : 0;
+  const int half = unit % PAIRS;   // this lane's candidate within a step
   const int item = unit / PAIRS;
   const int i = valid ? perm[item / SEGS] : 0;
   const int sg = item % SEGS;
@@ -312,8 +327,8 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
   if constexpr (PAIRS == 1) {
     if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0xB1>(mx));
     if constexpr (SEGS >= 4) mx = fmaxf(mx, dpp_f<0x4E>(mx));
-  } else {
-    if constexpr (SEGS >= 2) mx = fmaxf(mx, dpp_f<0x4E>(mx));
+  } else if constexpr (SEGS >= 2) {
+    mx = fmaxf(mx, PAIRS == 2 ? dpp_f<0x4E>(mx) : __shfl_xor(mx, PAIRS));
   }
   const int b = bits[i];
   CT* dst = Ct + (size_t)(sg * SEG) * LD + i;
@@ -369,15 +384,25 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
         if (err <= best) { best = err; mb = m; }
       }
     } else {
-      for (int m0 = N_FIT - 1; m0 >= 1; m0 -= 2) {
-        const int m1 = m0 - 1;
-        const float d0 = f16_to_f32(f32_to_f16_sat_nonneg(mx * phi[b][m0]));
-        const float d1 = f16_to_f32(f32_to_f16_sat_nonneg(mx * phi[b][m1]));
-        const float e0 = __builtin_fmaf(-nf, d0, mx), e1 = __builtin_fmaf(-nf, d1, mx);
-        if (e0 >= 0.f && e0 * e0 > best) break;           // row-uniform decisions
-        const bool stop1 = e1 >= 0.f && e1 * e1 > best;
-        const float d = half ? d1 : d0;
-        if (!half || !stop1) ++evals;
+      for (int m0 = N_FIT - 1; m0 >= PAIRS - 1; m0 -= PAIRS) {
+        // the step's candidates m0 - q, their bounds against the best so far
+        float dq[PAIRS];
+        bool stop[PAIRS];
+#pragma unroll
+        for (int q = 0; q < PAIRS; ++q) {
+          dq[q] = f16_to_f32(f32_to_f16_sat_nonneg(mx * phi[b][m0 - q]));
+          const float e = __builtin_fmaf(-nf, dq[q], mx);
+          stop[q] = e >= 0.f && e * e > best;
+        }
+        if (stop[0]) break;                       // row-uniform decisions
+        float d = dq[0];
+        bool skip = false;
+#pragma unroll
+        for (int q = 1; q < PAIRS; ++q) {
+          d = half == q ? dq[q] : d;
+          skip = half == q ? stop[q] : skip;
+        }
+        if (!skip) ++evals;
         const float inv = recip_f16_value(d);
         float err = 0.f;
 #pragma unroll
@@ -386,12 +411,26 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
           const float e = __builtin_fmaf(-c, d, x[j]);
           err = __builtin_fmaf(e, e, err);
         }
-        err = seg_combine_p<SEGS, 2>(err);
-        const float other = dpp_f<0xB1>(err);   // the partner lane's candidate
-        const float err0 = half ? other : err, err1 = half ? err : other;
-        if (err0 <= best) { best = err0; mb = m0; }
-        if (!stop1 && err1 <= best) { best = err1; mb = m1; }
-        if (stop1) break;
+        err = seg_combine_p<SEGS, PAIRS>(err);
+        // every lane of the step merges the errors in candidate order
+        float eq[PAIRS];
+        if constexpr (PAIRS == 2) {
+          const float other = dpp_f<0xB1>(err);   // the partner lane's candidate
+          eq[0] = half ? other : err;
+          eq[1] = half ? err : other;
+        } else {
+          eq[0] = quad_lane<0>(err);
+          eq[1] = quad_lane<1>(err);
+          eq[2] = quad_lane<2>(err);
+          eq[3] = quad_lane<3>(err);
+        }
+        bool any = false;
+#pragma unroll
+        for (int q = 0; q < PAIRS; ++q) {
+          if (!stop[q] && eq[q] <= best) { best = eq[q]; mb = m0 - q; }
+          any = any || stop[q];
+        }
+        if (any) break;
       }
     }
     const uint16_t dh = f32_to_f16_sat_nonneg(mx * phi[b][mb]);
@@ -415,35 +454,55 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
 }
 
 // Pack codes Ct[DV][CT_LD] (column-major) with widths bits[] into column
-// bit streams.  Thread (column, half) packs rows [half*DK/2, (half+1)*DK/2)
-// starting at bit P[half*DK/2]; the word both halves share (if the boundary is
-// not word aligned) is merged through LDS.  A wave holds one half, so the
-// widths, the bit position and every word boundary are wave-uniform (scalar
+// bit streams, rows [r0, r0 + ROWS) of the head (a block may take part of a
+// head's rows).  Thread (column, half) packs half of those rows, starting at
+// bit P of its first row; the word both halves share (if the boundary is not
+// word aligned) is merged through LDS.  A wave holds one half, so the widths,
+// the bit position and every word boundary are wave-uniform (scalar
 // registers and branches): each code costs one field extract and one
-// shift-or into the current word.
-template <int DK, int DV, typename CT>
+// shift-or into the current word.  A word that holds bits of rows outside
+// the range (a neighbouring block's) is written with an atomic AND that
+// clears this block's bits and an atomic OR that sets them, so the two
+// blocks' writes commute; words the block owns entirely are plain stores.
+template <int DK, int DV, int ROWS = DK, typename CT>
 __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, const int* P,
-                                          uint32_t* words, uint32_t* tail) {
-  constexpr int HALF = DK / 2;
+                                          uint32_t* words, uint32_t* tail, int r0 = 0) {
+  constexpr int HALF = ROWS / 2;
   static_assert(DV == DK && DV % WAVE == 0, "one (column, half) per thread, halves wave-aligned");
   const int tid = threadIdx.x;
   const int col = tid % DV;
   // threads past 2 d_v (blocks of the paired fit) only join the barrier
   const int half = __builtin_amdgcn_readfirstlane(tid / DV);
   const bool packer = half < 2;
-  const int r0 = (packer ? half : 0) * HALF;
-  const int start = __builtin_amdgcn_readfirstlane(P[r0]);
-  const int split = __builtin_amdgcn_readfirstlane(P[HALF]);
+  const int a = r0 + (packer ? half : 0) * HALF;
+  const int start = __builtin_amdgcn_readfirstlane(P[a]);
+  const int split = __builtin_amdgcn_readfirstlane(P[r0 + HALF]);
+  // stream bits this block owns: [own_lo, own_hi); the block of the last
+  // rows also owns the padding of the last word
+  const int own_lo = __builtin_amdgcn_readfirstlane(P[r0]);
+  const int own_hi = r0 + ROWS >= DK ? 0x7fffffff : __builtin_amdgcn_readfirstlane(P[r0 + ROWS]);
+  auto put = [&](int wi, uint32_t v) {   // wi is wave-uniform
+    uint32_t* dst = words + (size_t)wi * DV + col;
+    const int b0 = own_lo - 32 * wi, b1 = own_hi - 32 * wi;
+    if (b0 <= 0 && b1 >= 32) {
+      *dst = v;
+    } else {
+      const uint32_t m = (b1 >= 32 ? ~0u : (1u << b1) - 1u) & (b0 <= 0 ? ~0u : ~((1u << b0) - 1u));
+      atomicAnd(dst, ~m);
+      atomicOr(dst, v & m);
+    }
+  };
   // widths, four per LDS word (bits[] is 4-byte aligned), read as broadcasts
-  const uint32_t* bw = (const uint32_t*)(bits + r0);
+  const uint32_t* bw = (const uint32_t*)(bits + a);
   uint32_t cur = 0;         // bits [32 wi, 32 wi + nb) of this column's stream
-  int nb = start & 31;      // bits below nb in the first word belong to the lower half
+  int nb = start & 31;      // bits below nb in the first word belong to earlier rows
   int wi = start >> 5;
   uint32_t first = 0;       // upper half: its first word, merged after the barrier
   bool first_pending = half == 1 && (split & 31) != 0;
   constexpr int CB = (int)sizeof(CT);   // bytes per code
   constexpr int CPR = 16 / CB;                  // codes per 16-byte read
-  const CT* cc = Ct + (size_t)col * ct_ld<DK, CT>() + r0;
+  static_assert(HALF % CPR == 0, "whole 16-byte code reads per half");
+  const CT* cc = Ct + (size_t)col * ct_ld<DK, CT>() + a;
   const bool shared = (split & 31) != 0;
   if (packer) {
 #pragma unroll
@@ -465,8 +524,7 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
           first = cur;
           first_pending = false;
         } else {
-          uint32_t* wrow = words + wi * DV;   // uniform base, per-lane offset
-          wrow[col] = cur;
+          put(wi, cur);
         }
         ++wi;
         cur = field >> (b - nb);   // the nb bits that did not fit (0 if none)
@@ -476,7 +534,7 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
   // the lower half's last partial word goes to LDS when the upper half shares it
   if (half == 0 && nb > 0) {
     if (shared) tail[col] = cur;
-    else words[wi * DV + col] = cur;
+    else put(wi, cur);
   }
   }
   __syncthreads();
@@ -484,26 +542,31 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
     if (shared) {
       // first word of the upper half (complete, or still open if short)
       const uint32_t mine = first_pending ? cur : first;
-      words[(split >> 5) * DV + col] = mine | tail[col];
-      if (!first_pending && nb > 0) words[wi * DV + col] = cur;
+      put(split >> 5, mine | tail[col]);
+      if (!first_pending && nb > 0) put(wi, cur);
     } else if (nb > 0) {
-      words[wi * DV + col] = cur;
+      put(wi, cur);
     }
   }
 }
 
 // Write a record's metadata (header, widths, scales, stat codes).
-template <int DK>
+// Rows [r0, r0 + ROWS) (r0 and ROWS even); the block of row 0 writes the header.
+template <int DK, int ROWS = DK>
 __device__ __forceinline__ void store_meta(uint8_t* rec, const Layout& L, unsigned ntok, const uint8_t* bits,
-                           const uint16_t* scale16, const uint16_t* z, const uint16_t* r16) {
+                           const uint16_t* scale16, const uint16_t* z, const uint16_t* r16,
+                           int r0 = 0) {
   const int tid = threadIdx.x;
-  if (tid < 4) ((unsigned*)rec)[tid] = tid == 0 ? ntok : 0u;
-  if (tid < DK / 2)
-    rec[L.w_off + tid] = (uint8_t)((bits[2 * tid] - 1) | ((bits[2 * tid + 1] - 1) << 4));
-  if (tid < DK) {
-    ((uint16_t*)(rec + L.sc_off))[tid] = scale16[tid];
-    ((uint16_t*)(rec + L.z_off))[tid] = z[tid];
-    ((uint16_t*)(rec + L.r_off))[tid] = r16[tid];
+  if (r0 == 0 && tid < 4) ((unsigned*)rec)[tid] = tid == 0 ? ntok : 0u;
+  if (tid < ROWS / 2) {
+    const int q = r0 / 2 + tid;
+    rec[L.w_off + q] = (uint8_t)((bits[2 * q] - 1) | ((bits[2 * q + 1] - 1) << 4));
+  }
+  if (tid < ROWS) {
+    const int i = r0 + tid;
+    ((uint16_t*)(rec + L.sc_off))[i] = scale16[i];
+    ((uint16_t*)(rec + L.z_off))[i] = z[i];
+    ((uint16_t*)(rec + L.r_off))[i] = r16[i];
   }
 }
 
@@ -768,10 +831,15 @@ struct RequantLds {
 // rebuilt row by row from the record and the token's vectors the stats pass
 // left in the workspace, S_ij = fma(g_i, w_j, fl32(a_i x^_ij)) with x^ the
 // record's dequantised value -- the same operations as the stats pass, so the
-// same float32 state.  Otherwise the stats pass left the float32 state itself.
-// All threads of the block (2 d_k) call it.
-template <int DK, int DV, bool COMPACT, typename CT, int PAIRS = 1>
-__device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLds<DK, DV, COMPACT, CT>& sm) {
+// same float32 state.  Otherwise the stats pass left the float32 state itself,
+// and PARTS blocks may share the head: block `part` fits and packs rows
+// [part DK / PARTS, (part + 1) DK / PARTS).  All threads of the block call it.
+template <int DK, int DV, bool COMPACT, typename CT, int PAIRS = 1, int PARTS = 1>
+__device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLds<DK, DV, COMPACT, CT>& sm,
+                                             int part = 0) {
+  static_assert(!COMPACT || PARTS == 1, "the decode step rebuilds whole heads");
+  constexpr int ROWS = DK / PARTS;
+  const int r0 = part * ROWS;
   const Layout L = p.L;
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
   const int t = threadIdx.x;
@@ -827,15 +895,15 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
     fit_rows<DK, DV, true>(rebuild, sm.nb, sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
   } else {
     __syncthreads();
-    width_order<DK>(sm.nb, sm.perm, sm.os);
+    width_order<DK>(sm.nb, sm.perm, sm.os, r0, r0 + ROWS);
     const float* S = p.ws_s32 + (size_t)bh * DK * DV;
-    fit_rows<DK, DV, false, PAIRS>(
+    fit_rows<DK, DV, false, PAIRS, ROWS>(
         [&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(S, i, sg, x); }, sm.nb, sm.perm,
         sm.phi, sm.Ct, sm.sc16, p.diag_fit);
   }
   __syncthreads();
-  pack_cols<DK, DV>(sm.Ct, sm.nb, sm.os.P, (uint32_t*)(rec + L.codes_off), sm.tail);
-  store_meta<DK>(rec, L, ntok + (unsigned)p.ntk, sm.nb, sm.sc16, sm.zz, sm.rr);
+  pack_cols<DK, DV, ROWS>(sm.Ct, sm.nb, sm.os.P, (uint32_t*)(rec + L.codes_off), sm.tail, r0);
+  store_meta<DK, ROWS>(rec, L, ntok + (unsigned)p.ntk, sm.nb, sm.sc16, sm.zz, sm.rr, r0);
 }
 
 // Code tile element: bytes when widths fit (b_max <= 8), else 16 bits.
@@ -843,16 +911,18 @@ template <bool C8>
 using CodeTile = typename std::conditional<C8, int8_t, int16_t>::type;
 
 // Threads of a requantisation block: 2 d_k, or one per (row, segment,
-// candidate lane) when that is more.
-constexpr int requant_threads(int dk, int dv, int pairs) {
-  return 2 * dk > dk * (dv / SEG) * pairs ? 2 * dk : dk * (dv / SEG) * pairs;
+// candidate lane) of its dk / parts rows when that is more.
+constexpr int requant_threads(int dk, int dv, int pairs, int parts = 1) {
+  return 2 * dk > (dk / parts) * (dv / SEG) * pairs ? 2 * dk : (dk / parts) * (dv / SEG) * pairs;
 }
 
-template <int DK, int DV, bool COMPACT, bool C8, int PAIRS = 1>
-__global__ void __launch_bounds__(requant_threads(DK, DV, PAIRS))
+// Block (head, part) = blockIdx.x / PARTS, blockIdx.x % PARTS.
+template <int DK, int DV, bool COMPACT, bool C8, int PAIRS = 1, int PARTS = 1>
+__global__ void __launch_bounds__(requant_threads(DK, DV, PAIRS, PARTS))
     __attribute__((amdgpu_waves_per_eu(4))) k_requant(KParams p) {
   __shared__ RequantLds<DK, DV, COMPACT, CodeTile<C8>> sm;
-  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS>(p, blockIdx.x, sm);
+  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS, PARTS>(p, blockIdx.x / PARTS, sm,
+                                                            blockIdx.x % PARTS);
 }
 
 // Buffer resource over n bytes at base (word 3 of a gfx9 resource: untyped
@@ -1468,16 +1538,21 @@ hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st) {
   hipError_t e = launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl,
                         (const float*)p.ws_rpart, (const double*)p.ws_gam, p.ws_bits);
   if (e != hipSuccess) return e;
-  // d_v <= 128: the fit evaluates candidate pairs (twice the lanes per head;
-  // a prefill has few heads, so the grid alone would leave SIMDs idle)
+  // d_v <= 128: the fit evaluates FL candidates of a row segment at once
+  // (FL times the lanes per head; a prefill has few heads, so the grid alone
+  // would leave SIMDs idle, and the rows with the longest candidate scans
+  // would set the time of the block)
+  // and two blocks share each head (rows split in halves)
+  constexpr int FL = 4, PT = 2;
   const bool c8 = DK > 128 || p.bmax <= 8;
-  constexpr int T64 = requant_threads(64, 64, 2), T128 = requant_threads(128, 128, 2);
+  constexpr int T64 = requant_threads(64, 64, FL, PT), T128 = requant_threads(128, 128, FL, PT);
+  const int nblk = p.B * p.H * PT;
   if (DK == 64)
-    return c8 ? launch("requant", k_requant<64, 64, false, true, 2>, p.B * p.H, T64, 0, st, p)
-              : launch("requant", k_requant<64, 64, false, false, 2>, p.B * p.H, T64, 0, st, p);
+    return c8 ? launch("requant", k_requant<64, 64, false, true, FL, PT>, nblk, T64, 0, st, p)
+              : launch("requant", k_requant<64, 64, false, false, FL, PT>, nblk, T64, 0, st, p);
   if (DK == 256) return launch("requant", k_requant<256, 256, false, true>, p.B * p.H, 512, 0, st, p);
-  return c8 ? launch("requant", k_requant<128, 128, false, true, 2>, p.B * p.H, T128, 0, st, p)
-            : launch("requant", k_requant<128, 128, false, false, 2>, p.B * p.H, T128, 0, st, p);
+  return c8 ? launch("requant", k_requant<128, 128, false, true, FL, PT>, nblk, T128, 0, st, p)
+            : launch("requant", k_requant<128, 128, false, false, FL, PT>, nblk, T128, 0, st, p);
 }
 
 hipError_t launch_prefill(KParams p, int C, hipStream_t st) {

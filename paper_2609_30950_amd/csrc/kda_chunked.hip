@@ -193,28 +193,39 @@ __device__ __forceinline__ void prep_unit(const KParams& p, int C, uint8_t* cws,
     const int j = sg * SEGL + u;
     sv[u] = j < n ? (p.per_head ? p.s[th(j)] : p.s[th(j) * DK + ri]) : 0.f;
   }
-  for (int e = t; e < CT * V8; e += NTP) {
+  // every load is issued before the first LDS store, so that the round
+  // trips overlap
+  constexpr int NE = CT * V8 / NTP;   // 16-byte vectors per thread and array
+  static_assert(CT * V8 % NTP == 0, "whole vectors per thread");
+  uint4 kv[NE], qv[NE], vv[NE];
+#pragma unroll
+  for (int r = 0; r < NE; ++r) {
+    const int e = t + r * NTP;
     const int j = e / V8, g = e % V8;
-    uint4 kv = make_uint4(0u, 0u, 0u, 0u), qv = kv;
+    const int jv = e % CT, gv = e / CT;   // V^T: consecutive lanes, consecutive tokens
+    kv[r] = qv[r] = vv[r] = make_uint4(0u, 0u, 0u, 0u);
     if (j < n) {
-      kv = ((const uint4*)p.k)[th(j) * V8 + g];
-      qv = ((const uint4*)p.q)[th(j) * V8 + g];
+      kv[r] = ((const uint4*)p.k)[th(j) * V8 + g];
+      qv[r] = ((const uint4*)p.q)[th(j) * V8 + g];
     }
-    *(uint4*)&sm.k[j][8 * g] = kv;
-    *(uint4*)&sm.q[j][8 * g] = qv;
+    if (jv < n) vv[r] = ((const uint4*)p.v)[th(jv) * V8 + gv];
   }
-  for (int e = t; e < CT * V8; e += NTP) {
-    const int j = e % CT, g = e / CT;   // consecutive lanes: consecutive tokens
-    uint4 vv = make_uint4(0u, 0u, 0u, 0u);
-    if (j < n) vv = ((const uint4*)p.v)[th(j) * V8 + g];
-    const uint32_t x[4] = {vv.x, vv.y, vv.z, vv.w};
+  const float bt = t < CT && t < n ? p.beta[th(t)] : 0.f;
+#pragma unroll
+  for (int r = 0; r < NE; ++r) {
+    const int e = t + r * NTP;
+    const int j = e / V8, g = e % V8;
+    const int jv = e % CT, gv = e / CT;
+    *(uint4*)&sm.k[j][8 * g] = kv[r];
+    *(uint4*)&sm.q[j][8 * g] = qv[r];
+    const uint32_t x[4] = {vv[r].x, vv[r].y, vv[r].z, vv[r].w};
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      sm.vt[8 * g + 2 * u][j] = (uint16_t)(x[u] & 0xFFFFu);
-      sm.vt[8 * g + 2 * u + 1][j] = (uint16_t)(x[u] >> 16);
+      sm.vt[8 * gv + 2 * u][jv] = (uint16_t)(x[u] & 0xFFFFu);
+      sm.vt[8 * gv + 2 * u + 1][jv] = (uint16_t)(x[u] >> 16);
     }
   }
-  if (t < CT) sm.beta[t] = t < n ? p.beta[th(t)] : 0.f;
+  if (t < CT) sm.beta[t] = bt;
   __syncthreads();
 
   // decay scan and EMA sums over this thread's segment (token order, double)
@@ -535,34 +546,27 @@ struct ApplySmem {
   uint16_t ut[2][SLICE][US];    // U of the slice, transposed, bf16 hi and lo planes
 };
 
-// One write-back interval of one 64-column slice of one head: tokens
-// [p.tok0, p.tok0 + p.ntk) from the record's state; writes the outputs, the
-// float32 state, its per-slice row maxima and (slice 0) Gamma and the rate
-// codes, as the token-sequential stats kernel does.  Every product takes its
-// operands as hi and lo bf16 planes (mma3), float32 accumulation.
+// The chunk record's operands one wave of the apply holds in registers:
+// hi and lo planes of its token tile of Wk, Qhat and A, of its state-row
+// tiles of Ktil^T, its rows of Uv in the slice and gamma_{n-1} of its rows.
 template <int DK>
-__global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw) {
-  using CW = ChunkWs<DK>;
-  constexpr int RT = DK / 64;            // 16-row state tiles per wave
-  constexpr int KS = DK / 32;            // k-steps over the state's rows
-  const int nsl = p.dv / SLICE;
-  int bh, sl;
-  slice_block(p.B * p.H, nsl, bh, sl);
-  const int b = bh / p.H, h = bh % p.H;
-  const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
-  const int n = p.ntk;
-  const int k8 = 8 * (lane >> 4), l16 = lane & 15;
-  const int jrow = 16 * w + l16;
-  const uint8_t* in = cw + (size_t)bh * CW::bytes;
-  const Layout L = p.L;
-  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
-  __shared__ MetaSmem<DK> meta;
-  __shared__ ApplySmem<DK> sm;
-  extern __shared__ uint4 dyn_lds[];
-  uint32_t* words = (uint32_t*)dyn_lds;
+struct ApplyFrags {
+  static constexpr int RT = DK / 64;   // 16-row state tiles per wave
+  static constexpr int KS = DK / 32;   // k-steps over the state's rows
+  uint4 fw[2][KS], fq[2][KS], fa[2][CT / 32], fk[2][RT][CT / 32];
+  float fu[4][4], fg[RT][4];
+};
 
-  // the chunk record's operands of this lane (hi and lo planes), loaded
-  // before the state's record so that both round trips overlap
+// Wave w (of the four of a slice) of slice sl; `in` is the head's chunk record.
+// PART 1: the operands of the first products (Wk, Qhat, Uv, gamma), PART 2:
+// the later ones (A, Ktil^T), 3: all.
+template <int DK, int PART = 3>
+__device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, int sl, int w,
+                                           ApplyFrags<DK>& f) {
+  using CW = ChunkWs<DK>;
+  constexpr int RT = ApplyFrags<DK>::RT, KS = ApplyFrags<DK>::KS;
+  const int lane = lane_id(), k8 = 8 * (lane >> 4), l16 = lane & 15;
+  const int jrow = 16 * w + l16;
   const uint16_t* wk = (const uint16_t*)(in + CW::wk);
   const uint16_t* qh = (const uint16_t*)(in + CW::qh);
   const uint16_t* am = (const uint16_t*)(in + CW::am);
@@ -571,43 +575,62 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   const float* gend = (const float*)(in + CW::gend);
   const bool erase = !p.no_erase;
   constexpr int PL = CT * DK;            // elements of one plane
-  uint4 fw[2][KS], fq[2][KS], fa[2][CT / 32], fk[2][RT][CT / 32];
-  float fu[4][4], fg[RT][4];
 #pragma unroll
   for (int hl = 0; hl < 2; ++hl) {
+    if constexpr ((PART & 1) != 0) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      fw[hl][ks] = erase ? *(const uint4*)&wk[hl * PL + jrow * DK + 32 * ks + k8]
-                         : make_uint4(0u, 0u, 0u, 0u);
-      fq[hl][ks] = *(const uint4*)&qh[hl * PL + jrow * DK + 32 * ks + k8];
+      for (int ks = 0; ks < KS; ++ks) {
+        f.fw[hl][ks] = erase ? *(const uint4*)&wk[hl * PL + jrow * DK + 32 * ks + k8]
+                             : make_uint4(0u, 0u, 0u, 0u);
+        f.fq[hl][ks] = *(const uint4*)&qh[hl * PL + jrow * DK + 32 * ks + k8];
+      }
     }
+    if constexpr ((PART & 2) != 0) {
 #pragma unroll
-    for (int ks = 0; ks < CT / 32; ++ks)
-      fa[hl][ks] = 32 * ks <= 16 * w + 15 ? *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8]
-                                          : make_uint4(0u, 0u, 0u, 0u);
+      for (int ks = 0; ks < CT / 32; ++ks)
+        f.fa[hl][ks] = 32 * ks <= 16 * w + 15 ? *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8]
+                                              : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int ks = 0; ks < CT / 32; ++ks)
+          f.fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
+    }
+  }
+  if constexpr ((PART & 1) != 0) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int ks = 0; ks < CT / 32; ++ks)
-        fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
+      for (int r = 0; r < 4; ++r) f.fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        f.fu[ct][r] = uv[(16 * w + 4 * (lane >> 4) + r) * DK + SLICE * sl + 16 * ct + l16];
   }
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
-#pragma unroll
-  for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) fu[ct][r] = uv[(16 * w + 4 * (lane >> 4) + r) * DK + SLICE * sl + 16 * ct + l16];
+}
 
-  {
-    // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
-    const uint4* src = (const uint4*)(rec + L.codes_off);
-    constexpr int Q = SLICE / 4;
-    const int n4 = L.wc * Q;
-    for (int e = t; e < n4; e += NT) ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
-  }
-  load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
+// One write-back interval of one 64-column slice of one head, tokens
+// [p.tok0, p.tok0 + p.ntk), by the four waves w of the slice (t: thread
+// within them); every thread of the block calls it (two barriers).  s0(i, c)
+// is the dequantised state at row i, column c of the slice; rates(t, m0, e0)
+// gives the EMA values stored with the state (threads t < DK of slice 0).
+// Writes the outputs, the float32 state, its per-slice row maxima and (slice
+// 0) Gamma and the rate codes, as the token-sequential stats kernel does.
+// Every product takes its operands as hi and lo bf16 planes (mma3), float32
+// accumulation.
+template <int DK, typename S0, typename Rates>
+__device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in, int bh, int sl, int w,
+                                            int t, const ApplyFrags<DK>& f, ApplySmem<DK>& sm,
+                                            S0 s0, Rates rates) {
+  using CW = ChunkWs<DK>;
+  constexpr int RT = ApplyFrags<DK>::RT, KS = ApplyFrags<DK>::KS;
+  const int nsl = p.dv / SLICE;
+  const int b = bh / p.H, h = bh % p.H;
+  const int lane = lane_id();
+  const int n = p.ntk;
+  const int k8 = 8 * (lane >> 4), l16 = lane & 15;
+  const bool erase = !p.no_erase;
 
   // S0 at this lane's state-tile positions: float32 gamma_{n-1} * S0 as the
   // accumulator of S_n, S0^T in LDS as hi and lo planes for the products
@@ -617,16 +640,11 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * (RT * w + rt) + 4 * (lane >> 4) + r;
-      const uint4 d = meta.desc[i];
-      const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
-      const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
         const int c = 16 * ct + l16;
-        const uint32_t lo = words[d.x + c], hi = words[d.x + SLICE + c];
-        const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
-        const float x = ((float)code + add) * mul;
-        acc[rt][ct][r] = fg[rt][r] * x;
+        const float x = s0(i, c);
+        acc[rt][ct][r] = f.fg[rt][r] * x;
         const uint16_t xh = bf16_rne(x);
         sm.s0t[0][c][i] = xh;
         sm.s0t[1][c][i] = bf16_lo(x, xh);
@@ -648,8 +666,8 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     for (int ct = 0; ct < 4; ++ct) {
       const uint4 bh_ = *(const uint4*)&sm.s0t[0][16 * ct + l16][32 * ks + k8];
       const uint4 bl_ = *(const uint4*)&sm.s0t[1][16 * ct + l16][32 * ks + k8];
-      if (erase) aw[ct] = mma3(fw[0][ks], fw[1][ks], bh_, bl_, aw[ct]);
-      ao[ct] = mma3(fq[0][ks], fq[1][ks], bh_, bl_, ao[ct]);
+      if (erase) aw[ct] = mma3(f.fw[0][ks], f.fw[1][ks], bh_, bl_, aw[ct]);
+      ao[ct] = mma3(f.fq[0][ks], f.fq[1][ks], bh_, bl_, ao[ct]);
     }
   }
   // U = Uv - W, transposed into LDS as hi and lo planes
@@ -658,7 +676,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int j = 16 * w + 4 * (lane >> 4) + r, c = 16 * ct + l16;
-      const float u = fu[ct][r] - aw[ct][r];
+      const float u = f.fu[ct][r] - aw[ct][r];
       const uint16_t uh = bf16_rne(u);
       sm.ut[0][c][j] = uh;
       sm.ut[1][c][j] = bf16_lo(u, uh);
@@ -674,7 +692,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     for (int ct = 0; ct < 4; ++ct) {
       const uint4 uh = *(const uint4*)&sm.ut[0][16 * ct + l16][32 * ks + k8];
       const uint4 ul = *(const uint4*)&sm.ut[1][16 * ct + l16][32 * ks + k8];
-      ao[ct] = mma3(fa[0][ks], fa[1][ks], uh, ul, ao[ct]);
+      ao[ct] = mma3(f.fa[0][ks], f.fa[1][ks], uh, ul, ao[ct]);
     }
   }
 #pragma unroll
@@ -696,7 +714,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
       for (int ct = 0; ct < 4; ++ct) {
         const uint4 uh = *(const uint4*)&sm.ut[0][16 * ct + l16][32 * ks + k8];
         const uint4 ul = *(const uint4*)&sm.ut[1][16 * ct + l16][32 * ks + k8];
-        acc[rt][ct] = mma3(fk[0][rt][ks], fk[1][rt][ks], uh, ul, acc[rt][ct]);
+        acc[rt][ct] = mma3(f.fk[0][rt][ks], f.fk[1][rt][ks], uh, ul, acc[rt][ct]);
       }
     }
   }
@@ -722,13 +740,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     // EMA rates after the chunk: m = (1 - alpha)^n m_0 + Q
     const double* ema = (const double*)(in + CW::ema);
     double m0, e0;
-    if (meta.ntok == 0) {
-      m0 = ema[2 * DK + t];
-      e0 = ema[3 * DK + t];
-    } else {
-      m0 = exp(-2.0 * logq_decode(meta.z[t]));
-      e0 = 2.0 * (double)f16_to_f32(meta.r16[t]);
-    }
+    rates(t, m0, e0);
     double P = 1.0;
     for (int j = 0; j < n; ++j) P *= p.one_minus_alpha;
     const double m_run = P * m0 + ema[t];
@@ -738,6 +750,56 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
+}
+
+// One write-back interval of one 64-column slice of one head from the
+// record's state (block = (head, slice), see slice_block).
+template <int DK>
+__global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw) {
+  using CW = ChunkWs<DK>;
+  const int nsl = p.dv / SLICE;
+  int bh, sl;
+  slice_block(p.B * p.H, nsl, bh, sl);
+  const int t = threadIdx.x, w = t / WAVE;
+  const uint8_t* in = cw + (size_t)bh * CW::bytes;
+  const Layout L = p.L;
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ ApplySmem<DK> sm;
+  extern __shared__ uint4 dyn_lds[];
+  uint32_t* words = (uint32_t*)dyn_lds;
+
+  // the chunk record's operands of this wave, loaded before the state's
+  // record so that both round trips overlap
+  ApplyFrags<DK> f;
+  load_frags<DK>(p, in, sl, w, f);
+  {
+    // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
+    const uint4* src = (const uint4*)(rec + L.codes_off);
+    constexpr int Q = SLICE / 4;
+    const int n4 = L.wc * Q;
+    for (int e = t; e < n4; e += NT) ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
+  }
+  load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
+  auto s0 = [&](int i, int c) {
+    const uint4 d = meta.desc[i];
+    const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
+    const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
+    const uint32_t lo = words[d.x + c], hi = words[d.x + SLICE + c];
+    const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
+    return ((float)code + add) * mul;
+  };
+  auto rates = [&](int r, double& m0, double& e0) {
+    if (meta.ntok == 0) {
+      const double* ema = (const double*)(in + CW::ema);
+      m0 = ema[2 * DK + r];
+      e0 = ema[3 * DK + r];
+    } else {
+      m0 = exp(-2.0 * logq_decode(meta.z[r]));
+      e0 = 2.0 * (double)f16_to_f32(meta.r16[r]);
+    }
+  };
+  apply_slice<DK>(p, in, bh, sl, w, t, f, sm, s0, rates);
 }
 
 size_t chunk_record_bytes(int dk) {
@@ -844,6 +906,16 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
     }
     return hipSuccess;
   };
+  auto group_of = [&](int k) {
+    int g = 0;
+    while (first(g + 1) <= k) ++g;
+    return g;
+  };
+  auto rec = [&](int k) {   // chunk k's records
+    const int g = group_of(k);
+    return (const uint8_t*)(buf(g) + (size_t)(k - first(g)) * nbh * ChunkWs<DK>::bytes);
+  };
+  auto tokens = [&](int k) { return (p.T - k * C) < C ? (p.T - k * C) : C; };
   hipError_t e = prep(0, st, false);
   if (e != hipSuccess) return e;
   if (two && ngr > 1) {
@@ -852,30 +924,28 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
     if ((e = prep(1, fk.aux, true)) != hipSuccess) return e;
     if ((e = hipEventRecord(fk.ev[2], fk.aux)) != hipSuccess) return e;
   }
-  for (int g = 0; g < ngr; ++g) {
-    if (g > 0) {
+  // interval k: apply, allocation, requantisation
+  for (int k = 0; k < nch; ++k) {
+    const int g = group_of(k);
+    if (k > 0 && k == first(g)) {
       if (two) {
         if ((e = hipStreamWaitEvent(st, fk.ev[1 + (g & 1)], 0)) != hipSuccess) return e;
       } else if ((e = prep(g, st, false)) != hipSuccess) {
         return e;
       }
     }
-    const int g0 = first(g), ng = count(g);
-    for (int c = 0; c < ng; ++c) {
-      p.tok0 = (g0 + c) * C;
-      p.ntk = (p.T - p.tok0) < C ? (p.T - p.tok0) : C;
-      e = launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p,
-                 (const uint8_t*)(buf(g) + (size_t)c * nbh * ChunkWs<DK>::bytes));
-      if (e != hipSuccess) return e;
-      e = launch_chunk_writeback(p, nsl, st);
-      if (e != hipSuccess) return e;
-    }
-    if (two && g + 2 < ngr) {
-      // group g + 2 reuses this group's records once its intervals are done
+    p.tok0 = k * C;
+    p.ntk = tokens(k);
+    e = launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p, rec(k));
+    if (e != hipSuccess) return e;
+    if (two && k == first(g) + count(g) - 1 && g + 2 < ngr) {
+      // chunk k's apply is the last read of group g's records: group g + 2
+      // reuses them
       if ((e = fk.fork()) != hipSuccess) return e;
       if ((e = prep(g + 2, fk.aux, true)) != hipSuccess) return e;
       if ((e = hipEventRecord(fk.ev[1 + (g & 1)], fk.aux)) != hipSuccess) return e;
     }
+    if ((e = launch_chunk_writeback(p, nsl, st)) != hipSuccess) return e;
   }
   return hipSuccess;   // fk joins aux into st
 }

@@ -558,8 +558,8 @@ struct ApplyFrags {
 };
 
 // Wave w (of the four of a slice) of slice sl; `in` is the head's chunk record.
-// PART 1: the operands of the first products (Wk, Qhat, Uv, gamma), PART 2:
-// the later ones (A, Ktil^T), 3: all.
+// PART 1: the operands of the first products (Wk, Qhat, gamma), PART 2: the
+// later ones (Uv, A, Ktil^T), 3: all.
 template <int DK, int PART = 3>
 __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, int sl, int w,
                                            ApplyFrags<DK>& f) {
@@ -602,6 +602,8 @@ __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, 
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) f.fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+  }
+  if constexpr ((PART & 2) != 0) {
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
@@ -755,7 +757,8 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
 // One write-back interval of one 64-column slice of one head from the
 // record's state (block = (head, slice), see slice_block).
 template <int DK>
-__global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw) {
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
+    k_chunk_apply(KParams p, const uint8_t* cw) {
   using CW = ChunkWs<DK>;
   const int nsl = p.dv / SLICE;
   int bh, sl;
@@ -772,7 +775,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
   // the chunk record's operands of this wave, loaded before the state's
   // record so that both round trips overlap
   ApplyFrags<DK> f;
-  load_frags<DK>(p, in, sl, w, f);
+  load_frags<DK, 1>(p, in, sl, w, f);
   {
     // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
     const uint4* src = (const uint4*)(rec + L.codes_off);
@@ -781,6 +784,7 @@ __global__ void __launch_bounds__(NT) k_chunk_apply(KParams p, const uint8_t* cw
     for (int e = t; e < n4; e += NT) ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
   }
   load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
+  load_frags<DK, 2>(p, in, sl, w, f);           // the later products' operands
   auto s0 = [&](int i, int c) {
     const uint4 d = meta.desc[i];
     const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);

@@ -28,7 +28,7 @@ ROOT = os.path.dirname(HERE)
 
 # device-kernel sources that the counter summaries describe
 KERNEL_SOURCES = ("kda_alloc.hpp", "kda_chunked.hip", "kda_device.hpp", "kda_kernels.hip",
-                  "kda_kernels.hpp", "kda_record.hpp", "kda_recur.hpp")
+                  "kda_kernels.hpp", "kda_record.hpp", "kda_recur.hpp", "kda_requant.hpp")
 
 
 def source_hash():

@@ -20,6 +20,7 @@
 #pragma once
 
 #include "kda_device.hpp"
+#include "kda_kernels.hpp"
 
 namespace kda {
 
@@ -319,6 +320,62 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     const int n = tid + k * nt;
     if (n < N) out[n] = (uint8_t)(bmin + slots_ge(E[k], beta + 1, bmin, L) + sm.extra[n]);
   }
+}
+
+// Row statistics of one write-back for one head (threads t < DK own row t).
+template <int DK>
+struct StatSmem {
+  float R[DK];     // first member: 16-byte aligned with the struct
+  double gam[DK];
+  double rms[DK];
+  double c[DK];
+};
+
+// Sum of squares of the float32 values x[r0..r1) in float64, in order; with
+// 16-byte aligned bounds the reads are issued four values at a time ahead of
+// the sequential sum.
+__device__ __forceinline__ double run_sumsq(const float* x, int r0, int r1) {
+  double acc = 0.0;
+  int j = r0;
+  if (((r0 | r1) & 3) == 0) {
+    const float4* x4 = (const float4*)(x + r0);
+#pragma unroll 4
+    for (; j < r1; j += 4) {
+      const float4 v = x4[(j - r0) >> 2];
+      acc = acc + (double)v.x * (double)v.x;
+      acc = acc + (double)v.y * (double)v.y;
+      acc = acc + (double)v.z * (double)v.z;
+      acc = acc + (double)v.w * (double)v.w;
+    }
+  }
+  for (; j < r1; ++j) acc = acc + (double)x[j] * (double)x[j];
+  return acc;
+}
+
+// Weights c = Gamma R~^2 from the row ranges st.R (group RMS in float64: the
+// squares summed in runs of RMS_RUN rows, each run in row order, the run
+// sums in order).  The caller has synchronised after writing st.R.
+template <int DK>
+__device__ __forceinline__ void row_weights(const KParams& p, int bh, StatSmem<DK>& st, int t) {
+  const int G = p.G, runs = (G + RMS_RUN - 1) / RMS_RUN;
+  if (t < (DK / G) * runs) {
+    const int g = t / runs, r0 = g * G + (t % runs) * RMS_RUN;
+    st.c[t] = run_sumsq(st.R, r0, min(r0 + RMS_RUN, (g + 1) * G));   // run sums, in the
+    // space of the weights until those are formed
+  }
+  __syncthreads();
+  if (t < DK / G) {
+    double acc = 0.0;
+    for (int k = 0; k < runs; ++k) acc = acc + st.c[t * runs + k];
+    st.rms[t] = sqrt(acc / (double)G);
+  }
+  __syncthreads();
+  if (t < DK) {
+    const double c = mode_key(p.weight_mode, st.gam[t], st.R[t], st.rms[t / p.G]);
+    st.c[t] = c;
+    p.ws_c[(size_t)bh * DK + t] = c;
+  }
+  __syncthreads();
 }
 
 }  // namespace kda

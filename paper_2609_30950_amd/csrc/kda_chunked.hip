@@ -43,6 +43,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kda_alloc.hpp"
 #include "kda_device.hpp"
 #include "kda_kernels.hpp"
 #include "kda_profile.hpp"
@@ -624,7 +625,8 @@ __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, 
 template <int DK, typename S0, typename Rates>
 __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in, int bh, int sl, int w,
                                             int t, const ApplyFrags<DK>& f, ApplySmem<DK>& sm,
-                                            S0 s0, Rates rates) {
+                                            S0 s0, Rates rates, float* rmax_lds = nullptr,
+                                            double* gam_lds = nullptr) {
   using CW = ChunkWs<DK>;
   constexpr int RT = ApplyFrags<DK>::RT, KS = ApplyFrags<DK>::KS;
   const int nsl = p.dv / SLICE;
@@ -735,7 +737,10 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
         m = fmaxf(m, fabsf(x));
       }
       m = max16(m);
-      if (l16 == 0) p.ws_rpart[((size_t)bh * DK + i) * nsl + sl] = m;
+      if (l16 == 0) {
+        p.ws_rpart[((size_t)bh * DK + i) * nsl + sl] = m;
+        if (rmax_lds != nullptr) rmax_lds[sl * DK + i] = m;
+      }
     }
   }
   if (sl == 0 && t < DK) {
@@ -749,7 +754,9 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
     const double e_run = P * e0 + ema[DK + t];
     const double s_hat = -0.5 * log(m_run);
     const double r = 0.5 * e_run;
-    p.ws_gam[(size_t)bh * DK + t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
+    const double gm = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
+    p.ws_gam[(size_t)bh * DK + t] = gm;
+    if (gam_lds != nullptr) gam_lds[t] = gm;
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
 }
@@ -804,6 +811,70 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
     }
   };
   apply_slice<DK>(p, in, bh, sl, w, t, f, sm, s0, rates);
+}
+
+// The same interval for all slices of one head in one block (four waves per
+// slice, block = head), used when the normalisation groups lie within a head:
+// the block then holds every row's maximum and Gamma and forms the allocation
+// weights itself (row maxima over the slices, group RMS, keys into ws_c), so
+// that the allocation that follows only selects.
+template <int DK>
+__global__ void __launch_bounds__((DK / SLICE) * NT) __attribute__((amdgpu_waves_per_eu(2)))
+    k_chunk_apply_head(KParams p, const uint8_t* cw) {
+  using CW = ChunkWs<DK>;
+  constexpr int NSL = DK / SLICE;
+  const int bh = blockIdx.x;
+  const int t = threadIdx.x, sl = t / NT, tl = t % NT, w = tl / WAVE;
+  const uint8_t* in = cw + (size_t)bh * CW::bytes;
+  const Layout L = p.L;
+  const uint8_t* rec = slot_ptr(p.records, L.slot, bh);
+  __shared__ MetaSmem<DK> meta;
+  __shared__ ApplySmem<DK> sm[NSL];
+  __shared__ __align__(16) StatSmem<DK> st;
+  __shared__ float rmax[NSL * DK];
+  extern __shared__ uint4 dyn_lds[];
+  uint32_t* words = (uint32_t*)dyn_lds;
+
+  ApplyFrags<DK> f;
+  load_frags<DK, 1>(p, in, sl, w, f);
+  {
+    // the head's code words as stored: word kw of column j at words[kw d_v + j]
+    const uint4* src = (const uint4*)(rec + L.codes_off);
+    const int n4 = L.wc * (DK / 4);
+    for (int e = t; e < n4; e += NSL * NT) ((uint4*)words)[e] = src[e];
+  }
+  load_meta<DK, DK>(rec, L, p.bmax, meta);   // its barrier covers the staging
+  load_frags<DK, 2>(p, in, sl, w, f);         // the later products' operands
+  auto s0 = [&](int i, int c) {
+    const uint4 d = meta.desc[i];
+    const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
+    const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
+    const int j = SLICE * sl + c;
+    const uint32_t lo = words[d.x + j], hi = words[d.x + DK + j];
+    const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
+    return ((float)code + add) * mul;
+  };
+  auto rates = [&](int r, double& m0, double& e0) {
+    if (meta.ntok == 0) {
+      const double* ema = (const double*)(in + CW::ema);
+      m0 = ema[2 * DK + r];
+      e0 = ema[3 * DK + r];
+    } else {
+      m0 = exp(-2.0 * logq_decode(meta.z[r]));
+      e0 = 2.0 * (double)f16_to_f32(meta.r16[r]);
+    }
+  };
+  apply_slice<DK>(p, in, bh, sl, w, tl, f, sm[sl], s0, rates, rmax, st.gam);
+  __syncthreads();
+  if (t < DK) {
+    // the row's range: the maximum over the slices in slice order
+    float m = rmax[t];
+#pragma unroll
+    for (int q = 1; q < NSL; ++q) m = fmaxf(m, rmax[q * DK + t]);
+    st.R[t] = m;
+  }
+  __syncthreads();
+  row_weights<DK>(p, bh, st, t);   // group RMS and keys into ws_c
 }
 
 size_t chunk_record_bytes(int dk) {
@@ -886,6 +957,9 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
   const int nch = (p.T + C - 1) / C;
   const int gc = chunk_group(nbh);
   const size_t dyn = (size_t)(p.L.wc + 1) * SLICE * 4;
+  // groups within a head: one apply block per head forms the allocation keys
+  const bool keys = p.G <= DK;
+  const size_t dyn_head = (size_t)(p.L.wc + 1) * DK * 4;
   const size_t half = (size_t)gc * nbh * ChunkWs<DK>::bytes;   // records of up to gc chunks
   AuxFork fk(st, nch > 1 ? aux_stream : nullptr);
   const bool two = fk.ok;
@@ -940,7 +1014,8 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
     }
     p.tok0 = k * C;
     p.ntk = tokens(k);
-    e = launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p, rec(k));
+    e = keys ? launch("apply", k_chunk_apply_head<DK>, nbh, nsl * NT, dyn_head, st, p, rec(k))
+             : launch("apply", k_chunk_apply<DK>, nbh * nsl, NT, dyn, st, p, rec(k));
     if (e != hipSuccess) return e;
     if (two && k == first(g) + count(g) - 1 && g + 2 < ngr) {
       // chunk k's apply is the last read of group g's records: group g + 2
@@ -949,7 +1024,7 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
       if ((e = prep(g + 2, fk.aux, true)) != hipSuccess) return e;
       if ((e = hipEventRecord(fk.ev[1 + (g & 1)], fk.aux)) != hipSuccess) return e;
     }
-    if ((e = launch_chunk_writeback(p, nsl, st)) != hipSuccess) return e;
+    if ((e = launch_chunk_writeback(p, nsl, st, keys)) != hipSuccess) return e;
   }
   return hipSuccess;   // fk joins aux into st
 }

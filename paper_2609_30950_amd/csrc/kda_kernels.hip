@@ -151,15 +151,6 @@ __device__ __forceinline__ void row_max(const float (&X)[ROW_BLOCK][DV / WAVE], 
 
 // ---------------------------------------------------------- kernels ---
 
-// Row statistics of one write-back for one head (threads t < DK own row t).
-template <int DK>
-struct StatSmem {
-  float R[DK];     // first member: 16-byte aligned with the struct
-  double gam[DK];
-  double rms[DK];
-  double c[DK];
-};
-
 // Rate statistics of row t after the interval (threads t < DK): s^, r, the
 // weight Gamma^ (or the given window weight) and the stored rate codes.
 template <int DK>
@@ -171,53 +162,6 @@ __device__ __forceinline__ void row_rates(const KParams& p, int bh, StatSmem<DK>
     st.gam[t] = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
     p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
   }
-}
-
-// Sum of squares of the float32 values x[r0..r1) in float64, in order; with
-// 16-byte aligned bounds the reads are issued four values at a time ahead of
-// the sequential sum.
-__device__ __forceinline__ double run_sumsq(const float* x, int r0, int r1) {
-  double acc = 0.0;
-  int j = r0;
-  if (((r0 | r1) & 3) == 0) {
-    const float4* x4 = (const float4*)(x + r0);
-#pragma unroll 4
-    for (; j < r1; j += 4) {
-      const float4 v = x4[(j - r0) >> 2];
-      acc = acc + (double)v.x * (double)v.x;
-      acc = acc + (double)v.y * (double)v.y;
-      acc = acc + (double)v.z * (double)v.z;
-      acc = acc + (double)v.w * (double)v.w;
-    }
-  }
-  for (; j < r1; ++j) acc = acc + (double)x[j] * (double)x[j];
-  return acc;
-}
-
-// Weights c = Gamma R~^2 from the row ranges st.R (group RMS in float64: the
-// squares summed in runs of RMS_RUN rows, each run in row order, the run
-// sums in order).  The caller has synchronised after writing st.R.
-template <int DK>
-__device__ __forceinline__ void row_weights(const KParams& p, int bh, StatSmem<DK>& st, int t) {
-  const int G = p.G, runs = (G + RMS_RUN - 1) / RMS_RUN;
-  if (t < (DK / G) * runs) {
-    const int g = t / runs, r0 = g * G + (t % runs) * RMS_RUN;
-    st.c[t] = run_sumsq(st.R, r0, min(r0 + RMS_RUN, (g + 1) * G));   // run sums, in the
-    // space of the weights until those are formed
-  }
-  __syncthreads();
-  if (t < DK / G) {
-    double acc = 0.0;
-    for (int k = 0; k < runs; ++k) acc = acc + st.c[t * runs + k];
-    st.rms[t] = sqrt(acc / (double)G);
-  }
-  __syncthreads();
-  if (t < DK) {
-    const double c = mode_key(p.weight_mode, st.gam[t], st.R[t], st.rms[t / p.G]);
-    st.c[t] = c;
-    p.ws_c[(size_t)bh * DK + t] = c;
-  }
-  __syncthreads();
 }
 
 // Decode steps of heads with d_k <= 128 hand the requantisation the token's
@@ -998,9 +942,11 @@ static hipError_t launch_interval_slices(const KParams& p, hipStream_t st) {
   return launch_chunk_writeback(p, nsl, st);
 }
 
-static hipError_t launch_chunk_alloc(const KParams& p, int nsl, hipStream_t st) {
+static hipError_t launch_chunk_alloc(const KParams& p, int nsl, hipStream_t st, bool keys) {
   const int units = p.scope == 0 ? p.B : p.B * p.H;
   const int N = p.scope == 0 ? p.H * p.dk : p.dk;
+  if (keys)
+    return launch("alloc", k_alloc, units, 1024, 0, st, p.ws_c, N, p.need, p.bmin, p.bmax, p.ws_bits);
   return launch("alloc", k_alloc_slices, units, 1024, 0, st, p, N, nsl,
                 (const float*)p.ws_rpart, (const double*)p.ws_gam, p.ws_bits);
 }
@@ -1024,8 +970,8 @@ static hipError_t launch_chunk_requant(const KParams& p, hipStream_t st) {
             : launch("requant", k_requant<128, 128, false, false, FL, PT>, nblk, T128, 0, st, p);
 }
 
-hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st) {
-  const hipError_t e = launch_chunk_alloc(p, nsl, st);
+hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st, bool keys) {
+  const hipError_t e = launch_chunk_alloc(p, nsl, st, keys);
   return e != hipSuccess ? e : launch_chunk_requant(p, st);
 }
 

@@ -46,8 +46,8 @@ hipError_t launch_step_writeback(const KParams& p, hipStream_t st);
 hipError_t launch_prefill(KParams p, int C, hipStream_t st);
 // Allocation and requantisation of one prefill write-back from the float32
 // state, per-slice row maxima (nsl per row), Gamma and rate codes in the
-// workspace.
-hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st);
+// workspace (keys: the allocation weights are in ws_c already).
+hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st, bool keys = false);
 // Chunked prefill (WY/UT form on MFMA), d_k = d_v in {64, 128}, C <= 64.
 hipError_t launch_prefill_chunked(const KParams& p, int C, hipStream_t st, hipStream_t aux);
 // Bytes of one chunk record (per chunk and head) and chunks per group for

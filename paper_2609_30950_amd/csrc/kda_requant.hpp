@@ -513,9 +513,14 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
     const float* hv = p.ws_hv + (size_t)bh * (DV + 2 * DK);
     load_meta<DK, DV>(rec, L, p.bmax, sm.rb.meta);   // synchronises
     // the record's code words, column-major: word k of column j at
-    // stg[j * str + k], so a field that straddles two words is one pair
+    // stg[j * STR + k], so a field that straddles two words is one pair; the
+    // stride is the largest word count of any width bound the tile holds,
+    // plus one (odd: the columns of a wave's lanes fall in distinct banks),
+    // and a compile-time constant, so every read below is one immediate
+    // offset from the lane's base address
     uint32_t* stg = (uint32_t*)sm.Ct;
-    const int str = L.wc + 1;
+    constexpr int STR = DK * (sizeof(CT) == 1 ? 8 : MAX_B) / 32 + 1;
+    const int str = STR;
     const int nw = (sm.rb.meta.P[DK] + 31) >> 5;
     const uint4* src = (const uint4*)(rec + L.codes_off);
     for (int e = t; e < nw * (DV / 4); e += blockDim.x) {

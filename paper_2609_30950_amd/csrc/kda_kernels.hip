@@ -239,6 +239,9 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
     fresh = false;
   };
   ema(in);
+  // the step's rates and weights (float64 chains of the row threads) while
+  // the code words are in flight
+  row_rates<DK>(p, bh, st, m_run, e_run, t);
 #pragma unroll
   for (int u = 0; u < NPT; ++u) {
     const int e = t + u * (int)blockDim.x;
@@ -263,7 +266,6 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
     recur_token<DK, DV, BF16>(X, sm.rs, sm.rsm, p.v, th * DV, p.o + th * DV, !p.no_erase,
                               compact ? hv : nullptr);
   }
-  row_rates<DK>(p, bh, st, m_run, e_run, t);
   if (!compact) {
     // float32 state after the last token, row-major, for the requantisation
     const int w = t / WAVE, lane = lane_id();

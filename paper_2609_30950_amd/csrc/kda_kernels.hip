@@ -176,13 +176,20 @@ template <int DK, int DV>
 struct StatsLds {
   MetaSmem<DK> meta;
   RowSmem<DK> rs;
-  RecSmem<DK, DV> rsm;
   __align__(16) StatSmem<DK> st;
 };
 
-// Bytes of the code-word staging area that follows StatsLds.
+// Bytes of the code-word staging area that follows StatsLds.  The
+// recurrence's partials reuse it once the words are decoded (so a block needs
+// less LDS and more blocks fit a compute unit), and so does the per-head
+// allocator after the recurrence.
 __host__ __device__ inline size_t stats_words_bytes(int wc, int dv) {
   return (size_t)(wc + 1) * dv * 4;
+}
+template <int DK, int DV>
+inline size_t stats_dyn_bytes(int wc) {
+  const size_t w = stats_words_bytes(wc, DV);
+  return w > sizeof(RecSmem<DK, DV>) ? w : sizeof(RecSmem<DK, DV>);
 }
 
 // Decode token tok0 of one head with the state resident in registers,
@@ -263,7 +270,8 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
       hv[DV + DK + t] = sm.rs.gq[t].x;   // g = fl32(beta k)
     }
     const size_t th = ((size_t)b * p.T + tok) * p.H + h;
-    recur_token<DK, DV, BF16>(X, sm.rs, sm.rsm, p.v, th * DV, p.o + th * DV, !p.no_erase,
+    // the words are decoded (barrier above): their space holds the partials
+    recur_token<DK, DV, BF16>(X, sm.rs, *(RecSmem<DK, DV>*)words, p.v, th * DV, p.o + th * DV, !p.no_erase,
                               compact ? hv : nullptr);
   }
   if (!compact) {
@@ -294,7 +302,7 @@ __device__ __forceinline__ void stats_head(const KParams& p, int bh, StatsLds<DK
 }
 
 template <int DK, int DV, bool HEAD, bool BF16>
-__global__ void __launch_bounds__(2 * DK) k_chunk(KParams p) {
+__global__ void __launch_bounds__(2 * DK) __attribute__((amdgpu_waves_per_eu(6))) k_chunk(KParams p) {
   extern __shared__ uint4 dyn_lds[];
   __shared__ StatsLds<DK, DV> sm;
   uint32_t* words = (uint32_t*)dyn_lds;
@@ -890,7 +898,7 @@ static hipError_t launch_interval_t(const KParams& p, hipStream_t st, int phases
   if (phases & 1) {
     // code-word staging; with the per-head budget the allocator's scratch
     // reuses it after the words are decoded
-    size_t dyn = stats_words_bytes(p.L.wc, DV);
+    size_t dyn = stats_dyn_bytes<DK, DV>(p.L.wc);
     if (p.scope == 1 && dyn < sizeof(AllocSmem)) dyn = sizeof(AllocSmem);
     if (p.scope == 1)
       e = p.in_bf16 ? launch("stats", k_chunk<DK, DV, true, true>, nbh, 2 * DK, dyn, st, p)

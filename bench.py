@@ -192,12 +192,13 @@ def run_state32_reference(w, args, K, torch):
                 device_copy_GBps=2 * half / (copy_ms * 1e-3) / 1e9)
 
 
-# Chunked prefill: one chunk record per chunk and head (bytes at d_k = d_v =
-# 128: Wk, Qhat, Ktil^T bf16 [64][128], A bf16 [64][64], Uv f32 [64][128],
-# gamma f32 [128], EMA sums f64 [4][128]).
-# per chunk and head at d = 128: Wk, Qhat, Ktil^T and A as bf16 hi and lo
-# planes, Uv float32, gamma_end float32, EMA sums float64
-CHUNK_RECORD_BYTES = 2 * (3 * 64 * 128 * 2 + 64 * 64 * 2) + 64 * 128 * 4 + 128 * 4 + 4 * 128 * 8
+# Chunked prefill: what the apply reads of one chunk record per head at
+# d_k = d_v = 128: Wk, Qhat, Ktil^T [64][128] and A [64][64] as bf16 hi and lo
+# planes, Uv float32 [64][128], gamma_end float32 [128], Gamma float64 [128]
+# and the rate codes u32 [128] (the EMA sums stored beside them are read by
+# the rate pass, not by the apply)
+CHUNK_RECORD_BYTES = (2 * (3 * 64 * 128 * 2 + 64 * 64 * 2) + 64 * 128 * 4 + 128 * 4
+                      + 128 * 8 + 128 * 4)
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 

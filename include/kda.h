@@ -298,7 +298,7 @@ int kda_gate_quant(const kda_config* cfg, int32_t T, int32_t bits, int32_t mode,
  * chunked (WY/UT) form of eq. rule; C must then be at most 64 (KDA_ERR_ARG
  * otherwise) and the workspace (kda_workspace_bytes of the same config) also
  * holds the per-chunk records of two groups of up to 16 chunks per head
- * (152 064 bytes per chunk and head at d_k = 128).  All work is enqueued on
+ * (153 600 bytes per chunk and head at d_k = 128).  All work is enqueued on
  * `stream`.
  * In:  q, k [B][T][H][d_k] bf16 (raw 16-bit patterns); v [B][T][H][d_v] bf16;
  *      s [B][T][H][d_k] f32 (or [B][T][H]); beta [B][T][H] f32; gamma as in

@@ -133,7 +133,9 @@ struct ChunkWs {
   static constexpr size_t uv = am + (size_t)2 * CT * CT * 2;  // f32 [CT][DK]: T diag(beta) V
   static constexpr size_t gend = uv + (size_t)CT * DK * 4;// f32 [DK]: gamma_{n-1}
   static constexpr size_t ema = gend + (size_t)DK * 4;    // f64 [4][DK]: Q_m, Q_e, first samples
-  static constexpr size_t bytes = (ema + (size_t)4 * DK * 8 + 255) / 256 * 256;
+  static constexpr size_t gam = ema + (size_t)4 * DK * 8; // f64 [DK]: Gamma after the chunk
+  static constexpr size_t zr = gam + (size_t)DK * 8;      // u32 [DK]: rate codes stored after it
+  static constexpr size_t bytes = (zr + (size_t)DK * 4 + 255) / 256 * 256;
 };
 
 template <int DK>
@@ -616,16 +618,15 @@ __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, 
 // One write-back interval of one 64-column slice of one head, tokens
 // [p.tok0, p.tok0 + p.ntk), by the four waves w of the slice (t: thread
 // within them); every thread of the block calls it (two barriers).  s0(i, c)
-// is the dequantised state at row i, column c of the slice; rates(t, m0, e0)
-// gives the EMA values stored with the state (threads t < DK of slice 0).
+// is the dequantised state at row i, column c of the slice.
 // Writes the outputs, the float32 state, its per-slice row maxima and (slice
 // 0) Gamma and the rate codes, as the token-sequential stats kernel does.
 // Every product takes its operands as hi and lo bf16 planes (mma3), float32
 // accumulation.
-template <int DK, typename S0, typename Rates>
+template <int DK, typename S0>
 __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in, int bh, int sl, int w,
                                             int t, const ApplyFrags<DK>& f, ApplySmem<DK>& sm,
-                                            S0 s0, Rates rates, float* rmax_lds = nullptr,
+                                            S0 s0, float* rmax_lds = nullptr,
                                             double* gam_lds = nullptr) {
   using CW = ChunkWs<DK>;
   constexpr int RT = ApplyFrags<DK>::RT, KS = ApplyFrags<DK>::KS;
@@ -744,20 +745,11 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
     }
   }
   if (sl == 0 && t < DK) {
-    // EMA rates after the chunk: m = (1 - alpha)^n m_0 + Q
-    const double* ema = (const double*)(in + CW::ema);
-    double m0, e0;
-    rates(t, m0, e0);
-    double P = 1.0;
-    for (int j = 0; j < n; ++j) P *= p.one_minus_alpha;
-    const double m_run = P * m0 + ema[t];
-    const double e_run = P * e0 + ema[DK + t];
-    const double s_hat = -0.5 * log(m_run);
-    const double r = 0.5 * e_run;
-    const double gm = p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
+    // Gamma and the rate codes after the chunk (k_chunk_rates)
+    const double gm = ((const double*)(in + CW::gam))[t];
     p.ws_gam[(size_t)bh * DK + t] = gm;
     if (gam_lds != nullptr) gam_lds[t] = gm;
-    p.ws_zr[(size_t)bh * DK + t] = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
+    p.ws_zr[(size_t)bh * DK + t] = ((const uint32_t*)(in + CW::zr))[t];
   }
 }
 
@@ -800,17 +792,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
     const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
     return ((float)code + add) * mul;
   };
-  auto rates = [&](int r, double& m0, double& e0) {
-    if (meta.ntok == 0) {
-      const double* ema = (const double*)(in + CW::ema);
-      m0 = ema[2 * DK + r];
-      e0 = ema[3 * DK + r];
-    } else {
-      m0 = exp(-2.0 * logq_decode(meta.z[r]));
-      e0 = 2.0 * (double)f16_to_f32(meta.r16[r]);
-    }
-  };
-  apply_slice<DK>(p, in, bh, sl, w, t, f, sm, s0, rates);
+  apply_slice<DK>(p, in, bh, sl, w, t, f, sm, s0);
 }
 
 // The same interval for all slices of one head in one block (four waves per
@@ -854,17 +836,7 @@ __global__ void __launch_bounds__((DK / SLICE) * NT) __attribute__((amdgpu_waves
     const int code = __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh), 0, bw);
     return ((float)code + add) * mul;
   };
-  auto rates = [&](int r, double& m0, double& e0) {
-    if (meta.ntok == 0) {
-      const double* ema = (const double*)(in + CW::ema);
-      m0 = ema[2 * DK + r];
-      e0 = ema[3 * DK + r];
-    } else {
-      m0 = exp(-2.0 * logq_decode(meta.z[r]));
-      e0 = 2.0 * (double)f16_to_f32(meta.r16[r]);
-    }
-  };
-  apply_slice<DK>(p, in, bh, sl, w, tl, f, sm[sl], s0, rates, rmax, st.gam);
+  apply_slice<DK>(p, in, bh, sl, w, tl, f, sm[sl], s0, rmax, st.gam);
   __syncthreads();
   if (t < DK) {
     // the row's range: the maximum over the slices in slice order
@@ -875,6 +847,61 @@ __global__ void __launch_bounds__((DK / SLICE) * NT) __attribute__((amdgpu_waves
   }
   __syncthreads();
   row_weights<DK>(p, bh, st, t);   // group RMS and keys into ws_c
+}
+
+// Rates of the chunks first_chunk .. first_chunk + nc - 1 (one group, records
+// `cws`), one thread per row: the EMA over each chunk is m = (1 - alpha)^n m_0
+// + Q (R24) with m_0 decoded from the rate codes the previous write-back
+// stores; this chain depends on the inputs only (each write-back stores the
+// codes of the EMA values, and the next interval continues from their decoded
+// values), so it runs beside the intervals.  Writes each chunk's Gamma and
+// rate codes into its record; `carry` holds every row's last codes for the
+// next group (the call's first chunk starts from the record's codes, or from
+// its first samples if the record is fresh).
+template <int DK>
+__global__ void __launch_bounds__(256) k_chunk_rates(KParams p, int C, uint8_t* cws, int first_chunk,
+                                                     int nc, uint32_t* carry) {
+  using CW = ChunkWs<DK>;
+  const int nbh = p.B * p.H;
+  const int gi = blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= nbh * DK) return;
+  const int bh = gi / DK, t = gi % DK;
+  bool fresh = false;
+  uint32_t zr;
+  if (first_chunk == 0) {
+    const uint8_t* rec = slot_ptr(p.records, p.L.slot, bh);
+    fresh = *(const unsigned*)rec == 0u;
+    zr = (uint32_t)((const uint16_t*)(rec + p.L.z_off))[t] |
+         ((uint32_t)((const uint16_t*)(rec + p.L.r_off))[t] << 16);
+  } else {
+    zr = carry[gi];
+  }
+  for (int c = 0; c < nc; ++c) {
+    const int k = first_chunk + c;
+    const int n = (p.T - k * C) < C ? (p.T - k * C) : C;
+    uint8_t* out = cws + ((size_t)c * nbh + bh) * CW::bytes;
+    const double* ema = (const double*)(out + CW::ema);
+    double m0, e0;
+    if (fresh) {
+      m0 = ema[2 * DK + t];
+      e0 = ema[3 * DK + t];
+      fresh = false;
+    } else {
+      m0 = exp(-2.0 * logq_decode((uint16_t)(zr & 0xffffu)));
+      e0 = 2.0 * (double)f16_to_f32((uint16_t)(zr >> 16));
+    }
+    double P = 1.0;
+    for (int j = 0; j < n; ++j) P *= p.one_minus_alpha;
+    const double m_run = P * m0 + ema[t];
+    const double e_run = P * e0 + ema[DK + t];
+    const double s_hat = -0.5 * log(m_run);
+    const double r = 0.5 * e_run;
+    ((double*)(out + CW::gam))[t] =
+        p.gamma ? p.gamma[(size_t)bh * DK + t] : mode_gamma(p.weight_mode, s_hat, r, p.wb_C);
+    zr = (uint32_t)logq_encode(s_hat) | ((uint32_t)r_encode(r) << 16);
+    ((uint32_t*)(out + CW::zr))[t] = zr;
+  }
+  carry[gi] = zr;
 }
 
 size_t chunk_record_bytes(int dk) {
@@ -982,7 +1009,10 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
                                   NTP, 0, s, q, C, buf(g), u0);
       if (e != hipSuccess) return e;
     }
-    return hipSuccess;
+    // the group's rates, continued from the previous group's (the decode
+    // step's token-vector space of the workspace carries them between groups)
+    return launch("rates", k_chunk_rates<DK>, (nbh * DK + 255) / 256, 256, 0, s, p, C, buf(g), first(g),
+                  count(g), (uint32_t*)p.ws_hv);
   };
   auto group_of = [&](int k) {
     int g = 0;

@@ -74,11 +74,12 @@ __device__ __forceinline__ unsigned long long frac_bits(double c) {
   return (unsigned long long)ldexp(m, 53) - (1ull << 52);
 }
 
-// c_at(n): weight of row n (any address space); out: N widths.  RPT: rows per
-// thread, at least ceil(N / blockDim.x).
+// c_at(n): weight of row n (any address space); out[n - lo]: the widths of
+// rows lo <= n < hi (the rest are not written).  RPT: rows per thread, at least
+// ceil(N / blockDim.x).
 template <int RPT, typename Load>
 __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int bmin, int bmax, uint8_t* out,
-                               AllocSmem& sm) {
+                               AllocSmem& sm, int lo = 0, int hi = 0x7fffffff) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id();
   const int L = bmax - bmin;
   // rows n = tid + k * nt, k < RPT, their weights held in registers (read
@@ -139,7 +140,8 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
   const long long ptot = (long long)npos * L;
 
   if (need <= 0) {
-    for (int n = tid; n < N; n += nt) out[n] = (uint8_t)bmin;
+    for (int n = tid; n < N; n += nt)
+      if (n >= lo && n < hi) out[n - lo] = (uint8_t)bmin;
     return;
   }
   if (ptot <= need) {
@@ -161,7 +163,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
           g = g < 0 ? 0 : (g > L ? L : g);
           b = bmin + (int)g;
         }
-        out[n] = (uint8_t)b;
+        if (n >= lo && n < hi) out[n - lo] = (uint8_t)b;
       }
       carry += tot;
       __syncthreads();
@@ -318,7 +320,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
     const int n = tid + k * nt;
-    if (n < N) out[n] = (uint8_t)(bmin + slots_ge(E[k], beta + 1, bmin, L) + sm.extra[n]);
+    if (n < N && n >= lo && n < hi) out[n - lo] = (uint8_t)(bmin + slots_ge(E[k], beta + 1, bmin, L) + sm.extra[n]);
   }
 }
 

@@ -318,12 +318,12 @@ __global__ void __launch_bounds__(1024) k_alloc(const double* c, int N, int need
                                      bits + (size_t)blockIdx.x * N, sm);
 }
 
-template <int DK, int DV, bool COMPACT, bool C8, int PAIRS = 1, int PARTS = 1>
+template <int DK, int DV, bool COMPACT, bool C8, int PAIRS = 1, int PARTS = 1, bool ALLOC = false>
 __global__ void __launch_bounds__(requant_threads(DK, DV, PAIRS, PARTS))
     __attribute__((amdgpu_waves_per_eu(4))) k_requant(KParams p) {
   __shared__ RequantLds<DK, DV, COMPACT, CodeTile<C8>> sm;
-  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS, PARTS>(p, blockIdx.x / PARTS, sm,
-                                                            blockIdx.x % PARTS);
+  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS, PARTS, ALLOC>(p, blockIdx.x / PARTS, sm,
+                                                                   blockIdx.x % PARTS);
 }
 
 // Buffer resource over n bytes at base (word 3 of a gfx9 resource: untyped
@@ -981,6 +981,15 @@ static hipError_t launch_chunk_requant(const KParams& p, hipStream_t st) {
 }
 
 hipError_t launch_chunk_writeback(const KParams& p, int nsl, hipStream_t st, bool keys) {
+  if (keys && p.dk == 128) {
+    // the weights are ready: each requantisation block selects its unit's
+    // widths itself (one launch per interval fewer)
+    constexpr int FL = 4, PT = 2, T128 = requant_threads(128, 128, FL, PT);
+    const int nblk = p.B * p.H * PT;
+    return p.bmax <= 8
+               ? launch("requant", k_requant<128, 128, false, true, FL, PT, true>, nblk, T128, 0, st, p)
+               : launch("requant", k_requant<128, 128, false, false, FL, PT, true>, nblk, T128, 0, st, p);
+  }
   const hipError_t e = launch_chunk_alloc(p, nsl, st, keys);
   return e != hipSuccess ? e : launch_chunk_requant(p, st);
 }

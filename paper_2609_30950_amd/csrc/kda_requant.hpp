@@ -10,6 +10,7 @@
 
 #include <type_traits>
 
+#include "kda_alloc.hpp"
 #include "kda_device.hpp"
 #include "kda_kernels.hpp"
 #include "kda_record.hpp"
@@ -478,6 +479,12 @@ struct RequantLds {
   uint32_t tail[DV];
 };
 
+// Threads of a requantisation block: 2 d_k, or one per (row, segment,
+// candidate lane) of its dk / parts rows when that is more.
+constexpr int requant_threads(int dk, int dv, int pairs, int parts = 1) {
+  return 2 * dk > (dk / parts) * (dv / SEG) * pairs ? 2 * dk : (dk / parts) * (dv / SEG) * pairs;
+}
+
 // Quantise the state after the write-back interval with the allocated widths
 // and pack it into the record in place (PAIRS: candidates per fit step, see
 // fit_rows).  COMPACT (a decode step): the state is
@@ -487,7 +494,12 @@ struct RequantLds {
 // same float32 state.  Otherwise the stats pass left the float32 state itself,
 // and PARTS blocks may share the head: block `part` fits and packs rows
 // [part DK / PARTS, (part + 1) DK / PARTS).  All threads of the block call it.
-template <int DK, int DV, bool COMPACT, typename CT, int PAIRS = 1, int PARTS = 1>
+//
+// ALLOC (prefill with the allocation weights in ws_c): the block first selects
+// the widths of its scope unit itself (every block of the unit the same, by
+// the same exact selection) and keeps those of its head, instead of reading
+// the widths of a separate allocation launch.
+template <int DK, int DV, bool COMPACT, typename CT, int PAIRS = 1, int PARTS = 1, bool ALLOC = false>
 __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLds<DK, DV, COMPACT, CT>& sm,
                                              int part = 0) {
   static_assert(!COMPACT || PARTS == 1, "the decode step rebuilds whole heads");
@@ -497,8 +509,19 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
   const int t = threadIdx.x;
   const unsigned ntok = *(const unsigned*)rec;
+  if constexpr (ALLOC) {
+    static_assert(!COMPACT && sizeof(AllocSmem) <= sizeof(sm.Ct), "allocator scratch in the code tile");
+    // scope unit: the sequence (its heads' rows in order) or the head
+    const int N = p.scope == 0 ? p.H * DK : DK;
+    const int unit = p.scope == 0 ? bh / p.H : bh;
+    const int row0 = p.scope == 0 ? (bh % p.H) * DK : 0;   // this head's first row in the unit
+    constexpr int RPT = ALLOC_MAX_N / requant_threads(DK, DV, PAIRS, PARTS);
+    block_allocate<RPT>([&](int n) { return p.ws_c[(size_t)unit * N + n]; }, N, p.need, p.bmin, p.bmax,
+                        sm.nb, *(AllocSmem*)sm.Ct, row0, row0 + DK);
+    __syncthreads();   // the head's widths are in nb; the tile is free again
+  }
   if (t < DK) {
-    sm.nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
+    if constexpr (!ALLOC) sm.nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
     const uint32_t zr = p.ws_zr[(size_t)bh * DK + t];
     sm.zz[t] = (uint16_t)(zr & 0xffffu);
     sm.rr[t] = (uint16_t)(zr >> 16);
@@ -568,11 +591,6 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
 template <bool C8>
 using CodeTile = typename std::conditional<C8, int8_t, int16_t>::type;
 
-// Threads of a requantisation block: 2 d_k, or one per (row, segment,
-// candidate lane) of its dk / parts rows when that is more.
-constexpr int requant_threads(int dk, int dv, int pairs, int parts = 1) {
-  return 2 * dk > (dk / parts) * (dv / SEG) * pairs ? 2 * dk : (dk / parts) * (dv / SEG) * pairs;
-}
 
 // Block (head, part) = blockIdx.x / PARTS, blockIdx.x % PARTS.
 }  // namespace kda

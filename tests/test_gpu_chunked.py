@@ -149,6 +149,17 @@ def test_chunk_per_head_decay_head_scope():
     _one_interval(w, st0, W.tokens(w, 24, 24 + 40), oc, kc, "chunk per-head decay")
 
 
+def test_chunk_d128_head_scope_two_groups_per_head():
+    """d = 128 with groups of 64 rows (two per head) and the per-head budget:
+    the apply blocks form both groups' weights and each requantisation block
+    selects its own head's widths."""
+    w = W.sized(W.WORKLOADS["prefill"], B=2, H=3, G=64)
+    kc, oc = _cfgs(w, scope=1)
+    warm = W.tokens(w, 0, 16)
+    st0, _ = step.warm_state(warm["q"], warm["k"], warm["v"], warm["s"], warm["beta"], oc)
+    _one_interval(w, st0, W.tokens(w, 16, 16 + 45), oc, kc, "chunk d=128 head scope G=64")
+
+
 def test_chunk_no_erase_d128():
     w = W.sized(W.WORKLOADS["mamba2"], B=1, H=12, T=64, bf16=True)
     kc, oc = _cfgs(w, no_erase=True)

@@ -706,7 +706,10 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
     if (j < n) {
       float* orow = p.o + (((size_t)b * p.T + p.tok0 + j) * p.H + h) * p.dv + SLICE * sl;
 #pragma unroll
-      for (int ct = 0; ct < 4; ++ct) orow[16 * ct + l16] = ao[ct][r];
+      // outputs and state are read by other kernels only: nontemporal
+      // stores keep them from filling the L2 that the next kernel's
+      // start must write back
+      for (int ct = 0; ct < 4; ++ct) __builtin_nontemporal_store(ao[ct][r], &orow[16 * ct + l16]);
     }
   }
 
@@ -734,7 +737,7 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
         const float x = acc[rt][ct][r];
-        srow[16 * ct + l16] = x;
+        __builtin_nontemporal_store(x, &srow[16 * ct + l16]);
         m = fmaxf(m, fabsf(x));
       }
       m = max16(m);

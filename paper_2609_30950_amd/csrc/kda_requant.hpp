@@ -354,7 +354,7 @@ __device__ __forceinline__ void pack_cols(const CT* Ct, const uint8_t* bits, con
     uint32_t* dst = words + (size_t)wi * DV + col;
     const int b0 = own_lo - 32 * wi, b1 = own_hi - 32 * wi;
     if (b0 <= 0 && b1 >= 32) {
-      *dst = v;
+      __builtin_nontemporal_store(v, dst);   // read again only by a later step
     } else {
       const uint32_t m = (b1 >= 32 ? ~0u : (1u << b1) - 1u) & (b0 <= 0 ? ~0u : ~((1u << b0) - 1u));
       atomicAnd(dst, ~m);

@@ -50,7 +50,7 @@ def per_kernel(d, counter):
 
 
 def short(name):
-    for k in ("k_chunk_prep", "k_chunk_apply"):
+    for k in ("k_chunk_prep", "k_chunk_apply", "k_chunk_rates"):
         if "kda::" + k in name:
             return k[8:]
     for k in ("k_requant", "k_chunk", "k_alloc", "k_step32", "k_pack", "k_unpack"):

@@ -956,20 +956,19 @@ struct AuxFork {
 // compute unit: its LDS and registers).
 constexpr int PREP_SIDE_GRID = 128;
 
-// Chunks per group.  With a side stream the groups grow from one chunk
-// (1, 1, 2, 3, 5, 8, ... up to gc), so that the first interval starts after
-// one chunk's preparation and each later group's preparation (beside the
-// intervals) takes about as long as the previous group's intervals; without
-// one, groups of gc chunks.  Once a size reaches gc every later one is gc.
+// Chunks per group.  With a side stream the groups grow from one chunk by
+// about a quarter per group (floor(1.25^g): 1, 1, 1, 1, 2, 3, 3, 4, 5, 7, 9,
+// ... up to gc), so that the first interval starts after one chunk's
+// preparation and each later group's preparation (a chunk's takes about
+// four fifths of an interval beside them) keeps pace with the previous
+// group's intervals; without one, groups of gc chunks.  Once a size reaches
+// gc every later one is gc.
 static int group_size(int g, int gc, bool grow) {
   if (!grow) return gc;
-  int a = 1, b = 1;
-  for (int j = 0; j < g && a < gc; ++j) {
-    const int n = a + b;
-    a = b;
-    b = n;
-  }
-  return a < gc ? a : gc;
+  double a = 1.0;
+  for (int j = 0; j < g && a < gc; ++j) a *= 1.25;
+  const int n = (int)a;
+  return n < gc ? n : gc;
 }
 static int group_first(int g, int gc, bool grow) {
   int c0 = 0;
@@ -1027,6 +1026,29 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
     return (const uint8_t*)(buf(g) + (size_t)(k - first(g)) * nbh * ChunkWs<DK>::bytes);
   };
   auto tokens = [&](int k) { return (p.T - k * C) < C ? (p.T - k * C) : C; };
+  // A group prepared beside the intervals is enqueued a few launches at a
+  // time, spread over the previous group's intervals: a queue holding many
+  // launches of whole-compute-unit blocks held up the intervals' launches on
+  // the main stream.  Its rates and its ready event follow its last launch.
+  int pend_g = -1, pend_u0 = 0, pend_per = 1;
+  auto feed = [&](int launches) -> hipError_t {
+    if (pend_g < 0) return hipSuccess;
+    KParams q = p;
+    q.tok0 = first(pend_g) * C;
+    const int units = nbh * count(pend_g);
+    for (int i = 0; i < launches && pend_u0 < units; ++i, pend_u0 += PREP_SIDE_GRID) {
+      const hipError_t e = launch("prep", k_chunk_prep<DK>,
+                                  units - pend_u0 < PREP_SIDE_GRID ? units - pend_u0 : PREP_SIDE_GRID, NTP, 0,
+                                  fk.aux, q, C, buf(pend_g), pend_u0);
+      if (e != hipSuccess) return e;
+    }
+    if (pend_u0 < units) return hipSuccess;
+    hipError_t e = launch("rates", k_chunk_rates<DK>, (nbh * DK + 255) / 256, 256, 0, fk.aux, p, C,
+                          buf(pend_g), first(pend_g), count(pend_g), (uint32_t*)p.ws_hv);
+    if (e == hipSuccess) e = hipEventRecord(fk.ev[1 + (pend_g & 1)], fk.aux);
+    pend_g = -1;
+    return e;
+  };
   hipError_t e = prep(0, st, false);
   if (e != hipSuccess) return e;
   if (two && ngr > 1) {
@@ -1040,6 +1062,7 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
     const int g = group_of(k);
     if (k > 0 && k == first(g)) {
       if (two) {
+        if (pend_g == g && (e = feed(0x7fffffff)) != hipSuccess) return e;   // all of it enqueued
         if ((e = hipStreamWaitEvent(st, fk.ev[1 + (g & 1)], 0)) != hipSuccess) return e;
       } else if ((e = prep(g, st, false)) != hipSuccess) {
         return e;
@@ -1052,12 +1075,16 @@ static hipError_t run_chunked(KParams p, int C, hipStream_t st, hipStream_t aux_
     if (e != hipSuccess) return e;
     if (two && k == first(g) + count(g) - 1 && g + 2 < ngr) {
       // chunk k's apply is the last read of group g's records: group g + 2
-      // reuses them
+      // reuses them, prepared during group g + 1's intervals
+      if ((e = feed(0x7fffffff)) != hipSuccess) return e;   // group g + 1 complete first
       if ((e = fk.fork()) != hipSuccess) return e;
-      if ((e = prep(g + 2, fk.aux, true)) != hipSuccess) return e;
-      if ((e = hipEventRecord(fk.ev[1 + (g & 1)], fk.aux)) != hipSuccess) return e;
+      pend_g = g + 2;
+      pend_u0 = 0;
+      const int launches = (nbh * count(g + 2) + PREP_SIDE_GRID - 1) / PREP_SIDE_GRID;
+      pend_per = (launches + count(g + 1) - 1) / count(g + 1);
     }
     if ((e = launch_chunk_writeback(p, nsl, st, keys)) != hipSuccess) return e;
+    if (two && (e = feed(pend_per)) != hipSuccess) return e;
   }
   return hipSuccess;   // fk joins aux into st
 }

@@ -60,6 +60,7 @@ constexpr float SPLIT_SPAN = 80.f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // 16-byte copies held in registers
 
 // float -> bf16 bits, round to nearest even (finite inputs)
 __device__ __forceinline__ uint16_t bf16_rne(float x) {
@@ -561,9 +562,8 @@ struct ApplyFrags {
 };
 
 // Wave w (of the four of a slice) of slice sl; `in` is the head's chunk record.
-// PART 1: the operands of the first products (Wk, Qhat, gamma), PART 2: the
-// later ones (Uv, A, Ktil^T), 3: all.
-template <int DK, int PART = 3>
+// The first products' operands (Wk, Qhat, gamma) are requested first.
+template <int DK>
 __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, int sl, int w,
                                            ApplyFrags<DK>& f) {
   using CW = ChunkWs<DK>;
@@ -576,43 +576,35 @@ __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, 
   const uint16_t* ktt = (const uint16_t*)(in + CW::ktt);
   const float* uv = (const float*)(in + CW::uv);
   const float* gend = (const float*)(in + CW::gend);
-  const bool erase = !p.no_erase;
   constexpr int PL = CT * DK;            // elements of one plane
 #pragma unroll
+  for (int hl = 0; hl < 2; ++hl)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      f.fw[hl][ks] = *(const uint4*)&wk[hl * PL + jrow * DK + 32 * ks + k8];   // used if erase
+      f.fq[hl][ks] = *(const uint4*)&qh[hl * PL + jrow * DK + 32 * ks + k8];
+    }
+#pragma unroll
   for (int hl = 0; hl < 2; ++hl) {
-    if constexpr ((PART & 1) != 0) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        f.fw[hl][ks] = erase ? *(const uint4*)&wk[hl * PL + jrow * DK + 32 * ks + k8]
-                             : make_uint4(0u, 0u, 0u, 0u);
-        f.fq[hl][ks] = *(const uint4*)&qh[hl * PL + jrow * DK + 32 * ks + k8];
-      }
-    }
-    if constexpr ((PART & 2) != 0) {
-#pragma unroll
-      for (int ks = 0; ks < CT / 32; ++ks)
-        f.fa[hl][ks] = 32 * ks <= 16 * w + 15 ? *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8]
-                                              : make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int ks = 0; ks < CT / 32; ++ks)
-          f.fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
-    }
-  }
-  if constexpr ((PART & 1) != 0) {
+    for (int ks = 0; ks < CT / 32; ++ks)
+      f.fa[hl][ks] = *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8];   // used up to
+                                                                                  // the tile's last token
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) f.fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+      for (int ks = 0; ks < CT / 32; ++ks)
+        f.fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
   }
-  if constexpr ((PART & 2) != 0) {
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        f.fu[ct][r] = uv[(16 * w + 4 * (lane >> 4) + r) * DK + SLICE * sl + 16 * ct + l16];
-  }
+    for (int r = 0; r < 4; ++r) f.fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      f.fu[ct][r] = uv[(16 * w + 4 * (lane >> 4) + r) * DK + SLICE * sl + 16 * ct + l16];
 }
 
 // One write-back interval of one 64-column slice of one head, tokens
@@ -637,9 +629,9 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
   const int k8 = 8 * (lane >> 4), l16 = lane & 15;
   const bool erase = !p.no_erase;
 
-  // S0 at this lane's state-tile positions: float32 gamma_{n-1} * S0 as the
-  // accumulator of S_n, S0^T in LDS as hi and lo planes for the products
-  f32x4 acc[RT][4];
+  // S0^T in LDS as hi and lo planes for the products (this lane's state-tile
+  // positions; the accumulator of S_n is formed from S0 again further down,
+  // so that it is not held through the first products)
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
@@ -649,7 +641,6 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
       for (int ct = 0; ct < 4; ++ct) {
         const int c = 16 * ct + l16;
         const float x = s0(i, c);
-        acc[rt][ct][r] = f.fg[rt][r] * x;
         const uint16_t xh = bf16_rne(x);
         sm.s0t[0][c][i] = xh;
         sm.s0t[1][c][i] = bf16_lo(x, xh);
@@ -713,7 +704,16 @@ __device__ __forceinline__ void apply_slice(const KParams& p, const uint8_t* in,
     }
   }
 
-  // S_n += Ktil^T U
+  // S_n = gamma_{n-1} * S0 + Ktil^T U (float32 gamma_{n-1} * S0 at this
+  // lane's state-tile positions as the accumulator)
+  f32x4 acc[RT][4];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+        acc[rt][ct][r] = f.fg[rt][r] * s0(16 * (RT * w + rt) + 4 * (lane >> 4) + r, 16 * ct + l16);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
@@ -774,19 +774,28 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
 
-  // the chunk record's operands of this wave, loaded before the state's
-  // record so that both round trips overlap
-  ApplyFrags<DK> f;
-  load_frags<DK, 1>(p, in, sl, w, f);
-  {
-    // the slice's code words: word kw of column sl*64 + c at words[kw*64 + c]
-    const uint4* src = (const uint4*)(rec + L.codes_off);
-    constexpr int Q = SLICE / 4;
-    const int n4 = L.wc * Q;
-    for (int e = t; e < n4; e += NT) ((uint4*)words)[e] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
+  // The state record's metadata and the slice's code words are requested
+  // first and every operand of the products after them (loads complete in
+  // order: the dequantisation waits for the record only).  Code words: word
+  // kw of column sl*64 + c at words[kw*64 + c]; at most d_k MAX_B / 32 words
+  // per column.
+  const MetaFetch mf = meta_fetch<DK>(rec, L);
+  constexpr int Q = SLICE / 4, WMAX = ((DK * MAX_B / 32) * Q + NT - 1) / NT;
+  const u32x4* src = (const u32x4*)(rec + L.codes_off);
+  const int n4 = L.wc * Q;
+  u32x4 wv[WMAX];
+#pragma unroll
+  for (int q = 0; q < WMAX; ++q) {
+    // indices past the last word read and store the last word again (the
+    // same value as its owner): no branch, so the loads stay up here
+    const int e = min(t + q * NT, n4 - 1);
+    wv[q] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
   }
-  load_meta<DK, SLICE>(rec, L, p.bmax, meta);   // its barrier covers the staging
-  load_frags<DK, 2>(p, in, sl, w, f);           // the later products' operands
+  ApplyFrags<DK> f;
+  load_frags<DK>(p, in, sl, w, f);
+#pragma unroll
+  for (int q = 0; q < WMAX; ++q) ((u32x4*)words)[min(t + q * NT, n4 - 1)] = wv[q];
+  meta_form<DK, SLICE>(mf, p.bmax, meta);   // its barrier covers the staging
   auto s0 = [&](int i, int c) {
     const uint4 d = meta.desc[i];
     const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);
@@ -820,16 +829,25 @@ __global__ void __launch_bounds__((DK / SLICE) * NT) __attribute__((amdgpu_waves
   extern __shared__ uint4 dyn_lds[];
   uint32_t* words = (uint32_t*)dyn_lds;
 
+  // The state record's metadata and code words are requested first and every
+  // operand of the products after them: loads complete in order, so the
+  // dequantisation below waits for the record only, with the operands still
+  // in flight.  Code words: word kw of column j at words[kw d_v + j]; at most
+  // d_k MAX_B / 32 words per column (wc <= that for every width bound).
+  const MetaFetch mf = meta_fetch<DK>(rec, L);
+  constexpr int NTH = NSL * NT, WMAX = ((DK * MAX_B / 32) * (DK / 4) + NTH - 1) / NTH;
+  const u32x4* src = (const u32x4*)(rec + L.codes_off);
+  const int n4 = L.wc * (DK / 4);
+  u32x4 wv[WMAX];
+#pragma unroll
+  for (int q = 0; q < WMAX; ++q)
+    wv[q] = src[min(t + q * NTH, n4 - 1)];   // past the end: the last word again, stored
+                                              // where its owner stores it (no branch)
   ApplyFrags<DK> f;
-  load_frags<DK, 1>(p, in, sl, w, f);
-  {
-    // the head's code words as stored: word kw of column j at words[kw d_v + j]
-    const uint4* src = (const uint4*)(rec + L.codes_off);
-    const int n4 = L.wc * (DK / 4);
-    for (int e = t; e < n4; e += NSL * NT) ((uint4*)words)[e] = src[e];
-  }
-  load_meta<DK, DK>(rec, L, p.bmax, meta);   // its barrier covers the staging
-  load_frags<DK, 2>(p, in, sl, w, f);         // the later products' operands
+  load_frags<DK>(p, in, sl, w, f);
+#pragma unroll
+  for (int q = 0; q < WMAX; ++q) ((u32x4*)words)[min(t + q * NTH, n4 - 1)] = wv[q];
+  meta_form<DK, DK>(mf, p.bmax, meta);   // its barrier covers the staging
   auto s0 = [&](int i, int c) {
     const uint4 d = meta.desc[i];
     const int sh = (int)(d.y & 31u), bw = (int)(d.y >> 8);

@@ -41,29 +41,50 @@ struct MetaSmem {
   uint4 desc[DK];
   uint8_t w[DK];      // widths of the stored record
   int P[DK + 1];      // prefix sums of widths (row bit offsets)
-  float sc[DK];       // stored scales (FP16 -> float)
+  uint16_t sc[DK];    // stored scales (FP16 bits)
   uint16_t z[DK];     // stored rate codes
   uint16_t r16[DK];   // stored erase rates
   unsigned ntok;
 };
 
-// Load widths/scales/stat codes of a record and form the row offsets.
-// Widths above b_max (never written by this library) are clamped so that a
-// damaged record cannot address code words outside its slot.
+// A record's stored metadata as one thread reads it (thread t < d_k: row t's
+// scale and codes; t < d_k / 2: the byte of rows 2t and 2t + 1; thread 0: the
+// token count), held in registers until meta_form writes it out.
+struct MetaFetch {
+  uint32_t wb, sc, z, r, ntok;
+};
+
+template <int DK>
+__device__ __forceinline__ MetaFetch meta_fetch(const uint8_t* rec, const Layout& L) {
+  const int tid = threadIdx.x;
+  MetaFetch f{0u, 0u, 0u, 0u, 0u};
+  if (tid < DK / 2) f.wb = rec[L.w_off + tid];
+  if (tid < DK) {
+    f.sc = ((const uint16_t*)(rec + L.sc_off))[tid];
+    f.z = ((const uint16_t*)(rec + L.z_off))[tid];
+    f.r = ((const uint16_t*)(rec + L.r_off))[tid];
+  }
+  if (tid == 0) f.ntok = *(const unsigned*)rec;
+  return f;
+}
+
+// Widths/scales/stat codes of a record and its row offsets and decode
+// descriptors, from what meta_fetch read.  Widths above b_max (never written
+// by this library) are clamped so that a damaged record cannot address code
+// words outside its slot.
 template <int DK, int DV>
-__device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
+__device__ __forceinline__ void meta_form(const MetaFetch& f, int bmax, MetaSmem<DK>& m) {
   const int tid = threadIdx.x;
   if (tid < DK / 2) {
-    const uint8_t byte = rec[L.w_off + tid];
-    m.w[2 * tid] = (uint8_t)min((byte & 15) + 1, bmax);
-    m.w[2 * tid + 1] = (uint8_t)min((byte >> 4) + 1, bmax);
+    m.w[2 * tid] = (uint8_t)min((int)(f.wb & 15u) + 1, bmax);
+    m.w[2 * tid + 1] = (uint8_t)min((int)(f.wb >> 4) + 1, bmax);
   }
   if (tid < DK) {
-    m.sc[tid] = f16_to_f32(((const uint16_t*)(rec + L.sc_off))[tid]);
-    m.z[tid] = ((const uint16_t*)(rec + L.z_off))[tid];
-    m.r16[tid] = ((const uint16_t*)(rec + L.r_off))[tid];
+    m.sc[tid] = (uint16_t)f.sc;
+    m.z[tid] = (uint16_t)f.z;
+    m.r16[tid] = (uint16_t)f.r;
   }
-  if (tid == 0) m.ntok = *(const unsigned*)rec;
+  if (tid == 0) m.ntok = f.ntok;
   __syncthreads();
   if (tid < WAVE) {
     constexpr int PER = (DK + WAVE - 1) / WAVE;
@@ -83,7 +104,7 @@ __device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, i
         m.P[i] = run;
         // x^ = (code + add) mul: (Delta, 0) for b >= 2, (2 mu, 1/2) for one bit
         const int b = loc[q];
-        const float sc = m.sc[i];
+        const float sc = f16_to_f32(m.sc[i]);
         const float mul = b == 1 ? 2.0f * sc : sc;
         const float add = b == 1 ? 0.5f : 0.0f;
         m.desc[i] = make_uint4((uint32_t)((run >> 5) * DV), (uint32_t)((run & 31) | (b << 8)),
@@ -94,6 +115,12 @@ __device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, i
     if (tid == WAVE - 1) m.P[DK] = incl;
   }
   __syncthreads();
+}
+
+// Load a record's metadata and form the row offsets (both steps at once).
+template <int DK, int DV>
+__device__ __forceinline__ void load_meta(const uint8_t* rec, const Layout& L, int bmax, MetaSmem<DK>& m) {
+  meta_form<DK, DV>(meta_fetch<DK>(rec, L), bmax, m);
 }
 
 template <bool BF16>

@@ -509,6 +509,25 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
   uint8_t* rec = (uint8_t*)slot_ptr(p.records, L.slot, bh);
   const int t = threadIdx.x;
   const unsigned ntok = *(const unsigned*)rec;
+  // The float32 rows of this block's part (not the decode step: it rebuilds
+  // its rows), when they fit in LDS: requested first, so that their latency
+  // passes during the allocation and the width order, and read by the fit
+  // from LDS.  Row r at sx[r SROW], segment g of it SEG + 4 floats further
+  // per segment (the rows and segments of a wave's items fall in different
+  // banks).
+  constexpr int SROW = DV + 4 * (DV / SEG), NTH = requant_threads(DK, DV, PAIRS, PARTS);
+  constexpr bool STAGE = !COMPACT && (size_t)ROWS * SROW * 4 <= 40 * 1024;
+  constexpr int NV = STAGE ? ROWS * DV / 4 / NTH : 1;
+  static_assert(!STAGE || (ROWS * DV / 4) % NTH == 0, "whole float4 per thread");
+  typedef float v4f __attribute__((ext_vector_type(4)));   // held in registers, not copied through memory
+  __shared__ __align__(16) float sx[STAGE ? ROWS * SROW : 4];
+  v4f sv[NV];
+  if constexpr (STAGE) {
+    const v4f* S4 = (const v4f*)(p.ws_s32 + ((size_t)bh * DK + r0) * DV);
+#pragma unroll
+    for (int q = 0; q < NV; ++q) sv[q] = S4[t + q * NTH];
+  }
+  const uint32_t zr = t < DK ? p.ws_zr[(size_t)bh * DK + t] : 0u;
   if constexpr (ALLOC) {
     static_assert(!COMPACT && sizeof(AllocSmem) <= sizeof(sm.Ct), "allocator scratch in the code tile");
     // scope unit: the sequence (its heads' rows in order) or the head
@@ -522,9 +541,15 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
   }
   if (t < DK) {
     if constexpr (!ALLOC) sm.nb[t] = (uint8_t)min(max((int)p.ws_bits[(size_t)bh * DK + t], 1), p.bmax);
-    const uint32_t zr = p.ws_zr[(size_t)bh * DK + t];
     sm.zz[t] = (uint16_t)(zr & 0xffffu);
     sm.rr[t] = (uint16_t)(zr >> 16);
+  }
+  if constexpr (STAGE) {
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int e = 4 * (t + q * NTH), r = e / DV, c = e % DV;
+      *(v4f*)&sx[r * SROW + c + 4 * (c / SEG)] = sv[q];
+    }
   }
   for (int e = t; e < (MAX_B + 1) * N_FIT; e += blockDim.x)
     sm.phi[e / N_FIT][e % N_FIT] = p.phi[e / N_FIT][e % N_FIT];
@@ -578,9 +603,23 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
     __syncthreads();
     width_order<DK>(sm.nb, sm.perm, sm.os, r0, r0 + ROWS);
     const float* S = p.ws_s32 + (size_t)bh * DK * DV;
-    fit_rows<DK, DV, false, PAIRS, ROWS>(
-        [&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(S, i, sg, x); }, sm.nb, sm.perm,
-        sm.phi, sm.Ct, sm.sc16, p.diag_fit);
+    auto staged = [&](int i, int sg, float (&x)[SEG]) {
+      const int li = min(max(i - r0, 0), ROWS - 1);
+      const float4* src = (const float4*)&sx[li * SROW + sg * (SEG + 4)];
+#pragma unroll
+      for (int q = 0; q < SEG / 4; ++q) {
+        const float4 v = src[q];
+        x[4 * q] = v.x;
+        x[4 * q + 1] = v.y;
+        x[4 * q + 2] = v.z;
+        x[4 * q + 3] = v.w;
+      }
+    };
+    auto dense = [&](int i, int sg, float (&x)[SEG]) { load_dense<DV>(S, i, sg, x); };
+    if constexpr (STAGE)
+      fit_rows<DK, DV, false, PAIRS, ROWS>(staged, sm.nb, sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
+    else
+      fit_rows<DK, DV, false, PAIRS, ROWS>(dense, sm.nb, sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
   }
   __syncthreads();
   pack_cols<DK, DV, ROWS>(sm.Ct, sm.nb, sm.os.P, (uint32_t*)(rec + L.codes_off), sm.tail, r0);

@@ -562,7 +562,7 @@ struct ApplyFrags {
 };
 
 // Wave w (of the four of a slice) of slice sl; `in` is the head's chunk record.
-// The first products' operands (Wk, Qhat, gamma) are requested first.
+// Requested in the order the products use them (loads complete in order).
 template <int DK>
 __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, int sl, int w,
                                            ApplyFrags<DK>& f) {
@@ -577,6 +577,7 @@ __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, 
   const float* uv = (const float*)(in + CW::uv);
   const float* gend = (const float*)(in + CW::gend);
   constexpr int PL = CT * DK;            // elements of one plane
+  // W = Wk S0 and O = Qhat S0
 #pragma unroll
   for (int hl = 0; hl < 2; ++hl)
 #pragma unroll
@@ -584,27 +585,30 @@ __device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, 
       f.fw[hl][ks] = *(const uint4*)&wk[hl * PL + jrow * DK + 32 * ks + k8];   // used if erase
       f.fq[hl][ks] = *(const uint4*)&qh[hl * PL + jrow * DK + 32 * ks + k8];
     }
-#pragma unroll
-  for (int hl = 0; hl < 2; ++hl) {
-#pragma unroll
-    for (int ks = 0; ks < CT / 32; ++ks)
-      f.fa[hl][ks] = *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8];   // used up to
-                                                                                  // the tile's last token
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int ks = 0; ks < CT / 32; ++ks)
-        f.fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
-  }
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) f.fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+  // U = Uv - W
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       f.fu[ct][r] = uv[(16 * w + 4 * (lane >> 4) + r) * DK + SLICE * sl + 16 * ct + l16];
+  // O += A U (blocks used up to the tile's last token)
+#pragma unroll
+  for (int hl = 0; hl < 2; ++hl)
+#pragma unroll
+    for (int ks = 0; ks < CT / 32; ++ks)
+      f.fa[hl][ks] = *(const uint4*)&am[hl * CT * CT + jrow * CT + 32 * ks + k8];
+  // S = gamma S0 + Ktil^T U
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) f.fg[rt][r] = gend[16 * (RT * w + rt) + 4 * (lane >> 4) + r];
+#pragma unroll
+  for (int hl = 0; hl < 2; ++hl)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < CT / 32; ++ks)
+        f.fk[hl][rt][ks] = *(const uint4*)&ktt[hl * PL + (16 * (RT * w + rt) + l16) * CT + 32 * ks + k8];
 }
 
 // One write-back interval of one 64-column slice of one head, tokens

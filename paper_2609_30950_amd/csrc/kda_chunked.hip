@@ -73,10 +73,6 @@ __device__ __forceinline__ float bf16_f32(uint16_t h) {
   return __builtin_bit_cast(float, (uint32_t)h << 16);
 }
 
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  return (uint32_t)bf16_rne(a) | ((uint32_t)bf16_rne(b) << 16);
-}
-
 // x = hi + lo with hi = bf16(x) and lo = bf16(x - hi) (x - hi is exact in
 // float32): the pair holds x to a relative 2^-18.
 __device__ __forceinline__ uint16_t bf16_lo(float x, uint16_t hi) { return bf16_rne(x - bf16_f32(hi)); }
@@ -564,8 +560,7 @@ struct ApplyFrags {
 // Wave w (of the four of a slice) of slice sl; `in` is the head's chunk record.
 // Requested in the order the products use them (loads complete in order).
 template <int DK>
-__device__ __forceinline__ void load_frags(const KParams& p, const uint8_t* in, int sl, int w,
-                                           ApplyFrags<DK>& f) {
+__device__ __forceinline__ void load_frags(const uint8_t* in, int sl, int w, ApplyFrags<DK>& f) {
   using CW = ChunkWs<DK>;
   constexpr int RT = ApplyFrags<DK>::RT, KS = ApplyFrags<DK>::KS;
   const int lane = lane_id(), k8 = 8 * (lane >> 4), l16 = lane & 15;
@@ -796,7 +791,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
     wv[q] = src[(size_t)(e / Q) * (p.dv / 4) + sl * Q + e % Q];
   }
   ApplyFrags<DK> f;
-  load_frags<DK>(p, in, sl, w, f);
+  load_frags<DK>(in, sl, w, f);
 #pragma unroll
   for (int q = 0; q < WMAX; ++q) ((u32x4*)words)[min(t + q * NT, n4 - 1)] = wv[q];
   meta_form<DK, SLICE>(mf, p.bmax, meta);   // its barrier covers the staging
@@ -848,7 +843,7 @@ __global__ void __launch_bounds__((DK / SLICE) * NT) __attribute__((amdgpu_waves
     wv[q] = src[min(t + q * NTH, n4 - 1)];   // past the end: the last word again, stored
                                               // where its owner stores it (no branch)
   ApplyFrags<DK> f;
-  load_frags<DK>(p, in, sl, w, f);
+  load_frags<DK>(in, sl, w, f);
 #pragma unroll
   for (int q = 0; q < WMAX; ++q) ((u32x4*)words)[min(t + q * NTH, n4 - 1)] = wv[q];
   meta_form<DK, DK>(mf, p.bmax, meta);   // its barrier covers the staging

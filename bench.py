@@ -307,6 +307,15 @@ def run_prefill(args, K, torch):
             "apply": dict(tflops=fa * nbh / t_apply / 1e12,
                           frac=fa * nbh / t_apply / 1e12 / MFMA_BF16_PEAK_TFLOPS),
             "peak_tflops": MFMA_BF16_PEAK_TFLOPS}
+        # the same two kernels against HBM: prep reads a chunk's inputs and
+        # writes its record (less the Gamma and rate codes the rate chain adds)
+        prep_bytes = (3 * w.C * w.dk * 2 + w.C * w.dk * 4 + w.C * 4
+                      + CHUNK_RECORD_BYTES - w.dk * 12 + 4 * w.dk * 8)
+        pg = prep_bytes * chunks_per_prep / t_prep / 1e9
+        out["hbm"] = {"apply": dict(GBps=ach, frac=ach / HBM_PEAK_GBPS, bytes_per_launch=nbh * per_head),
+                      "prep": dict(GBps=pg, frac=pg / HBM_PEAK_GBPS,
+                                   bytes_per_launch=prep_bytes * chunks_per_prep),
+                      "peak_GBps": HBM_PEAK_GBPS}
         out["metric"] = out["metric"].replace("prefill", "chunked prefill")
     elif t_stats:
         ach = rec_ops / t_stats / 1e12

@@ -7,15 +7,15 @@
 //
 // Slot keys are compared exactly as (E_i - 2 l, M_i) with c_i = M_i 2^E_i,
 // M_i in [0.5, 1) (frexp).  The selection runs in exact stages:
-//  1. bucket E - 2l: a histogram of the row exponents (wave ballots) gives the
+//  1. bucket E - 2l: a histogram of the row exponents (LDS atomics) gives the
 //     slot count of every bucket; the boundary bucket beta* is the highest one
 //     at which the running count from the top reaches `need`;
 //  2. rows owning a slot in beta* (at most one slot per row) are narrowed by
 //     radix passes over the 52 fraction bits (256-bin LDS histograms), each
 //     keeping the digit bin that contains the boundary, until at most one
 //     wave of candidates remains;
-//  3. one wave ranks those by (fraction desc, row asc) and grants the first
-//     ones.
+//  3. those are ranked by (fraction desc, row asc), one ballot per
+//     candidate, and the first ones granted.
 // Rows with c_i = 0 own slots below every positive one, granted in row order.
 #pragma once
 
@@ -290,7 +290,7 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     }
     cand = 0u;
   }
-  // stage 3: at most one wave of candidates left; rank them in wave 0
+  // stage 3: at most one wave of candidates left: rank them
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
     if (!((cand >> k) & 1u)) continue;
@@ -299,22 +299,20 @@ __device__ __forceinline__ void block_allocate(Load c_at, int N, int need, int b
     sm.cand_row[pos] = tid + k * nt;
   }
   __syncthreads();
-  if (tid < WAVE) {
-    // keys held one per lane, the others read across lanes (no LDS round
-    // trip per comparison)
-    const int nc = sm.cand_n;
-    const unsigned long long my = lane < nc ? sm.cand_key[lane] : 0ull;
-    const int myr = lane < nc ? sm.cand_row[lane] : 0;
-    const unsigned mlo = (unsigned)my, mhi = (unsigned)(my >> 32);
-    int rank = 0;
-    for (int j = 0; j < nc; ++j) {
-      const unsigned long long o =
-          ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)mhi, j) << 32) |
-          (unsigned)__builtin_amdgcn_readlane((int)mlo, j);
-      const int orow = __builtin_amdgcn_readlane(myr, j);
-      rank += (o > my) || (o == my && orow < myr);
+  {
+    // the candidates' ranks by (fraction desc, row asc), every wave taking
+    // some of them: candidate i's rank is the number of lanes j whose
+    // candidate comes first (one ballot per candidate)
+    const int nc = sm.cand_n, nw = nt / WAVE, wv = tid / WAVE;
+    const unsigned long long kj = lane < nc ? sm.cand_key[lane] : 0ull;
+    const int rj = lane < nc ? sm.cand_row[lane] : 0;
+    for (int i = wv; i < nc; i += nw) {
+      const unsigned long long ki = sm.cand_key[i];
+      const int ri = sm.cand_row[i];
+      const bool first = lane < nc && (kj > ki || (kj == ki && rj < ri));
+      const int rank = __popcll(__ballot(first));
+      if (lane == 0 && rank < rem) sm.extra[ri] = 1;
     }
-    if (lane < nc && rank < rem) sm.extra[myr] = 1;
   }
   __syncthreads();
 #pragma unroll

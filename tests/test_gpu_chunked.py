@@ -4,7 +4,7 @@ The chunked form evaluates the same recurrence (eq. rule) in another order:
 products on bf16 MFMA with float32 accumulation, each operand that is not
 exact in bf16 split into hi and lo bf16 parts (relative 2^-18) and multiplied
 as three products.  Its state and outputs are compared with the float64
-recurrence from the same starting record within the benchmark spec's 1e-3 of the
+recurrence from the same starting record within 1e-3 (the outputs' accuracy bound) of the
 head's largest |S| (state) or largest |o| (outputs), normwise; observed
 errors are printed.  Its write-back is compared bit for bit with the oracle's
 quantiser applied to the GPU's own float32 state (EMA statistics from the

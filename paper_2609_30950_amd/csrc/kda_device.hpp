@@ -73,11 +73,12 @@ __device__ __forceinline__ uint16_t f32_to_f16_sat(float x) {
 
 // FP16 bits of a non-negative float (scales R phi of the fit), round to
 // nearest even, saturating at 65504: the same value as f32_to_f16_sat for
-// x >= 0 with the saturation as one minimum before the conversion (values
-// from 65504 up round to 65504 either way; NaN is not an input).
+// x >= 0 with the saturation as one median of (x, 0, 65504) before the
+// conversion (values from 65504 up round to 65504 either way; NaN and -0 are
+// not inputs).
 __device__ __forceinline__ uint16_t f32_to_f16_sat_nonneg(float x) {
   asm volatile("" : "+v"(x));
-  return __builtin_bit_cast(uint16_t, (_Float16)fminf(x, 65504.0f));
+  return __builtin_bit_cast(uint16_t, (_Float16)__builtin_amdgcn_fmed3f(x, 0.0f, 65504.0f));
 }
 
 // fl32(1 / d) for d an FP16 value (positive, or 0 -> 0): the hardware

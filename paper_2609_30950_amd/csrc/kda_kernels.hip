@@ -322,8 +322,12 @@ template <int DK, int DV, bool COMPACT, bool C8, int PAIRS = 1, int PARTS = 1, b
 __global__ void __launch_bounds__(requant_threads(DK, DV, PAIRS, PARTS))
     __attribute__((amdgpu_waves_per_eu(4))) k_requant(KParams p) {
   __shared__ RequantLds<DK, DV, COMPACT, CodeTile<C8>> sm;
-  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS, PARTS, ALLOC>(p, blockIdx.x / PARTS, sm,
-                                                                   blockIdx.x % PARTS);
+  // the parts of a head run on the XCD of the kernels before and after it
+  // (one block per head or per column slice of a head, dealt the same way),
+  // so the float32 state it reads and the record it writes stay in one L2
+  int bh = blockIdx.x, part = 0;
+  if constexpr (PARTS > 1) slice_block(p.B * p.H, PARTS, bh, part);
+  requant_head<DK, DV, COMPACT, CodeTile<C8>, PAIRS, PARTS, ALLOC>(p, bh, sm, part);
 }
 
 // Buffer resource over n bytes at base (word 3 of a gfx9 resource: untyped
@@ -498,7 +502,8 @@ template <int DK, bool BF16>
 __global__ void __launch_bounds__(2 * DK) k_chunk_slices(KParams p) {
   constexpr int TS = pf_tokens<DK>();
   const int nsl = p.dv / SLICE;
-  const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
+  int bh, sl;
+  slice_block(p.B * p.H, nsl, bh, sl);   // a head's slices on one XCD
   const int t = threadIdx.x;
   const int b = bh / p.H, h = bh % p.H;
   const Layout L = p.L;
@@ -663,7 +668,8 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_cols(KParams p) {
   constexpr int NV = TS * SLICE / (2 * DK); // values of v staged per thread and batch
   static_assert(NRB * CPW == SLICE && CPW >= 16, "16-lane DPP rows inside a row block");
   const int nsl = p.dv / SLICE;
-  const int bh = blockIdx.x / nsl, sl = blockIdx.x % nsl;
+  int bh, sl;
+  slice_block(p.B * p.H, nsl, bh, sl);   // a head's slices on one XCD
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
   const int rb = lane / CPW, col = w * CPW + lane % CPW;   // slice-local column
   const int b = bh / p.H, h = bh % p.H;

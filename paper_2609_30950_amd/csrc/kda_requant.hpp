@@ -224,10 +224,14 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
       // waves whose rows all have width 2 take the three-operation form of
       // the same evaluation (ternary_threshold)
       const bool ternary = __all(b == 2);
-      float ph = phi[b][N_FIT - 1];
+      // factors read through one running pointer: the read after the last
+      // candidate (m = 0) lands on the previous width's last factor (b >= 2
+      // here), in the table and unused
+      const float* pp = &phi[0][0] + b * N_FIT + N_FIT - 1;
+      float ph = *pp;
       for (int m = N_FIT - 1; m >= 0; --m) {
         const float d = f16_to_f32(f32_to_f16_sat_nonneg(mx * ph));
-        ph = phi[b][m > 0 ? m - 1 : 0];   // next candidate's factor, off the critical path
+        ph = *--pp;   // next candidate's factor, off the critical path
         const float emax = __builtin_fmaf(-nf, d, mx);
         if (emax >= 0.f && emax * emax > best) break;   // row-uniform decision
         ++evals;
@@ -306,10 +310,17 @@ __device__ __forceinline__ void fit_rows(LoadRow load_row, const uint8_t* bits, 
     const float d = f16_to_f32(dh);
     const float inv = recip_f16_value(d);
     if (writer) {
+      // c = clamp(rint(fl32(x inv)), -n, n) as M + c, M = 1.5 2^23: adding M
+      // to fl32(x inv) rounds it to an integer, ties to even, exactly as rint
+      // does while |x inv| < 2^22 (larger magnitudes clamp to the same code),
+      // and the low bits of M + c (a float in [2^23, 2^24)) are c in two's
+      // complement, which the truncating store keeps
+      constexpr float M = 12582912.0f;
+      const float lo = M - nf, hi = M + nf;
 #pragma unroll
       for (int j = 0; j < SEG; ++j) {
-        const float c = __builtin_amdgcn_fmed3f(__builtin_rintf(x[j] * inv), -nf, nf);
-        dst[(size_t)j * LD] = (CT)c;
+        const float c = __builtin_amdgcn_fmed3f(x[j] * inv + M, lo, hi);
+        dst[(size_t)j * LD] = (CT)__builtin_bit_cast(uint32_t, c);
       }
       if (sg == 0) scale_out[i] = dh;
     }
@@ -587,6 +598,10 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
       const int sh = P & 31, bo = sm.rb.meta.w[i];
       const uint4 d = sm.rb.meta.desc[i];
       const float mul = __builtin_bit_cast(float, d.z), add = __builtin_bit_cast(float, d.w);
+      // x^ = fma(code, mul, add mul): the value of (code + add) mul for every
+      // code (exact: add mul is 0 or mu, code mul is 0 or -2 mu for one-bit
+      // rows), signed zeros aside, which no code or scale below depends on
+      const float addm = add * mul;
       const float ai = hv[DV + i], gi = hv[DV + DK + i];
       const uint32_t* cw = stg + (size_t)(sg * SEG) * str + (P >> 5);
 #pragma unroll
@@ -594,7 +609,7 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
         const uint32_t lo = cw[j * str], hi = cw[j * str + 1];
         const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
         const int code = __builtin_amdgcn_sbfe((int)f, 0, bo);   // signed field
-        const float xh = ((float)code + add) * mul;
+        const float xh = __builtin_fmaf((float)code, mul, addm);
         x[j] = __builtin_fmaf(gi, sm.rb.wv[sg * SEG + j], ai * xh);
       }
     };

@@ -645,6 +645,4 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
 template <bool C8>
 using CodeTile = typename std::conditional<C8, int8_t, int16_t>::type;
 
-
-// Block (head, part) = blockIdx.x / PARTS, blockIdx.x % PARTS.
 }  // namespace kda

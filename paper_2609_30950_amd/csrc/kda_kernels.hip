@@ -776,21 +776,38 @@ __global__ void __launch_bounds__(2 * DK) k_chunk_cols(KParams p) {
         }
       }
     }
-    for (int j = 0; j < nt; ++j) {
-      // rows 32 rb + lane % 16 and 32 rb + 16 + lane % 16: DPP broadcast sources
-      const float4 s0 = ps.rq[j][rb * ROW_BLOCK + (lane & 15)];
-      const float4 s1 = ps.rq[j][rb * ROW_BLOCK + 16 + (lane & 15)];
+    // rows 32 rb + lane % 16 and 32 rb + 16 + lane % 16: DPP broadcast sources.
+    // The batch's first token runs its first pass alone; every later token's
+    // first pass is fused with the previous token's second pass (fused_pass),
+    // and the batch's last token runs its second pass alone.
+    float4 s0 = ps.rq[0][rb * ROW_BLOCK + (lane & 15)];
+    float4 s1 = ps.rq[0][rb * ROW_BLOCK + 16 + (lane & 15)];
+    float accU = 0.f;
+    pass1_16<0, 0, 1>(X, accU, s0.x, s0.y);
+    pass1_16<16, 0, 1>(X, accU, s1.x, s1.y);
+    for (int j = 0; j + 1 < nt; ++j) {
       const float vj = ps.v[j][col];
-      float acc = 0.f;
-      pass1_16<0, 0, 1>(X, acc, s0.x, s0.y);
-      pass1_16<16, 0, 1>(X, acc, s1.x, s1.y);
-      const float u = rowblock_sum<NRB>(acc);
+      const float4 n0 = ps.rq[j + 1][rb * ROW_BLOCK + (lane & 15)];
+      const float4 n1 = ps.rq[j + 1][rb * ROW_BLOCK + 16 + (lane & 15)];
+      const float u = rowblock_sum<NRB>(accU);
       const float wv = erase ? vj - u : vj;   // no erasure: w = v
-      acc = 0.f;
-      pass2_16<0, 0, 1>(X, acc, s0.z, s0.w, wv);
-      pass2_16<16, 0, 1>(X, acc, s1.z, s1.w, wv);
-      const float o = rowblock_sum<NRB>(acc);
+      float accO = 0.f;
+      accU = 0.f;
+      fused_pass(X, accO, accU, s0.z, s0.w, n0.x, n0.y, s1.z, s1.w, n1.x, n1.y, wv);
+      s0 = n0;
+      s1 = n1;
+      const float o = rowblock_sum<NRB>(accO);
       if (rb == 0) ps.o[j][col] = o;
+    }
+    {
+      const float vj = ps.v[nt - 1][col];
+      const float u = rowblock_sum<NRB>(accU);
+      const float wv = erase ? vj - u : vj;
+      float accO = 0.f;
+      pass2_16<0, 0, 1>(X, accO, s0.z, s0.w, wv);
+      pass2_16<16, 0, 1>(X, accO, s1.z, s1.w, wv);
+      const float o = rowblock_sum<NRB>(accO);
+      if (rb == 0) ps.o[nt - 1][col] = o;
     }
     prev0 = j0;
     prevn = nt;

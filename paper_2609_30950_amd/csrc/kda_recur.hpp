@@ -87,6 +87,157 @@ __device__ __forceinline__ void pass2_16(float (&X)[ROW_BLOCK][CPL], float& acc,
       : "v"(G), "v"(Q), "v"(wv));
 }
 
+// Token j's second pass fused with token j + 1's first pass, over the 32 rows
+// of a lane's single column: per row r, X_r = fma(g_r, w, X_r),
+// accO = fma(q_r, X_r, accO), X_r = a'_r X_r, accU = fma(k'_r, X_r, accU),
+// i.e. the operations of pass2 (token j) and then pass1 (token j + 1) on
+// every element, each chain still in row order; the rows are skewed (step s
+// runs the first operation of row s, the next two of row s - 1 and the last
+// of row s - 2), so every operand was written four instructions earlier and
+// the two chains fill each other's latency.  Rows 0..15 take the sources
+// (G0, Q0, A0, K0) of the first 16-row DPP block, rows 16..31 (G1, ...) of
+// the second; the second asm block finishes rows 14 and 15.
+__device__ __forceinline__ void fused_pass(float (&X)[ROW_BLOCK][1], float& accO, float& accU, float G0,
+                                           float Q0, float A0, float K0, float G1, float Q1, float A1,
+                                           float K1, float wv) {
+  asm("s_nop 1\n"
+      "v_fmac_f32_dpp %0, %18, %22 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %1, %18, %22 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %0 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %0, %20, %0 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %2, %18, %22 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %1 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %1, %20, %1 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %0 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %3, %18, %22 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %2 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %2, %20, %2 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %1 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %4, %18, %22 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %3 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %3, %20, %3 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %2 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %5, %18, %22 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %4 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %4, %20, %4 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %3 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %6, %18, %22 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %5 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %5, %20, %5 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %4 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %7, %18, %22 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %6 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %6, %20, %6 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %5 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %8, %18, %22 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %7 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %7, %20, %7 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %6 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %9, %18, %22 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %8 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %8, %20, %8 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %7 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %10, %18, %22 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %9 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %9, %20, %9 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %8 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %11, %18, %22 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %10 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %10, %20, %10 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %9 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %12, %18, %22 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %11 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %11, %20, %11 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %10 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %13, %18, %22 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %12 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %12, %20, %12 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %11 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %14, %18, %22 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %13 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %13, %20, %13 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %12 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %15, %18, %22 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %19, %14 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %14, %20, %14 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %21, %13 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      : "+v"(X[0][0]), "+v"(X[1][0]), "+v"(X[2][0]), "+v"(X[3][0]), "+v"(X[4][0]), "+v"(X[5][0]), "+v"(X[6][0]), "+v"(X[7][0]), "+v"(X[8][0]), "+v"(X[9][0]), "+v"(X[10][0]), "+v"(X[11][0]), "+v"(X[12][0]), "+v"(X[13][0]), "+v"(X[14][0]), "+v"(X[15][0]),
+        "+v"(accO), "+v"(accU)
+      : "v"(G0), "v"(Q0), "v"(A0), "v"(K0), "v"(wv));
+  asm("s_nop 1\n"
+      "v_fmac_f32_dpp %2, %20, %27 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %24, %1 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %1, %25, %1 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %26, %0 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %3, %20, %27 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %2 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %2, %22, %2 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %26, %1 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %4, %20, %27 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %3 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %3, %22, %3 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %2 row_newbcast:0 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %5, %20, %27 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %4 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %4, %22, %4 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %3 row_newbcast:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %6, %20, %27 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %5 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %5, %22, %5 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %4 row_newbcast:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %7, %20, %27 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %6 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %6, %22, %6 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %5 row_newbcast:3 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %8, %20, %27 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %7 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %7, %22, %7 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %6 row_newbcast:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %9, %20, %27 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %8 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %8, %22, %8 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %7 row_newbcast:5 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %10, %20, %27 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %9 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %9, %22, %9 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %8 row_newbcast:6 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %11, %20, %27 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %10 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %10, %22, %10 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %9 row_newbcast:7 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %12, %20, %27 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %11 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %11, %22, %11 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %10 row_newbcast:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %13, %20, %27 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %12 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %12, %22, %12 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %11 row_newbcast:9 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %14, %20, %27 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %13 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %13, %22, %13 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %12 row_newbcast:10 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %15, %20, %27 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %14 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %14, %22, %14 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %13 row_newbcast:11 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %16, %20, %27 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %15 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %15, %22, %15 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %14 row_newbcast:12 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %17, %20, %27 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %16 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %16, %22, %16 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %15 row_newbcast:13 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %18, %21, %17 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_mul_f32_dpp %17, %22, %17 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %16 row_newbcast:14 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      "v_fmac_f32_dpp %19, %23, %17 row_newbcast:15 row_mask:0xf bank_mask:0xf bound_ctrl:1\n"
+      : "+v"(X[14][0]), "+v"(X[15][0]), "+v"(X[16][0]), "+v"(X[17][0]), "+v"(X[18][0]), "+v"(X[19][0]), "+v"(X[20][0]), "+v"(X[21][0]), "+v"(X[22][0]), "+v"(X[23][0]), "+v"(X[24][0]), "+v"(X[25][0]), "+v"(X[26][0]), "+v"(X[27][0]), "+v"(X[28][0]), "+v"(X[29][0]), "+v"(X[30][0]), "+v"(X[31][0]),
+        "+v"(accO), "+v"(accU)
+      : "v"(G1), "v"(Q1), "v"(A1), "v"(K1), "v"(Q0), "v"(A0), "v"(K0), "v"(wv));
+}
+
 template <int DK, int DV>
 struct RecSmem {
   float up[DK / ROW_BLOCK][DV];

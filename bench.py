@@ -590,7 +590,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{w.name} decode step B={w.B} H={w.H} d_k=d_v={w.dk}, mean "
+        "config": {"workload": ("" if w.name == "decode" else f"{w.name} ")
+                               + f"decode step B={w.B} H={w.H} d_k=d_v={w.dk}, mean "
                                f"{w.mean_bits} bits, widths [{w.b_min},{w.b_max}], groups of "
                                f"{w.G} rows, layer budget, "
                                f"{'per-head' if w.decay == 'head' else 'per-channel'} decay, "

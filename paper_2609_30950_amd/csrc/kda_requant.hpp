@@ -52,17 +52,18 @@ struct OrderSmem {
 };
 
 // perm[0 .. hi - lo) lists the rows lo .. hi - 1 by width, widest first
-// (ties in row order); os.P holds the bit offsets of all DK rows.
+// (ties in row order); os.P holds the bit offsets of all DK rows.  vmax: the
+// largest width any row may have (the counts above it are not formed).
 template <int DK>
 __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, OrderSmem<DK>& os,
-                                            int lo = 0, int hi = DK) {
+                                            int lo = 0, int hi = DK, int vmax = MAX_B) {
   const int t = threadIdx.x, w = t / WAVE, lane = lane_id();
   int b = 0, bp = 0, below = 0;
   if (t < DK) {
     b = bits[t];
     bp = t >= lo && t < hi ? b : 0;   // widths are at least 1: 0 marks rows outside the range
     const unsigned long long lt = (1ull << lane) - 1ull;
-    for (int v = 1; v <= MAX_B; ++v) {
+    for (int v = 1; v <= vmax; ++v) {
       const unsigned long long m = __ballot(bp == v);
       if (lane == 0) os.cnt[w][v] = __popcll(m);
       if (bp == v) below = __popcll(m & lt);
@@ -74,7 +75,7 @@ __device__ __forceinline__ void width_order(const uint8_t* bits, uint8_t* perm, 
   __syncthreads();
   if (bp > 0) {
     int pos = below;
-    for (int v = bp + 1; v <= MAX_B; ++v)
+    for (int v = bp + 1; v <= vmax; ++v)
       for (int q = 0; q < DK / WAVE; ++q) pos += os.cnt[q][v];
     for (int q = 0; q < w; ++q) pos += os.cnt[q][bp];
     perm[pos] = (uint8_t)t;
@@ -592,7 +593,7 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
     }
     for (int e = t; e < DV; e += blockDim.x) sm.rb.wv[e] = hv[e];
     __syncthreads();
-    width_order<DK>(sm.nb, sm.perm, sm.os);
+    width_order<DK>(sm.nb, sm.perm, sm.os, 0, DK, p.bmax);
     auto rebuild = [&](int i, int sg, float (&x)[SEG]) {
       const int P = sm.rb.meta.P[i];
       const int sh = P & 31, bo = sm.rb.meta.w[i];
@@ -616,7 +617,7 @@ __device__ __forceinline__ void requant_head(const KParams& p, int bh, RequantLd
     fit_rows<DK, DV, true>(rebuild, sm.nb, sm.perm, sm.phi, sm.Ct, sm.sc16, p.diag_fit);
   } else {
     __syncthreads();
-    width_order<DK>(sm.nb, sm.perm, sm.os, r0, r0 + ROWS);
+    width_order<DK>(sm.nb, sm.perm, sm.os, r0, r0 + ROWS, p.bmax);
     const float* S = p.ws_s32 + (size_t)bh * DK * DV;
     auto staged = [&](int i, int sg, float (&x)[SEG]) {
       const int li = min(max(i - r0, 0), ROWS - 1);

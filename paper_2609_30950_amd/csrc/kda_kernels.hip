@@ -73,8 +73,8 @@ __device__ __forceinline__ void unpack_cols(const uint32_t* words, const MetaSme
       const uint32_t hi = wr[DV + col];   // staged; masked off unless straddling
       const uint32_t f = __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
       const int code = __builtin_amdgcn_sbfe((int)f, 0, b);
-      // the row's width is wave-uniform: widths >= 2 (add = 0) skip the add
-      X[r][c] = b > 1 ? (float)code * mul : ((float)code + add) * mul;
+      // add is +0 for widths >= 2: code + 0 is code exactly (no select per row)
+      X[r][c] = ((float)code + add) * mul;
     }
     // finish row r before the reads of later rows are issued: the compiler
     // would otherwise keep every row's descriptor and words live at once
